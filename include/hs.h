@@ -1,0 +1,194 @@
+/*
+ * hs.h — C ABI of libhs, the MI355X (gfx950) language-decode engine for
+ * modality-disaggregated MLLM serving (arXiv 2603.12707).
+ *
+ * The boundary follows the paper's statement of the problem:
+ *   - the payload that crosses the modality boundary is the projected visual
+ *     embedding [1, N_v, d] (§5.1, §5.2 "Device Placement"), of N_v * d * b
+ *     bytes (embedding-size display, §4.1);
+ *   - the KV cache is allocated only when a request enters language prefill
+ *     (§5.4 "Lazy KV Cache Allocation") and holds 2 * L * n_kv * d_h * s_ctx * b
+ *     bytes per request (Eq. 1, §4.1), s_ctx = N_v + s_text (Theorem 1, §4.2);
+ *   - N_v varies per request (§4.2 "Handling dynamic visual token counts",
+ *     §5.2 "Aligned Batch Handoff");
+ *   - decode is the memory-bandwidth-bound phase that streams the weights and
+ *     the KV cache once per generated token (§2; Eq. 5, §4.3).
+ *
+ * Conventions
+ *   - Every call returns an int status: HS_OK (0) or a negative HS_E_* code;
+ *     hs_last_error() returns a thread-local message for the last failure.
+ *   - Device pointers are HIP device addresses on the device that was current
+ *     when the model was created; they stay owned by the caller.  The library
+ *     owns only what it allocates in hs_model_create / hs_kv_alloc
+ *     (workspaces and per-request metadata) and frees it in the matching
+ *     *_free call.
+ *   - Calls taking a stream are asynchronous on that stream (NULL = the
+ *     default stream).  hs_decode_step and hs_prefill_embeddings allocate no
+ *     device memory and perform no device-to-host copy.
+ *   - Argument, state and capacity checks run on host-side mirrors before any
+ *     launch; a failing call launches nothing and changes no state.
+ *
+ * Storage dtype codes: HS_F32 (IEEE binary32), HS_F16 (binary16),
+ * HS_BF16 (bfloat16).  Weights, vision rows, the KV cache and the
+ * intermediate activations named below are stored in the model dtype; the
+ * residual stream, logits and every accumulation are fp32; conversions to the
+ * storage dtype round to nearest, ties to even.
+ */
+#ifndef HS_H
+#define HS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HS_OK 0
+#define HS_E_INVALID (-1)  /* NULL/negative/shape/dtype mismatch, n_v > capacity */
+#define HS_E_CAPACITY (-2) /* a step would write position >= capacity */
+#define HS_E_BUFFER (-3)   /* caller's KV buffer smaller than required */
+#define HS_E_STATE (-4)    /* decode before prefill, prefill twice, ... */
+#define HS_E_DEVICE (-5)   /* HIP runtime error (message in hs_last_error) */
+
+#define HS_F32 0
+#define HS_F16 1
+#define HS_BF16 2
+
+#define HS_ROPE_1D 0 /* rotate-half RoPE at the row's sequence position */
+#define HS_ROPE_M3 1 /* 3-section multimodal RoPE driven by (t, h, w) ids */
+
+typedef void *hs_stream_t; /* a hipStream_t */
+
+/* Decoder shape.  d_model = any; head_dim even, head_dim / 2 a multiple of 16;
+ * n_heads a multiple of n_kv_heads (query head i reads KV head
+ * i / (n_heads / n_kv_heads)); d_model, n_heads * head_dim and ffn_dim
+ * multiples of 8 (16-bit dtypes) or 4 (fp32).  For HS_ROPE_M3 the three
+ * section sizes count frequency pairs and sum to head_dim / 2.  rope_theta and
+ * rms_eps are used exactly as these fp32 values. */
+typedef struct hs_config {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rope_theta, rms_eps;
+  int32_t rope_kind;
+  int32_t mrope_section[3];
+  int32_t qkv_bias;
+  int32_t dtype;
+} hs_config;
+
+/* One decoder layer's weights, device pointers, row-major [out, in]
+ * (nn.Linear layout), all in the model dtype:
+ *   attn_norm, mlp_norm      [d]
+ *   wq [n_h*d_h, d]   wk, wv [n_kv*d_h, d]   (bq, bk, bv: [rows] or NULL)
+ *   wo [d, n_h*d_h]   w_gate, w_up [F, d]    w_down [d, F]
+ * Row-major with no padding; every row starts 16-byte aligned. */
+typedef struct hs_layer_weights {
+  const void *attn_norm;
+  const void *wq, *wk, *wv;
+  const void *bq, *bk, *bv;
+  const void *wo;
+  const void *mlp_norm;
+  const void *w_gate, *w_up;
+  const void *w_down;
+} hs_layer_weights;
+
+/* embed [V, d]; final_norm [d]; lm_head [V, d].  lm_head == NULL declares a
+ * layer stack without a head: decode then produces no tokens or logits. */
+typedef struct hs_weights {
+  const void *embed;
+  const void *final_norm;
+  const void *lm_head;
+  const hs_layer_weights *layers; /* host array [n_layers] */
+} hs_weights;
+
+typedef struct hs_model hs_model;
+typedef struct hs_kv hs_kv;
+
+/* Thread-local description of the last failing call ("" if none). */
+const char *hs_last_error(void);
+
+/* KV-cache and embedding transfer sizes of one request (Eq. 1 and the
+ * embedding-size display, §4.1):
+ *   kv_bytes  = 2 * n_layers * n_kv_heads * head_dim * (n_v + s_text) * b
+ *   emb_bytes = n_v * d_model * b
+ * with b the dtype width; exact integers, no padding.  With
+ * s_text = capacity - n_v it is also the size hs_kv_alloc lays out for one
+ * request.  Pure host arithmetic; either output pointer may be NULL. */
+int hs_kv_bytes(const hs_config *cfg, int64_t n_v, int64_t s_text, uint64_t *kv_bytes, uint64_t *emb_bytes);
+
+/* Validates cfg, records the caller-owned weight pointers (they must outlive
+ * the model) and allocates the workspaces for decode batches of up to
+ * max_batch requests and requests of up to max_ctx positions (prefill rows,
+ * capacities and RoPE position ids are all < max_ctx).  Uses the current
+ * HIP device. */
+int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch, int32_t max_ctx, hs_model **out);
+int hs_model_free(hs_model *m);
+
+/* Lays out `batch` requests back to back, in order and without padding, in
+ * the caller-owned device buffer dev_buf, which must hold at least
+ * sum_b kv_bytes(capacity_b) bytes.  Request b occupies capacity[b]
+ * positions; its KV element (layer l, K|V = s, kv head j, position p,
+ * channel e) sits at element offset
+ *   base_b + (((l * 2 + s) * n_kv + j) * capacity_b + p) * head_dim + e,
+ *   base_b = sum_{b' < b} 2 * n_layers * n_kv * head_dim * capacity_b',
+ * so that each (request, layer, K|V, head) is one contiguous
+ * [capacity_b, head_dim] slab streamed row by row.  n_v[b] (host) is the
+ * request's vision-row count, checked again at prefill; capacity[b] (host)
+ * must satisfy 0 <= n_v[b] <= capacity[b] <= max_ctx.  All lengths start at 0.
+ * The handle owns small device metadata arrays; dev_buf stays the caller's. */
+int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *capacity, void *dev_buf,
+                uint64_t buf_bytes, hs_kv **out);
+int hs_kv_free(hs_kv *kv);
+
+/* Language prefill of request `req` from its projected visual embedding:
+ * rows 0..n_v-1 are emb [n_v, d] (device, model dtype), rows n_v..n_v+s_text-1
+ * are the embeddings of text_ids [s_text] (device int32, 0 <= id < vocab).
+ * RoPE: HS_ROPE_1D uses position r for row r and pos_thw must be NULL;
+ * HS_ROPE_M3 needs pos_thw (device int32 [3][n_v + s_text], the (t, h, w) ids
+ * of every row, each < max_ctx) and the next decode position becomes
+ * max(pos_thw) + 1.  Fills KV positions [0, s_ctx), sets the request length to
+ * s_ctx, writes the first generated token to first_token (device int32[1])
+ * and, if last_logits is not NULL, the fp32 logits of the last row
+ * (device [vocab]).  Requires the model to have an LM head and the request to
+ * be empty (HS_E_STATE otherwise). */
+int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, const int32_t *text_ids,
+                          int32_t s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_token,
+                          hs_stream_t stream);
+
+/* One greedy decode step for every request of the handle: request b embeds
+ * tokens_in[b] (device int32 [batch]), writes its K/V rows at position len_b,
+ * attends over positions [0, len_b], and (with an LM head) writes the argmax
+ * of its logits, lowest index on ties, to tokens_out[b] (device int32
+ * [batch]; may not alias tokens_in).  The lengths advance on the device, so
+ * repeated calls need no host input.  logits (device fp32 [batch, vocab]) and
+ * hidden_out (device fp32 [batch, d], the residual stream after the last
+ * layer) are optional outputs.  Errors: HS_E_STATE if a request is not
+ * prefilled, HS_E_CAPACITY if len_b == capacity_b for some b.  Token ids
+ * outside [0, vocab) are replaced by 0 and flagged (hs_model_status). */
+int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
+                   float *hidden_out, hs_stream_t stream);
+
+/* Reads and clears the device-side input flags (bit 0: an out-of-range token
+ * id was replaced by 0).  Synchronises the device. */
+int hs_model_status(hs_model *m, int32_t *flags);
+
+/* ---- test and fill hooks (synchronous) ---- */
+
+/* Host copy of every request's current length (int32 [batch]). */
+int hs_kv_lengths(const hs_kv *kv, int32_t *host_len);
+
+/* Copies n rows of head_dim elements (model dtype) into / out of the cache at
+ * (req, layer, kv_sel 0 = K / 1 = V, head, positions pos0..pos0+n-1);
+ * src_is_device selects whether src/dst is a device or a host pointer. */
+int hs_kv_write(hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
+                const void *src, int32_t src_is_device);
+int hs_kv_read(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
+               void *dst, int32_t dst_is_device);
+
+/* Marks request req as holding `len` valid positions (filled through
+ * hs_kv_write) with next RoPE position rope_pos, as a prefill would. */
+int hs_kv_set_length(hs_kv *kv, int32_t req, int32_t len, int32_t rope_pos);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,529 @@
+// hs_api.cpp — the C ABI of libhs (include/hs.h): argument/state checks on
+// host mirrors, workspace ownership, and the per-step launch sequence.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "hs_internal.h"
+
+using namespace hs;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                      \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail(HS_E_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+int dtype_bytes(int dt) { return dt == HS_F32 ? 4 : 2; }
+
+// Light checks needed by the size formula alone.
+bool shape_ok(const hs_config *c) {
+  return c && c->n_layers > 0 && c->n_kv_heads > 0 && c->head_dim > 0 && c->d_model > 0 && c->dtype >= HS_F32 &&
+         c->dtype <= HS_BF16;
+}
+
+int check_config(const hs_config *c) {
+  if (!shape_ok(c)) return fail(HS_E_INVALID, "config: non-positive size or unknown dtype");
+  if (c->n_heads <= 0 || c->ffn_dim <= 0 || c->vocab <= 0)
+    return fail(HS_E_INVALID, "config: non-positive n_heads/ffn_dim/vocab");
+  if (c->n_heads % c->n_kv_heads) return fail(HS_E_INVALID, "config: n_heads %% n_kv_heads != 0");
+  if (c->head_dim % 32) return fail(HS_E_INVALID, "config: head_dim / 2 must be a multiple of 16");
+  const int group = c->n_heads / c->n_kv_heads;
+  if (!attn_supported(c->dtype, c->head_dim, group))
+    return fail(HS_E_INVALID, "config: head_dim %d with %d query heads per KV head is not supported", c->head_dim,
+                group);
+  const int ce = 16 / dtype_bytes(c->dtype);
+  if (c->d_model % ce || (c->n_heads * c->head_dim) % ce || c->ffn_dim % ce)
+    return fail(HS_E_INVALID, "config: d_model, n_heads*head_dim and ffn_dim must be multiples of %d", ce);
+  if (c->rope_kind != HS_ROPE_1D && c->rope_kind != HS_ROPE_M3) return fail(HS_E_INVALID, "config: rope_kind");
+  if (c->rope_kind == HS_ROPE_M3) {
+    const int *s = c->mrope_section;
+    if (s[0] < 0 || s[1] < 0 || s[2] < 0 || s[0] + s[1] + s[2] != c->head_dim / 2)
+      return fail(HS_E_INVALID, "config: M-RoPE sections must sum to head_dim / 2");
+  }
+  if (!(c->rope_theta > 0.f) || !(c->rms_eps >= 0.f)) return fail(HS_E_INVALID, "config: rope_theta/rms_eps");
+  if (c->qkv_bias != 0 && c->qkv_bias != 1) return fail(HS_E_INVALID, "config: qkv_bias");
+  return HS_OK;
+}
+
+// Positions per attention split: the smallest power of two >= s_min that
+// keeps (queries x KV heads x splits) within a few thousand work groups.
+void split_policy(int nq, int n_kv, int max_len, int s_min, int *S, int *n_split) {
+  int s = s_min;
+  while (s < ATTN_SMAX && (int64_t)nq * n_kv * ((max_len + s - 1) / s) > 8192) s *= 2;
+  *S = s;
+  *n_split = std::max(1, (max_len + s - 1) / s);
+}
+constexpr int PREFILL_SMIN = 256;
+
+int64_t kv_request_elems(const hs_config &c, int cap) {
+  return 2ll * c.n_layers * c.n_kv_heads * (int64_t)c.head_dim * cap;
+}
+
+void free_model(hs_model *m) {
+  if (!m) return;
+  void *ptrs[] = {m->x, m->q, m->attn, m->act, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  delete m;
+}
+
+// Runs every decoder layer over ncols activation rows held in m->x.
+int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *rope_pos, int S, int n_split,
+               hipStream_t st) {
+  const hs_config &c = m->cfg;
+  const int d = c.d_model, hd = c.head_dim, nh = c.n_heads, nkv = c.n_kv_heads, F = c.ffn_dim;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const hs_layer_weights &W = m->layers[l];
+    GemmArgs g{};
+    g.w[0] = W.wq;
+    g.w[1] = W.wk;
+    g.w[2] = W.wv;
+    if (c.qkv_bias) {
+      g.bias[0] = W.bq;
+      g.bias[1] = W.bk;
+      g.bias[2] = W.bv;
+    }
+    g.rows[0] = nh * hd;
+    g.rows[1] = g.rows[2] = nkv * hd;
+    g.K = d;
+    g.ncols = ncols;
+    g.x = m->x;
+    g.gain = W.attn_norm;
+    g.eps = c.rms_eps;
+    g.out = m->q;
+    g.ld_out = nh * hd;
+    g.head_dim = hd;
+    g.n_heads = nh;
+    g.n_kv = nkv;
+    g.kv = kv->buf;
+    g.kv_base = kv->d_base;
+    g.kv_cap = kv->d_cap;
+    g.kv_len = kv->d_len;
+    g.layer = l;
+    g.prefill_req = prefill_req;
+    g.rope_pos = rope_pos;
+    g.rope_m3 = c.rope_kind == HS_ROPE_M3;
+    g.sec0 = c.mrope_section[0];
+    g.sec1 = c.mrope_section[0] + c.mrope_section[1];
+    g.rope_tab = m->rope_tab;
+    g.rope_max = m->max_ctx;
+    g.status = m->status;
+    HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, (nh + 2 * nkv) * hd / 32, st));
+
+    AttnArgs a{};
+    a.q = m->q;
+    a.ld_q = nh * hd;
+    a.kv = kv->buf;
+    a.kv_base = kv->d_base;
+    a.kv_cap = kv->d_cap;
+    a.kv_len = kv->d_len;
+    a.layer = l;
+    a.n_heads = nh;
+    a.n_kv = nkv;
+    a.prefill_req = prefill_req;
+    a.S = S;
+    a.n_split = n_split;
+    a.part_o = m->part_o;
+    a.part_ml = m->part_ml;
+    a.scale = (float)(1.0 / std::sqrt((double)hd));
+    a.out = m->attn;
+    HIP_TRY(launch_attention(c.dtype, hd, nh / nkv, ncols, a, st));
+    HIP_TRY(launch_combine(c.dtype, hd, ncols, a, st));
+
+    GemmArgs o{};
+    o.w[0] = W.wo;
+    o.rows[0] = d;
+    o.K = nh * hd;
+    o.ncols = ncols;
+    o.x = m->attn;
+    o.resid = m->x;
+    o.ld_resid = d;
+    HIP_TRY(launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, (d + 15) / 16, st));
+
+    GemmArgs u{};
+    u.w[0] = W.w_gate;
+    u.w[1] = W.w_up;
+    u.rows[0] = u.rows[1] = F;
+    u.K = d;
+    u.ncols = ncols;
+    u.x = m->x;
+    u.gain = W.mlp_norm;
+    u.eps = c.rms_eps;
+    u.out = m->act;
+    u.ld_out = F;
+    HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, (F + 15) / 16, st));
+
+    GemmArgs dn{};
+    dn.w[0] = W.w_down;
+    dn.rows[0] = d;
+    dn.K = F;
+    dn.ncols = ncols;
+    dn.x = m->act;
+    dn.resid = m->x;
+    dn.ld_resid = d;
+    HIP_TRY(launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, (d + 15) / 16, st));
+  }
+  return HS_OK;
+}
+
+// Final RMSNorm + LM head over ncols rows starting at x_rows -> logits.
+int run_head(hs_model *m, const float *x_rows, int ncols, float *logits, hipStream_t st) {
+  const hs_config &c = m->cfg;
+  GemmArgs g{};
+  g.w[0] = m->w.lm_head;
+  g.rows[0] = c.vocab;
+  g.K = c.d_model;
+  g.ncols = ncols;
+  g.x = x_rows;
+  g.gain = m->w.final_norm;
+  g.eps = c.rms_eps;
+  g.out = logits;
+  g.ld_out = c.vocab;
+  HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, (c.vocab + 31) / 32, st));
+  return HS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hs_last_error(void) { return g_err.c_str(); }
+
+int hs_kv_bytes(const hs_config *cfg, int64_t n_v, int64_t s_text, uint64_t *kv_bytes, uint64_t *emb_bytes) {
+  if (!shape_ok(cfg)) return fail(HS_E_INVALID, "hs_kv_bytes: bad config");
+  if (n_v < 0 || s_text < 0) return fail(HS_E_INVALID, "hs_kv_bytes: negative length");
+  const uint64_t factors[] = {2, (uint64_t)cfg->n_layers, (uint64_t)cfg->n_kv_heads, (uint64_t)cfg->head_dim,
+                              (uint64_t)n_v + (uint64_t)s_text, (uint64_t)dtype_bytes(cfg->dtype)};
+  uint64_t kv = 1, emb = 0;
+  for (uint64_t f : factors)
+    if (__builtin_mul_overflow(kv, f, &kv)) return fail(HS_E_INVALID, "hs_kv_bytes: size overflows 64 bits");
+  if (__builtin_mul_overflow((uint64_t)n_v, (uint64_t)cfg->d_model, &emb) ||
+      __builtin_mul_overflow(emb, (uint64_t)dtype_bytes(cfg->dtype), &emb))
+    return fail(HS_E_INVALID, "hs_kv_bytes: size overflows 64 bits");
+  if (kv_bytes) *kv_bytes = kv;
+  if (emb_bytes) *emb_bytes = emb;
+  return HS_OK;
+}
+
+int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch, int32_t max_ctx, hs_model **out) {
+  if (!out) return fail(HS_E_INVALID, "hs_model_create: out is NULL");
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!w || !w->embed || !w->layers) return fail(HS_E_INVALID, "hs_model_create: missing embed/layers");
+  if (w->lm_head && !w->final_norm) return fail(HS_E_INVALID, "hs_model_create: lm_head without final_norm");
+  if (max_batch <= 0 || max_ctx <= 0) return fail(HS_E_INVALID, "hs_model_create: max_batch/max_ctx must be > 0");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const hs_layer_weights &L = w->layers[l];
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.w_gate || !L.w_up || !L.w_down)
+      return fail(HS_E_INVALID, "hs_model_create: layer %d has a NULL weight", l);
+    if (cfg->qkv_bias && (!L.bq || !L.bk || !L.bv))
+      return fail(HS_E_INVALID, "hs_model_create: layer %d lacks q/k/v bias", l);
+  }
+  hs_model *m = new (std::nothrow) hs_model();
+  if (!m) return fail(HS_E_DEVICE, "hs_model_create: out of host memory");
+  m->cfg = *cfg;
+  m->w = *w;
+  m->layers.assign(w->layers, w->layers + cfg->n_layers);
+  m->w.layers = m->layers.data();
+  m->max_batch = max_batch;
+  m->max_ctx = max_ctx;
+  if (hipGetDevice(&m->device) != hipSuccess) {
+    free_model(m);
+    return fail(HS_E_DEVICE, "hs_model_create: no HIP device");
+  }
+  const hs_config &c = *cfg;
+  const int b = dtype_bytes(c.dtype), hd = c.head_dim, nh = c.n_heads;
+  const int64_t rows = std::max(max_batch, max_ctx);
+
+  // attention partial capacity: the largest (queries x heads x splits) any
+  // decode batch <= max_batch with capacities <= max_ctx, or any prefill of
+  // <= max_ctx rows, can ask for
+  int64_t entries = 0;
+  for (int nq = 1; nq <= max_batch; ++nq) {
+    int S, ns, prev_ns = -1, prev_S = -1;
+    for (int len = 1; len <= max_ctx; ++len) {
+      split_policy(nq, c.n_kv_heads, len, ATTN_SMIN, &S, &ns);
+      if (ns == prev_ns && S == prev_S) continue;
+      prev_ns = ns;
+      prev_S = S;
+      entries = std::max(entries, (int64_t)nq * nh * ns);
+    }
+  }
+  for (int r = 1; r <= max_ctx; ++r) {
+    int S, ns;
+    split_policy(r, c.n_kv_heads, r, PREFILL_SMIN, &S, &ns);
+    entries = std::max(entries, (int64_t)r * nh * ns);
+  }
+  m->part_entries = entries;
+
+  struct Alloc {
+    void **p;
+    size_t bytes;
+  } allocs[] = {
+      {(void **)&m->x, (size_t)rows * c.d_model * 4},
+      {&m->q, (size_t)rows * nh * hd * b},
+      {&m->attn, (size_t)rows * nh * hd * b},
+      {&m->act, (size_t)rows * c.ffn_dim * b},
+      {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
+      {(void **)&m->part_o, (size_t)entries * hd * 4},
+      {(void **)&m->part_ml, (size_t)entries * 2 * 4},
+      {(void **)&m->rope_tab, (size_t)max_ctx * (hd / 2) * 2 * 4},
+      {(void **)&m->status, 4},
+  };
+  for (auto &a : allocs) {
+    if (!a.bytes) continue;
+    if (hipMalloc(a.p, a.bytes) != hipSuccess) {
+      free_model(m);
+      return fail(HS_E_DEVICE, "hs_model_create: hipMalloc of %zu bytes failed", a.bytes);
+    }
+  }
+  // RoPE table: pair i at position p turns by p * theta^(-2i/d_h); angle and
+  // cos/sin in fp64, stored as fp32
+  std::vector<float> tab((size_t)max_ctx * (hd / 2) * 2);
+  for (int p = 0; p < max_ctx; ++p)
+    for (int i = 0; i < hd / 2; ++i) {
+      const double inv = std::pow((double)c.rope_theta, -(double)(2 * i) / (double)hd);
+      const double ang = (double)p * inv;
+      tab[((size_t)p * (hd / 2) + i) * 2] = (float)std::cos(ang);
+      tab[((size_t)p * (hd / 2) + i) * 2 + 1] = (float)std::sin(ang);
+    }
+  if (hipMemcpy(m->rope_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemset(m->status, 0, 4) != hipSuccess) {
+    free_model(m);
+    return fail(HS_E_DEVICE, "hs_model_create: initial copies failed");
+  }
+  *out = m;
+  return HS_OK;
+}
+
+int hs_model_free(hs_model *m) {
+  if (!m) return fail(HS_E_INVALID, "hs_model_free: NULL");
+  free_model(m);
+  return HS_OK;
+}
+
+int hs_model_status(hs_model *m, int32_t *flags) {
+  if (!m || !flags) return fail(HS_E_INVALID, "hs_model_status: NULL argument");
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(flags, m->status, 4, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemset(m->status, 0, 4));
+  return HS_OK;
+}
+
+int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *capacity, void *dev_buf,
+                uint64_t buf_bytes, hs_kv **out) {
+  if (!out) return fail(HS_E_INVALID, "hs_kv_alloc: out is NULL");
+  *out = nullptr;
+  if (!m || !n_v || !capacity || !dev_buf) return fail(HS_E_INVALID, "hs_kv_alloc: NULL argument");
+  if (batch <= 0) return fail(HS_E_INVALID, "hs_kv_alloc: batch must be > 0");
+  const hs_config &c = m->cfg;
+  const int b = dtype_bytes(c.dtype);
+  uint64_t total = 0;
+  for (int i = 0; i < batch; ++i) {
+    if (n_v[i] < 0 || capacity[i] <= 0 || n_v[i] > capacity[i] || capacity[i] > m->max_ctx)
+      return fail(HS_E_INVALID, "hs_kv_alloc: request %d has n_v %d, capacity %d (max_ctx %d)", i, n_v[i],
+                  capacity[i], m->max_ctx);
+    total += (uint64_t)kv_request_elems(c, capacity[i]) * b;
+  }
+  if (buf_bytes < total)
+    return fail(HS_E_BUFFER, "hs_kv_alloc: buffer holds %llu bytes, layout needs %llu",
+                (unsigned long long)buf_bytes, (unsigned long long)total);
+  if (((uintptr_t)dev_buf) % 16) return fail(HS_E_INVALID, "hs_kv_alloc: buffer must be 16-byte aligned");
+  hs_kv *kv = new (std::nothrow) hs_kv();
+  if (!kv) return fail(HS_E_DEVICE, "hs_kv_alloc: out of host memory");
+  kv->m = m;
+  kv->batch = batch;
+  kv->buf = dev_buf;
+  kv->buf_bytes = buf_bytes;
+  kv->n_v.assign(n_v, n_v + batch);
+  kv->cap.assign(capacity, capacity + batch);
+  kv->len.assign(batch, 0);
+  kv->rope.assign(batch, 0);
+  kv->ready.assign(batch, 0);
+  kv->base.resize(batch);
+  int64_t off = 0;
+  for (int i = 0; i < batch; ++i) {
+    kv->base[i] = off;
+    off += kv_request_elems(c, capacity[i]);
+    kv->max_cap = std::max(kv->max_cap, capacity[i]);
+  }
+  bool ok = hipMalloc(&kv->d_base, batch * 8) == hipSuccess && hipMalloc(&kv->d_cap, batch * 4) == hipSuccess &&
+            hipMalloc(&kv->d_len, batch * 4) == hipSuccess && hipMalloc(&kv->d_rope, batch * 4) == hipSuccess;
+  ok = ok && hipMemcpy(kv->d_base, kv->base.data(), batch * 8, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_cap, kv->cap.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemset(kv->d_len, 0, batch * 4) == hipSuccess && hipMemset(kv->d_rope, 0, batch * 4) == hipSuccess;
+  if (!ok) {
+    hs_kv_free(kv);
+    return fail(HS_E_DEVICE, "hs_kv_alloc: metadata allocation failed");
+  }
+  *out = kv;
+  return HS_OK;
+}
+
+int hs_kv_free(hs_kv *kv) {
+  if (!kv) return fail(HS_E_INVALID, "hs_kv_free: NULL");
+  void *ptrs[] = {kv->d_base, kv->d_cap, kv->d_len, kv->d_rope};
+  for (void *p : ptrs)
+    if (p) (void)hipFree(p);
+  delete kv;
+  return HS_OK;
+}
+
+int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, const int32_t *text_ids,
+                          int32_t s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_token,
+                          hs_stream_t stream) {
+  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_prefill_embeddings: model/handle mismatch");
+  if (req < 0 || req >= kv->batch) return fail(HS_E_INVALID, "hs_prefill_embeddings: request %d out of range", req);
+  if (!m->w.lm_head) return fail(HS_E_STATE, "hs_prefill_embeddings: model has no LM head");
+  if (!first_token) return fail(HS_E_INVALID, "hs_prefill_embeddings: first_token is NULL");
+  if (s_text < 0) return fail(HS_E_INVALID, "hs_prefill_embeddings: negative s_text");
+  const hs_config &c = m->cfg;
+  const int n_v = kv->n_v[req], s_ctx = n_v + s_text;
+  if (s_ctx <= 0) return fail(HS_E_INVALID, "hs_prefill_embeddings: empty context");
+  if ((n_v > 0 && !emb) || (s_text > 0 && !text_ids))
+    return fail(HS_E_INVALID, "hs_prefill_embeddings: missing embedding rows or text ids");
+  if (c.rope_kind == HS_ROPE_M3 && !pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: M-RoPE needs pos_thw");
+  if (c.rope_kind == HS_ROPE_1D && pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: 1-D RoPE takes no pos_thw");
+  if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "hs_prefill_embeddings: request %d is not empty", req);
+  if (s_ctx > kv->cap[req])
+    return fail(HS_E_CAPACITY, "hs_prefill_embeddings: context %d exceeds capacity %d", s_ctx, kv->cap[req]);
+  int S, ns;
+  split_policy(s_ctx, c.n_kv_heads, s_ctx, PREFILL_SMIN, &S, &ns);
+  if ((int64_t)s_ctx * c.n_heads * ns > m->part_entries)
+    return fail(HS_E_INVALID, "hs_prefill_embeddings: attention workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
+  int rc = run_layers(m, kv, s_ctx, req, pos_thw, S, ns, st);
+  if (rc) return rc;
+  float *lg = last_logits ? last_logits : m->logits;
+  rc = run_head(m, m->x + (int64_t)(s_ctx - 1) * c.d_model, 1, lg, st);
+  if (rc) return rc;
+  HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, 1, first_token, nullptr, nullptr, 0, st));
+  HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, req, s_ctx, pos_thw, st));
+  kv->len[req] = s_ctx;
+  kv->ready[req] = 1;
+  return HS_OK;
+}
+
+int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
+                   float *hidden_out, hs_stream_t stream) {
+  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_decode_step: model/handle mismatch");
+  if (!tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_in is NULL");
+  const hs_config &c = m->cfg;
+  const int B = kv->batch;
+  if (B > m->max_batch) return fail(HS_E_INVALID, "hs_decode_step: batch %d exceeds max_batch %d", B, m->max_batch);
+  if (m->w.lm_head) {
+    if (!tokens_out) return fail(HS_E_INVALID, "hs_decode_step: tokens_out is NULL");
+    if (tokens_out == tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_out aliases tokens_in");
+  } else if (logits) {
+    return fail(HS_E_INVALID, "hs_decode_step: model has no LM head, logits must be NULL");
+  }
+  for (int b = 0; b < B; ++b) {
+    if (!kv->ready[b]) return fail(HS_E_STATE, "hs_decode_step: request %d is not prefilled", b);
+    if (kv->len[b] >= kv->cap[b])
+      return fail(HS_E_CAPACITY, "hs_decode_step: request %d is full (%d positions)", b, kv->cap[b]);
+  }
+  int S, ns;
+  split_policy(B, c.n_kv_heads, kv->max_cap, ATTN_SMIN, &S, &ns);
+  if ((int64_t)B * c.n_heads * ns > m->part_entries)
+    return fail(HS_E_INVALID, "hs_decode_step: attention workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st));
+  int rc = run_layers(m, kv, B, -1, kv->d_rope, S, ns, st);
+  if (rc) return rc;
+  if (hidden_out)
+    HIP_TRY(hipMemcpyAsync(hidden_out, m->x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
+  if (m->w.lm_head) {
+    float *lg = logits ? logits : m->logits;
+    rc = run_head(m, m->x, B, lg, st);
+    if (rc) return rc;
+    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st));
+  } else {
+    HIP_TRY(launch_advance(kv->d_len, kv->d_rope, B, st));
+  }
+  for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  return HS_OK;
+}
+
+int hs_kv_lengths(const hs_kv *kv, int32_t *host_len) {
+  if (!kv || !host_len) return fail(HS_E_INVALID, "hs_kv_lengths: NULL argument");
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(host_len, kv->d_len, kv->batch * 4, hipMemcpyDeviceToHost));
+  return HS_OK;
+}
+
+static int kv_slab(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0,
+                   int32_t n, const void *p, int64_t *off_bytes, size_t *bytes) {
+  if (!kv || !p) return fail(HS_E_INVALID, "kv copy: NULL argument");
+  const hs_config &c = kv->m->cfg;
+  if (req < 0 || req >= kv->batch || layer < 0 || layer >= c.n_layers || kv_sel < 0 || kv_sel > 1 || head < 0 ||
+      head >= c.n_kv_heads || pos0 < 0 || n < 0 || pos0 + (int64_t)n > kv->cap[req])
+    return fail(HS_E_INVALID, "kv copy: (req %d, layer %d, kv %d, head %d, pos %d + %d) outside the cache", req, layer,
+                kv_sel, head, pos0, n);
+  const int b = dtype_bytes(c.dtype);
+  const int64_t elem =
+      kv->base[req] + ((int64_t)((layer * 2 + kv_sel) * c.n_kv_heads + head) * kv->cap[req] + pos0) * c.head_dim;
+  *off_bytes = elem * b;
+  *bytes = (size_t)n * c.head_dim * b;
+  return HS_OK;
+}
+
+int hs_kv_write(hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
+                const void *src, int32_t src_is_device) {
+  int64_t off;
+  size_t bytes;
+  int rc = kv_slab(kv, req, layer, kv_sel, head, pos0, n, src, &off, &bytes);
+  if (rc) return rc;
+  if (!bytes) return HS_OK;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy((char *)kv->buf + off, src, bytes, src_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice));
+  HIP_TRY(hipDeviceSynchronize());
+  return HS_OK;
+}
+
+int hs_kv_read(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
+               void *dst, int32_t dst_is_device) {
+  int64_t off;
+  size_t bytes;
+  int rc = kv_slab(kv, req, layer, kv_sel, head, pos0, n, dst, &off, &bytes);
+  if (rc) return rc;
+  if (!bytes) return HS_OK;
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(dst, (const char *)kv->buf + off, bytes,
+                    dst_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost));
+  return HS_OK;
+}
+
+int hs_kv_set_length(hs_kv *kv, int32_t req, int32_t len, int32_t rope_pos) {
+  if (!kv) return fail(HS_E_INVALID, "hs_kv_set_length: NULL");
+  if (req < 0 || req >= kv->batch || len < 0 || len > kv->cap[req] || rope_pos < 0)
+    return fail(HS_E_INVALID, "hs_kv_set_length: bad request/length");
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(kv->d_len + req, &len, 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(kv->d_rope + req, &rope_pos, 4, hipMemcpyHostToDevice));
+  kv->len[req] = len;
+  kv->rope[req] = rope_pos;
+  kv->ready[req] = len > 0;
+  return HS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// hs_internal.h — private structures of libhs shared by the host API and the
+// kernel launchers.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "hs.h"
+
+namespace hs {
+
+// Arguments of the weight-streaming GEMM  Y[c][n] = sum_k X[c][k] * W[n][k].
+// Columns c are activation rows (decode requests or prefill rows); rows n are
+// output features.  Row tiles of 16 are enumerated over up to three matrices.
+struct GemmArgs {
+  const void *w[3];
+  const void *bias[3];
+  int rows[3];
+  int K;
+  int ncols;
+  // prologue: plain activations (model dtype [ncols][K]) or the fp32 residual
+  // stream [ncols][K] normalised on the fly with gain[K] and eps
+  const void *x;
+  const void *gain;
+  float eps;
+  // epilogue outputs
+  void *out;    // logits fp32 / SwiGLU output / q after RoPE, row stride ld_out
+  int ld_out;
+  float *resid; // residual stream fp32 [ncols][ld_resid], updated in place
+  int ld_resid;
+  // q/k/v epilogue: RoPE and KV append
+  int head_dim, n_heads, n_kv;
+  void *kv;
+  const int64_t *kv_base;
+  const int *kv_cap;
+  const int *kv_len;
+  int layer;
+  int prefill_req;     // < 0: decode (column = request, position = len); else prefill row = position
+  const int *rope_pos; // decode: [ncols]; prefill M-RoPE: [3][ncols]; prefill 1-D: NULL
+  int rope_m3;
+  int sec0, sec1;      // M-RoPE section boundaries (pairs)
+  const float *rope_tab;
+  int rope_max;
+  int *status;
+};
+
+enum { PRO_PLAIN = 0, PRO_NORM = 1 };
+
+// attention: positions per split are a power of two in [ATTN_SMIN, ATTN_SMAX]
+constexpr int ATTN_SMAX = 1024;
+constexpr int ATTN_SMIN = 64;
+enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+
+struct AttnArgs {
+  const void *q;
+  int ld_q;
+  const void *kv;
+  const int64_t *kv_base;
+  const int *kv_cap;
+  const int *kv_len;
+  int layer;
+  int n_heads, n_kv;
+  int prefill_req; // < 0: decode (query = request, length = len + 1); else prefill row r, length r + 1
+  int S;           // positions per split
+  int n_split;     // splits per (query, kv head)
+  float *part_o;   // [nq][n_heads][n_split][head_dim]
+  float *part_ml;  // [nq][n_heads][n_split][2]
+  float scale;
+  void *out;       // combined output, model dtype [nq][n_heads * head_dim]
+};
+
+hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, int n_groups, hipStream_t st);
+hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);
+hipError_t launch_combine(int dtype, int head_dim, int nq, const AttnArgs &a, hipStream_t st);
+hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x,
+                        int *status, hipStream_t st);
+hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *embed, int vocab, int d,
+                               const int *ids, int s_text, float *x, int *status, hipStream_t st);
+hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
+                         int advance, hipStream_t st);
+hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st);
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, hipStream_t st);
+
+bool attn_supported(int dtype, int head_dim, int group);
+
+}  // namespace hs
+
+struct hs_model {
+  hs_config cfg;
+  hs_weights w;
+  std::vector<hs_layer_weights> layers;
+  int device = 0;
+  int max_batch = 0, max_ctx = 0;
+  int64_t part_entries = 0; // capacity of the attention partial buffers in (query, head, split) entries
+  // workspaces (device)
+  float *x = nullptr;       // [max_rows][d] residual stream
+  void *q = nullptr;        // [max_rows][n_h * d_h] q after RoPE
+  void *attn = nullptr;     // [max_rows][n_h * d_h] attention output
+  void *act = nullptr;      // [max_rows][F] SwiGLU output
+  float *logits = nullptr;  // [max_batch][V] (used when the caller passes no logits buffer)
+  float *part_o = nullptr;
+  float *part_ml = nullptr;
+  float *rope_tab = nullptr; // [max_ctx][d_h / 2][2]
+  int *status = nullptr;
+};
+
+struct hs_kv {
+  hs_model *m = nullptr;
+  int batch = 0;
+  void *buf = nullptr;
+  uint64_t buf_bytes = 0;
+  std::vector<int> n_v, cap, len, rope;
+  std::vector<int64_t> base;
+  std::vector<char> ready;
+  int max_cap = 0;
+  int64_t *d_base = nullptr;
+  int *d_cap = nullptr, *d_len = nullptr, *d_rope = nullptr;
+};

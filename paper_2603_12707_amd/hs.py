@@ -1,0 +1,231 @@
+"""Thin ctypes binding of libhs (include/hs.h).
+
+Argument marshalling only: every step of prefill and decode runs in the HIP
+kernels of libhs.so.  torch tensors supply device memory and the current HIP
+stream.  The library is loaded from this package directory; if it is missing
+the import fails loudly (there is no fallback path).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhs.so")
+
+HS_OK, HS_E_INVALID, HS_E_CAPACITY, HS_E_BUFFER, HS_E_STATE, HS_E_DEVICE = 0, -1, -2, -3, -4, -5
+HS_F32, HS_F16, HS_BF16 = 0, 1, 2
+HS_ROPE_1D, HS_ROPE_M3 = 0, 1
+
+# every symbol include/hs.h declares
+EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
+           "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
+           "hs_kv_read", "hs_kv_set_length")
+
+
+class HsError(RuntimeError):
+    def __init__(self, func: str, code: int, msg: str):
+        super().__init__(f"{func} failed with status {code}: {msg}")
+        self.code = code
+
+
+class hs_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("rope_kind", ctypes.c_int32), ("mrope_section", ctypes.c_int32 * 3),
+                ("qkv_bias", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class hs_layer_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "wq", "wk", "wv", "bq", "bk", "bv", "wo", "mlp_norm",
+                                                 "w_gate", "w_up", "w_down")]
+
+
+class hs_weights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(hs_layer_weights))]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libhs.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    # torch ships its own HIP runtime under the same soname as the system one;
+    # importing it first makes libhs.so bind to that runtime instead of
+    # loading a second copy into the process
+    import torch  # noqa: F401
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with paper_2603_12707_amd/build.py "
+                          "(or __graft_entry__.build()); there is no fallback implementation")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, U64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    L.hs_last_error.restype = ctypes.c_char_p
+    L.hs_last_error.argtypes = []
+    sig = {
+        "hs_kv_bytes": [ctypes.POINTER(hs_config), I64, I64, ctypes.POINTER(U64), ctypes.POINTER(U64)],
+        "hs_model_create": [ctypes.POINTER(hs_config), ctypes.POINTER(hs_weights), I32, I32, ctypes.POINTER(P)],
+        "hs_model_free": [P],
+        "hs_kv_alloc": [P, I32, P, P, P, U64, ctypes.POINTER(P)],
+        "hs_kv_free": [P],
+        "hs_prefill_embeddings": [P, P, I32, P, P, I32, P, P, P, P],
+        "hs_decode_step": [P, P, P, P, P, P, P],
+        "hs_model_status": [P, ctypes.POINTER(I32)],
+        "hs_kv_lengths": [P, P],
+        "hs_kv_write": [P, I32, I32, I32, I32, I32, I32, P, I32],
+        "hs_kv_read": [P, I32, I32, I32, I32, I32, I32, P, I32],
+        "hs_kv_set_length": [P, I32, I32, I32],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def check(func: str, rc: int) -> None:
+    if rc != HS_OK:
+        raise HsError(func, rc, lib().hs_last_error().decode())
+
+
+def _call(func: str, *args) -> None:
+    check(func, getattr(lib(), func)(*args))
+
+
+def make_config(cfg: dict) -> hs_config:
+    c = hs_config()
+    for k in ("n_layers", "d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "vocab", "rope_kind",
+              "qkv_bias"):
+        setattr(c, k, int(cfg[k]))
+    c.rope_theta = float(cfg["rope_theta"])
+    c.rms_eps = float(cfg["rms_eps"])
+    c.mrope_section[:] = [int(v) for v in cfg["mrope_section"]]
+    c.dtype = {"f32": HS_F32, "f16": HS_F16, "bf16": HS_BF16}[cfg["dtype"]]
+    return c
+
+
+def hs_kv_bytes(cfg: dict, n_v: int, s_text: int) -> tuple:
+    kv, emb = ctypes.c_uint64(), ctypes.c_uint64()
+    _call("hs_kv_bytes", ctypes.byref(make_config(cfg)), n_v, s_text, ctypes.byref(kv), ctypes.byref(emb))
+    return kv.value, emb.value
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+class Model:
+    """A model over caller-owned device weight tensors named as in the
+    workload generator (embed, layers.{i}.wq, ..., final_norm, lm_head)."""
+
+    def __init__(self, cfg: dict, weights: dict, max_batch: int, max_ctx: int):
+        self.cfg = cfg
+        self._w = weights  # keeps the tensors alive
+        L = cfg["n_layers"]
+        self._layers = (hs_layer_weights * L)()
+        for i in range(L):
+            p = f"layers.{i}."
+            for n in ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down"):
+                setattr(self._layers[i], n, weights[p + n].data_ptr())
+            if cfg["qkv_bias"]:
+                for n in ("bq", "bk", "bv"):
+                    setattr(self._layers[i], n, weights[p + n].data_ptr())
+        hw = hs_weights()
+        hw.embed = weights["embed"].data_ptr()
+        if cfg.get("lm_head", True):
+            hw.final_norm = weights["final_norm"].data_ptr()
+            hw.lm_head = weights["lm_head"].data_ptr()
+        hw.layers = self._layers
+        self._hw = hw
+        self._cfg_c = make_config(cfg)
+        h = ctypes.c_void_p()
+        _call("hs_model_create", ctypes.byref(self._cfg_c), ctypes.byref(hw), max_batch, max_ctx, ctypes.byref(h))
+        self.handle = h
+        self.max_batch, self.max_ctx = max_batch, max_ctx
+
+    def status(self) -> int:
+        f = ctypes.c_int32()
+        _call("hs_model_status", self.handle, ctypes.byref(f))
+        return f.value
+
+    def close(self) -> None:
+        if self.handle:
+            _call("hs_model_free", self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class KVCache:
+    """Per-request contiguous KV cache over a caller-owned uint8 device tensor."""
+
+    def __init__(self, model: Model, n_v, capacity, buf=None):
+        import torch
+        self.model = model
+        self.batch = len(capacity)
+        self.n_v = [int(v) for v in n_v]
+        self.capacity = [int(c) for c in capacity]
+        cfg = model.cfg
+        need = sum(hs_kv_bytes(cfg, 0, c)[0] for c in self.capacity)
+        if buf is None:
+            buf = torch.empty(need, dtype=torch.uint8, device="cuda")
+        self.buf = buf
+        nv = (ctypes.c_int32 * self.batch)(*self.n_v)
+        cap = (ctypes.c_int32 * self.batch)(*self.capacity)
+        h = ctypes.c_void_p()
+        _call("hs_kv_alloc", model.handle, self.batch, nv, cap, _ptr(buf), buf.numel() * buf.element_size(),
+              ctypes.byref(h))
+        self.handle = h
+
+    def prefill(self, req: int, emb, text_ids, pos_thw=None, last_logits=None, first_token=None):
+        import torch
+        if first_token is None:
+            first_token = torch.empty(1, dtype=torch.int32, device="cuda")
+        _call("hs_prefill_embeddings", self.model.handle, self.handle, req, _ptr(emb), _ptr(text_ids),
+              0 if text_ids is None else text_ids.numel(), _ptr(pos_thw), _ptr(last_logits), _ptr(first_token),
+              _stream())
+        return first_token
+
+    def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None) -> None:
+        _call("hs_decode_step", self.model.handle, self.handle, _ptr(tokens_in), _ptr(tokens_out), _ptr(logits),
+              _ptr(hidden_out), _stream())
+
+    def lengths(self) -> list:
+        out = (ctypes.c_int32 * self.batch)()
+        _call("hs_kv_lengths", self.handle, out)
+        return list(out)
+
+    def write(self, req: int, layer: int, kv_sel: int, head: int, pos0: int, rows) -> None:
+        n = rows.shape[0]
+        _call("hs_kv_write", self.handle, req, layer, kv_sel, head, pos0, n, _ptr(rows), int(rows.is_cuda))
+
+    def read(self, req: int, layer: int, kv_sel: int, head: int, pos0: int, n: int, out) -> None:
+        _call("hs_kv_read", self.handle, req, layer, kv_sel, head, pos0, n, _ptr(out), int(out.is_cuda))
+
+    def set_length(self, req: int, length: int, rope_pos: int) -> None:
+        _call("hs_kv_set_length", self.handle, req, length, rope_pos)
+
+    def close(self) -> None:
+        if self.handle:
+            _call("hs_kv_free", self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

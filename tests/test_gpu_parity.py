@@ -1,0 +1,122 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle on the same
+seeded inputs, at sizes the oracle finishes in seconds that still span several
+tiles, splits and ragged tails."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import LOGIT_TOL, Pair, rel_err, small_cfg, token_ok
+from workload import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False):
+    """Prefills every request on both sides, then runs n_dec decode steps for
+    the whole batch (teacher-forced on the oracle's tokens unless
+    free_running).  Returns the number of near ties."""
+    import paper_2603_12707_amd as hs
+    B = len(n_v_list)
+    caps = [n + s + n_dec + extra_cap for n, s in zip(n_v_list, s_text_list)]
+    pair = Pair(cfg, max_batch=B, max_ctx=max(caps))
+    kv = hs.KVCache(pair.gpu, n_v_list, caps)
+    seqs, cur_ref, cur_gpu = [], [], []
+    near = 0
+    V = cfg["vocab"]
+    for b in range(B):
+        emb, ids, pos = pair.request_inputs(b, n_v_list[b], s_text_list[b])
+        s = pair.ora.new_seq(caps[b])
+        ref_logits, ref_tok = s.prefill(emb if n_v_list[b] else None, ids, pos)
+        seqs.append(s)
+        lg = torch.empty(V, dtype=torch.float32, device="cuda")
+        tok = kv.prefill(b, emb.cuda() if n_v_list[b] else None, ids.cuda() if s_text_list[b] else None,
+                         None if pos is None else pos.cuda(), last_logits=lg)
+        torch.cuda.synchronize()
+        g = lg.cpu().numpy()
+        assert rel_err(g, ref_logits) <= LOGIT_TOL, (b, rel_err(g, ref_logits))
+        ok, tie = token_ok(int(tok.item()), g, ref_logits)
+        assert ok, (b, int(tok.item()), ref_tok)
+        near += tie
+        cur_ref.append(ref_tok)
+        cur_gpu.append(int(tok.item()))
+    assert kv.lengths() == [n + s for n, s in zip(n_v_list, s_text_list)]
+    tin = torch.empty(B, dtype=torch.int32, device="cuda")
+    tout = torch.empty(B, dtype=torch.int32, device="cuda")
+    logits = torch.empty(B, V, dtype=torch.float32, device="cuda")
+    hidden = torch.empty(B, cfg["d_model"], dtype=torch.float32, device="cuda")
+    for step in range(n_dec):
+        feed = cur_gpu if free_running else cur_ref
+        tin.copy_(torch.tensor(feed, dtype=torch.int32))
+        kv.decode(tin, tout, logits, hidden)
+        torch.cuda.synchronize()
+        g_tok = tout.cpu().tolist()
+        g_log = logits.cpu().numpy()
+        g_hid = hidden.cpu().numpy()
+        nxt_ref = []
+        for b in range(B):
+            r_log, r_hid, r_tok = seqs[b].decode(feed[b])
+            assert rel_err(g_log[b], r_log) <= LOGIT_TOL, (step, b, rel_err(g_log[b], r_log))
+            assert rel_err(g_hid[b], r_hid) <= LOGIT_TOL, (step, b)
+            ok, tie = token_ok(g_tok[b], g_log[b], r_log)
+            assert ok, (step, b, g_tok[b], r_tok)
+            near += tie
+            nxt_ref.append(r_tok)
+        if free_running:
+            assert g_tok == nxt_ref, (step, g_tok, nxt_ref)
+        cur_ref, cur_gpu = nxt_ref, g_tok
+    assert kv.lengths() == [n + s + n_dec for n, s in zip(n_v_list, s_text_list)]
+    assert pair.gpu.status() == 0
+    kv.close()
+    pair.gpu.close()
+    return near
+
+
+def test_tiny_config_free_running_token_for_token():
+    """The tiny fp32 decoder: 576 vision rows + 32 text tokens, 16 greedy
+    steps, tokens identical to the oracle's without teacher forcing."""
+    cfg = configs.get("tiny")
+    n_v, s_text = synth.request_lengths(cfg)
+    near = _run_pair(cfg, n_v, s_text, cfg["n_dec"], free_running=True)
+    assert near == 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_mha_batch_ragged(dtype):
+    # three requests with different vision/text lengths; d = 384 leaves one
+    # wave without K blocks, F = 1000 and V = 997 leave ragged tails
+    near = _run_pair(small_cfg(dtype=dtype), [40, 0, 129], [7, 33, 1], 5)
+    assert near <= 1
+
+
+@pytest.mark.parametrize("group,n_heads,head_dim", [(2, 4, 128), (4, 8, 64), (7, 14, 64), (8, 8, 64)])
+def test_gqa_groups(group, n_heads, head_dim):
+    cfg = small_cfg(n_heads=n_heads, n_kv_heads=n_heads // group, head_dim=head_dim, dtype="bf16")
+    near = _run_pair(cfg, [33, 5], [20, 260], 4)
+    assert near <= 1
+
+
+def test_mrope_qkv_bias_gqa7():
+    cfg = small_cfg(n_heads=14, n_kv_heads=2, head_dim=64, dtype="bf16", rope_kind=1, mrope_section=(8, 12, 12),
+                    qkv_bias=1, rope_theta=1e6, rms_eps=1e-6)
+    near = _run_pair(cfg, [70, 16, 121], [12, 12, 3], 5)
+    assert near <= 1
+
+
+@pytest.mark.parametrize("B", [17, 33])
+def test_column_tiles(B):
+    """Batches spanning two and three 16-column tiles."""
+    cfg = small_cfg(n_layers=1, dtype="f16")
+    n_v = [(7 * b) % 23 for b in range(B)]
+    s_text = [1 + (5 * b) % 11 for b in range(B)]
+    near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 2
+
+
+def test_long_context_many_splits():
+    """A context long enough for many attention splits in decode and several
+    in prefill."""
+    cfg = small_cfg(n_layers=1, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=512, vocab=512)
+    near = _run_pair(cfg, [1100], [37], 3, extra_cap=400)
+    assert near == 0
