@@ -1,0 +1,279 @@
+#!/usr/bin/env python3
+"""Decode-step throughput of the language-decode hot path on one MI355X.
+
+A step is one hs_decode_step call: embedding gather, every decoder layer
+(RMSNorm + q/k/v + RoPE + KV append, split-K attention and combine, output
+projection, RMSNorm + gate/up + SwiGLU, down projection) and the final norm,
+LM head and greedy selection, for every request of the batch.  Inputs are
+seeded synthetic tensors generated directly in HBM; the KV cache is filled by
+hs_prefill_embeddings from the vision rows and text tokens before timing.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E
+METRIC = "decode tokens/s at batch B + achieved HBM GB/s vs peak, 7B-shaped fp16"
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def weight_bytes(cfg: dict) -> dict:
+    """Algorithmic bytes of each weight set streamed once per step."""
+    b = 2 if cfg["dtype"] != "f32" else 4
+    d, nh, nkv, hd, F, V = (cfg[k] for k in ("d_model", "n_heads", "n_kv_heads", "head_dim", "ffn_dim", "vocab"))
+    qkv = (nh + 2 * nkv) * hd * d + (nh + 2 * nkv) * hd * cfg["qkv_bias"] + d  # + attn_norm gain
+    out = {
+        "qkv": qkv * b,
+        "oproj": d * nh * hd * b,
+        "gateup": (2 * F * d + d) * b,  # + mlp_norm gain
+        "down": d * F * b,
+    }
+    out["head"] = (V * d + d) * b if cfg.get("lm_head", True) else 0
+    return out
+
+
+def step_bytes(cfg: dict, lens: list) -> int:
+    """Algorithmic HBM bytes of one step: every weight once, the embedding
+    rows, every request's K/V rows 0..len_b (read) and the appended row
+    (written)."""
+    b = 2 if cfg["dtype"] != "f32" else 4
+    wb = weight_bytes(cfg)
+    L, nkv, hd, d = cfg["n_layers"], cfg["n_kv_heads"], cfg["head_dim"], cfg["d_model"]
+    per_layer = wb["qkv"] + wb["oproj"] + wb["gateup"] + wb["down"]
+    kv_row = 2 * L * nkv * hd * b
+    B = len(lens)
+    return L * per_layer + wb["head"] + B * d * b + sum(kv_row * (n + 1) for n in lens) + B * kv_row
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in ("paper_2603_12707_amd/csrc/hs_kernels.hip", "paper_2603_12707_amd/csrc/hs_internal.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if there is none for this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    src = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not src or not val or src.group(1) != kernel_source_hash():
+        return None
+    return float(val.group(1))
+
+
+def setup(cfg: dict, n_steps_total: int):
+    import torch
+
+    import paper_2603_12707_amd as hs
+    from workload import synth
+    B = cfg["batch"]
+    t = time.time()
+    w = synth.make_weights(cfg, device="cuda")
+    torch.cuda.synchronize()
+    log(f"weights generated in HBM: {sum(v.numel() * v.element_size() for v in w.values()) / 1e9:.2f} GB "
+        f"in {time.time() - t:.1f} s")
+    if "kv_len" in cfg:  # layer stack fed from a synthetic cache
+        lens = synth.kv_lengths(cfg)
+        n_v = [0] * B
+    else:
+        n_v, s_text = synth.request_lengths(cfg)
+        lens = [a + b for a, b in zip(n_v, s_text)]
+    caps = [n + n_steps_total for n in lens]
+    model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps))
+    kv = hs.KVCache(model, n_v, caps)
+    first = torch.empty(B, dtype=torch.int32, device="cuda")
+    t = time.time()
+    if "kv_len" in cfg:
+        for r in range(B):
+            for layer in range(cfg["n_layers"]):
+                for sel in (0, 1):
+                    for h in range(cfg["n_kv_heads"]):
+                        kv.write(r, layer, sel, h, 0, synth.kv_block(cfg, r, layer, sel, h, lens[r], device="cuda"))
+            kv.set_length(r, lens[r], lens[r])
+        first.copy_(synth.decode_tokens(cfg, 0, B, device="cuda"))
+    else:
+        for r in range(B):
+            emb = synth.vision_rows(cfg, r, n_v[r], device="cuda")
+            ids = synth.text_ids(cfg, r, s_text[r], device="cuda")
+            pos = synth.mrope_positions(n_v[r], s_text[r]).cuda() if cfg["rope_kind"] == 1 else None
+            kv.prefill(r, emb if n_v[r] else None, ids if s_text[r] else None, pos, first_token=first[r:r + 1])
+    torch.cuda.synchronize()
+    log(f"context ready for {B} request(s) in {time.time() - t:.1f} s (lengths {min(lens)}..{max(lens)})")
+    return w, model, kv, first, lens
+
+
+def cpu_baseline(cfg: dict, w_gpu: dict, ctx: int, n_tokens: int = 2) -> dict:
+    """The oracle, single-threaded on one host core, decoding n_tokens for one
+    request of the workload from a synthetic cache of ctx positions."""
+    import torch
+
+    from oracle import oracle as O
+    from workload import synth
+    t = time.time()
+    w_cpu = {k: v.cpu() for k, v in w_gpu.items()}
+    model = O.Model(cfg, w_cpu)
+    seq = model.new_seq(ctx + n_tokens)
+    for layer in range(cfg["n_layers"]):
+        for sel in (0, 1):
+            for h in range(cfg["n_kv_heads"]):
+                seq.write_kv(layer, sel, h, 0, synth.kv_block(cfg, 0, layer, sel, h, ctx, device="cuda").float().cpu())
+    seq.set_len(ctx, ctx)
+    log(f"oracle inputs ready in {time.time() - t:.1f} s")
+    tok = int(synth.decode_tokens(cfg, 0, 1)[0])
+    t = time.perf_counter()
+    for _ in range(n_tokens):
+        _, _, nxt = seq.decode(tok)
+        tok = nxt if cfg.get("lm_head", True) else tok
+    el = time.perf_counter() - t
+    log(f"oracle: {n_tokens} tokens in {el:.1f} s")
+    del w_cpu
+    return {"value": n_tokens / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_tokens} greedy decode steps of one request of the workload from a synthetic "
+                      f"{ctx}-position KV cache, single-threaded plain C oracle (fp64 accumulation) on one host core"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=120)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="llava7b_b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: this build has no multi-GPU path (the decode step is sharded "
+              "by request across GPUs with no exchange; see the design notes). Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from workload import configs
+    cfg = configs.get(args.workload)
+    B = cfg["batch"]
+    torch.cuda.set_device(0)
+    n_prof = min(10, args.steps)
+    w, model, kv, first, lens0 = setup(cfg, args.warmup + args.steps + n_prof)
+
+    tin = first.clone()
+    tout = torch.empty_like(tin)
+    has_head = cfg.get("lm_head", True)
+
+    def step():
+        nonlocal tin, tout
+        kv.decode(tin, tout if has_head else None)
+        if has_head:
+            tin, tout = tout, tin
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K steps; the dominant kernel (gate/up projection) carries
+    # a HIP event pair on the library's stream for every launch
+    dominant = "gateup"
+    model.set_timing([dominant], cfg["n_layers"] * args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tim = model.timing()
+    model.set_timing([], 0)
+    lens_after = kv.lengths()
+
+    # per-kernel breakdown over a few more steps (every kind timed)
+    model.set_timing(["embed", "qkv", "attn", "combine", "oproj", "gateup", "down", "head", "argmax"], 400 * n_prof)
+    t1 = time.perf_counter()
+    for _ in range(n_prof):
+        step()
+    torch.cuda.synchronize()
+    prof_elapsed = time.perf_counter() - t1
+    breakdown = model.timing()
+    model.set_timing([], 0)
+
+    if args.copy_calibration_mib:
+        src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {args.copy_calibration_mib} MiB")
+
+    ms_per_step = elapsed / args.steps * 1e3
+    tok_s = B * args.steps / elapsed
+    lens_start = [n + args.warmup for n in lens0]
+    total_bytes = sum(step_bytes(cfg, [n + k for n in lens_start]) for k in range(args.steps))
+    gbs = total_bytes / elapsed / 1e9
+    assert lens_after == [n + args.steps for n in lens_start], (lens_after[:4], lens_start[:4])
+
+    dom_ms, dom_n = tim[dominant]
+    dom_avg_s = dom_ms / dom_n / 1e3
+    dom_bytes = weight_bytes(cfg)[dominant]
+    achieved = dom_bytes / dom_avg_s / 1e9
+    traffic = stored_traffic(args.workload, dominant)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "kernel": "k_gemm (RMSNorm + gate/up projection + SwiGLU)",
+                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": dom_n}
+    kernels = {k: {"avg_us": round(v[0] / v[1] * 1e3, 2), "launches_per_step": v[1] / n_prof,
+                   "ms_per_step": round(v[0] / n_prof, 4)}
+               for k, v in breakdown.items() if k != "dropped"}
+    kernel_ms = sum(v[0] for k, v in breakdown.items() if k != "dropped") / n_prof
+
+    out = {
+        "metric": METRIC,
+        "value": round(tok_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic (seeded: N(0,0.02) weights, N(0,1) vision rows, uniform text ids; generated in HBM)",
+        "config": {"workload": args.workload, "batch": B, "context_at_start": lens_start[0] if B == 1 else
+                   [min(lens_start), max(lens_start)], "n_layers": cfg["n_layers"], "d_model": cfg["d_model"],
+                   "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"], "ffn_dim": cfg["ffn_dim"],
+                   "vocab": cfg["vocab"] if has_head else None, "parallelism": "none (one GPU)"},
+        "hbm_gbps": round(gbs, 1),
+        "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "bytes_per_step": total_bytes // args.steps,
+        "roofline": roofline,
+        "kernels": kernels,
+        "kernel_ms_per_step": round(kernel_ms, 4),
+        "profiled_ms_per_step": round(prof_elapsed / n_prof * 1e3, 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, w, lens_start[0])
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

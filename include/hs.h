@@ -171,6 +171,33 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
  * id was replaced by 0).  Synchronises the device. */
 int hs_model_status(hs_model *m, int32_t *flags);
 
+/* ---- per-kernel timing (measurement hook) ---- */
+
+/* Kernel kinds of one decode step, in launch order within a layer. */
+#define HS_K_EMBED 0   /* token embedding gather */
+#define HS_K_QKV 1     /* RMSNorm + q/k/v projection + RoPE + KV append */
+#define HS_K_ATTN 2    /* split-K attention over the KV cache */
+#define HS_K_COMBINE 3 /* split combine */
+#define HS_K_OPROJ 4   /* output projection + residual */
+#define HS_K_GATEUP 5  /* RMSNorm + gate/up projection + SwiGLU */
+#define HS_K_DOWN 6    /* down projection + residual */
+#define HS_K_HEAD 7    /* final RMSNorm + LM head */
+#define HS_K_ARGMAX 8  /* greedy selection and length advance */
+#define HS_K_COUNT 9
+
+/* Attaches a HIP start/stop event pair to every later launch (on the call's
+ * stream) of the kinds in kind_mask (bit k = kind k), up to max_launches
+ * launches; launches beyond that run untimed and are counted as dropped.
+ * kind_mask 0 switches timing off and releases the events.  Event creation
+ * happens here, never inside the timed calls. */
+int hs_model_set_timing(hs_model *m, int32_t kind_mask, int32_t max_launches);
+
+/* Synchronises the device, adds up the elapsed time of every timed launch per
+ * kind into total_ms[n_kinds] (milliseconds) and launches[n_kinds], returns
+ * the number of dropped launches in *dropped (may be NULL), and resets the
+ * accumulators. */
+int hs_model_timing(hs_model *m, int32_t n_kinds, double *total_ms, int64_t *launches, int64_t *dropped);
+
 /* ---- test and fill hooks (synchronous) ---- */
 
 /* Host copy of every request's current length (int32 [batch]). */

@@ -33,6 +33,33 @@ int fail(int code, const char *fmt, ...) {
 
 int dtype_bytes(int dt) { return dt == HS_F32 ? 4 : 2; }
 
+// Runs one launcher, attaching a timing event pair when its kind is timed.
+template <typename F>
+hipError_t timed(hs_model *m, int kind, F &&launch) {
+  const bool on = (m->timing_mask >> kind) & 1;
+  if (on && m->ev_used < (int)m->ev_start.size()) {
+    g_launch_events.start = m->ev_start[m->ev_used];
+    g_launch_events.stop = m->ev_stop[m->ev_used];
+    m->ev_kind[m->ev_used++] = kind;
+  } else if (on) {
+    m->ev_dropped++;
+  }
+  const hipError_t e = launch();
+  g_launch_events = LaunchEvents{};
+  return e;
+}
+
+void release_events(hs_model *m) {
+  for (hipEvent_t e : m->ev_start) (void)hipEventDestroy(e);
+  for (hipEvent_t e : m->ev_stop) (void)hipEventDestroy(e);
+  m->ev_start.clear();
+  m->ev_stop.clear();
+  m->ev_kind.clear();
+  m->ev_used = 0;
+  m->ev_dropped = 0;
+  m->timing_mask = 0;
+}
+
 // Light checks needed by the size formula alone.
 bool shape_ok(const hs_config *c) {
   return c && c->n_layers > 0 && c->n_kv_heads > 0 && c->head_dim > 0 && c->d_model > 0 && c->dtype >= HS_F32 &&
@@ -79,6 +106,7 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
 
 void free_model(hs_model *m) {
   if (!m) return;
+  release_events(m);
   void *ptrs[] = {m->x, m->q, m->attn, m->act, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
@@ -126,7 +154,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
-    HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, (nh + 2 * nkv) * hd / 32, st));
+    HIP_TRY(timed(m, HS_K_QKV, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, (nh + 2 * nkv) * hd / 32, st); }));
 
     AttnArgs a{};
     a.q = m->q;
@@ -145,8 +173,8 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     a.part_ml = m->part_ml;
     a.scale = (float)(1.0 / std::sqrt((double)hd));
     a.out = m->attn;
-    HIP_TRY(launch_attention(c.dtype, hd, nh / nkv, ncols, a, st));
-    HIP_TRY(launch_combine(c.dtype, hd, ncols, a, st));
+    HIP_TRY(timed(m, HS_K_ATTN, [&] { return launch_attention(c.dtype, hd, nh / nkv, ncols, a, st); }));
+    HIP_TRY(timed(m, HS_K_COMBINE, [&] { return launch_combine(c.dtype, hd, ncols, a, st); }));
 
     GemmArgs o{};
     o.w[0] = W.wo;
@@ -156,7 +184,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     o.x = m->attn;
     o.resid = m->x;
     o.ld_resid = d;
-    HIP_TRY(launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, (d + 15) / 16, st));
+    HIP_TRY(timed(m, HS_K_OPROJ, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, (d + 15) / 16, st); }));
 
     GemmArgs u{};
     u.w[0] = W.w_gate;
@@ -169,7 +197,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     u.eps = c.rms_eps;
     u.out = m->act;
     u.ld_out = F;
-    HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, (F + 15) / 16, st));
+    HIP_TRY(timed(m, HS_K_GATEUP, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, (F + 15) / 16, st); }));
 
     GemmArgs dn{};
     dn.w[0] = W.w_down;
@@ -179,7 +207,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     dn.x = m->act;
     dn.resid = m->x;
     dn.ld_resid = d;
-    HIP_TRY(launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, (d + 15) / 16, st));
+    HIP_TRY(timed(m, HS_K_DOWN, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, (d + 15) / 16, st); }));
   }
   return HS_OK;
 }
@@ -197,7 +225,7 @@ int run_head(hs_model *m, const float *x_rows, int ncols, float *logits, hipStre
   g.eps = c.rms_eps;
   g.out = logits;
   g.ld_out = c.vocab;
-  HIP_TRY(launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, (c.vocab + 31) / 32, st));
+  HIP_TRY(timed(m, HS_K_HEAD, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, (c.vocab + 31) / 32, st); }));
   return HS_OK;
 }
 
@@ -329,6 +357,48 @@ int hs_model_status(hs_model *m, int32_t *flags) {
   return HS_OK;
 }
 
+int hs_model_set_timing(hs_model *m, int32_t kind_mask, int32_t max_launches) {
+  if (!m) return fail(HS_E_INVALID, "hs_model_set_timing: NULL model");
+  if (kind_mask < 0 || kind_mask >= (1 << HS_K_COUNT) || max_launches < 0)
+    return fail(HS_E_INVALID, "hs_model_set_timing: bad mask or launch count");
+  HIP_TRY(hipDeviceSynchronize());
+  release_events(m);
+  if (!kind_mask) return HS_OK;
+  m->ev_start.resize(max_launches, nullptr);
+  m->ev_stop.resize(max_launches, nullptr);
+  m->ev_kind.resize(max_launches, -1);
+  for (int i = 0; i < max_launches; ++i) {
+    if (hipEventCreate(&m->ev_start[i]) != hipSuccess || hipEventCreate(&m->ev_stop[i]) != hipSuccess) {
+      release_events(m);
+      return fail(HS_E_DEVICE, "hs_model_set_timing: hipEventCreate failed");
+    }
+  }
+  m->timing_mask = kind_mask;
+  return HS_OK;
+}
+
+int hs_model_timing(hs_model *m, int32_t n_kinds, double *total_ms, int64_t *launches, int64_t *dropped) {
+  if (!m || !total_ms || !launches || n_kinds < 0) return fail(HS_E_INVALID, "hs_model_timing: bad argument");
+  HIP_TRY(hipDeviceSynchronize());
+  for (int k = 0; k < n_kinds; ++k) {
+    total_ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  for (int i = 0; i < m->ev_used; ++i) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, m->ev_start[i], m->ev_stop[i]));
+    const int k = m->ev_kind[i];
+    if (k >= 0 && k < n_kinds) {
+      total_ms[k] += ms;
+      launches[k] += 1;
+    }
+  }
+  if (dropped) *dropped = m->ev_dropped;
+  m->ev_used = 0;
+  m->ev_dropped = 0;
+  return HS_OK;
+}
+
 int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *capacity, void *dev_buf,
                 uint64_t buf_bytes, hs_kv **out) {
   if (!out) return fail(HS_E_INVALID, "hs_kv_alloc: out is NULL");
@@ -447,7 +517,7 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
   if ((int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "hs_decode_step: attention workspace too small");
   hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st));
+  HIP_TRY(timed(m, HS_K_EMBED, [&] { return launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st); }));
   int rc = run_layers(m, kv, B, -1, kv->d_rope, S, ns, st);
   if (rc) return rc;
   if (hidden_out)
@@ -456,9 +526,9 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
     float *lg = logits ? logits : m->logits;
     rc = run_head(m, m->x, B, lg, st);
     if (rc) return rc;
-    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st));
+    HIP_TRY(timed(m, HS_K_ARGMAX, [&] { return launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st); }));
   } else {
-    HIP_TRY(launch_advance(kv->d_len, kv->d_rope, B, st));
+    HIP_TRY(timed(m, HS_K_ARGMAX, [&] { return launch_advance(kv->d_len, kv->d_rope, B, st); }));
   }
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
   return HS_OK;

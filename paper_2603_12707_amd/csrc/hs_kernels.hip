@@ -13,12 +13,20 @@
 #include <cmath>
 
 namespace hs {
+
+thread_local LaunchEvents g_launch_events;
+
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// every launch carries the timing hook's events (null when untimed)
+#define HS_LAUNCH(kernel, grid, block, shmem, stream, ...)                                                        \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, g_launch_events.start, g_launch_events.stop, 0, \
+                        __VA_ARGS__)
 
 // ---------------------------------------------------------------------------
 // storage dtypes
@@ -666,7 +674,7 @@ template <int DT, int R, int NT, int PRO, int EPI>
 hipError_t gemm_launch(const GemmArgs &a, int n_groups, hipStream_t st) {
   constexpr int NW = 4;
   const dim3 grid(n_groups, (a.ncols + 16 * NT - 1) / (16 * NT));
-  hipLaunchKernelGGL((k_gemm<DT, R, NT, NW, PRO, EPI>), grid, dim3(64 * NW), 0, st, a);
+  HS_LAUNCH((k_gemm<DT, R, NT, NW, PRO, EPI>), grid, dim3(64 * NW), 0, st, a);
   return hipGetLastError();
 }
 
@@ -692,11 +700,11 @@ template <int DT, int HD>
 hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
   const dim3 grid(a.n_split, a.n_kv, nq);
   switch (group) {
-    case 1: hipLaunchKernelGGL((k_attn<DT, HD, 1>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((k_attn<DT, HD, 2>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((k_attn<DT, HD, 4>), grid, dim3(256), 0, st, a); break;
-    case 7: hipLaunchKernelGGL((k_attn<DT, HD, 7>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((k_attn<DT, HD, 8>), grid, dim3(256), 0, st, a); break;
+    case 1: HS_LAUNCH((k_attn<DT, HD, 1>), grid, dim3(256), 0, st, a); break;
+    case 2: HS_LAUNCH((k_attn<DT, HD, 2>), grid, dim3(256), 0, st, a); break;
+    case 4: HS_LAUNCH((k_attn<DT, HD, 4>), grid, dim3(256), 0, st, a); break;
+    case 7: HS_LAUNCH((k_attn<DT, HD, 7>), grid, dim3(256), 0, st, a); break;
+    case 8: HS_LAUNCH((k_attn<DT, HD, 8>), grid, dim3(256), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -712,8 +720,8 @@ hipError_t attn_dt(int head_dim, int group, int nq, const AttnArgs &a, hipStream
 template <int DT>
 hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
   const dim3 grid(a.n_heads, nq);
-  if (head_dim == 64) hipLaunchKernelGGL((k_combine<DT, 64>), grid, dim3(64), 0, st, a);
-  else if (head_dim == 128) hipLaunchKernelGGL((k_combine<DT, 128>), grid, dim3(128), 0, st, a);
+  if (head_dim == 64) HS_LAUNCH((k_combine<DT, 64>), grid, dim3(64), 0, st, a);
+  else if (head_dim == 128) HS_LAUNCH((k_combine<DT, 128>), grid, dim3(128), 0, st, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -759,9 +767,9 @@ hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const in
                         hipStream_t st) {
   if (n <= 0) return hipSuccess;
   switch (dtype) {
-    case HS_F32: hipLaunchKernelGGL(k_embed<HS_F32>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
-    case HS_F16: hipLaunchKernelGGL(k_embed<HS_F16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
-    case HS_BF16: hipLaunchKernelGGL(k_embed<HS_BF16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_F32: HS_LAUNCH(k_embed<HS_F32>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_F16: HS_LAUNCH(k_embed<HS_F16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_BF16: HS_LAUNCH(k_embed<HS_BF16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -772,9 +780,9 @@ hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *
   const int rows = n_v + s_text;
   if (rows <= 0) return hipSuccess;
   switch (dtype) {
-    case HS_F32: hipLaunchKernelGGL(k_prefill_rows<HS_F32>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
-    case HS_F16: hipLaunchKernelGGL(k_prefill_rows<HS_F16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
-    case HS_BF16: hipLaunchKernelGGL(k_prefill_rows<HS_BF16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    case HS_F32: HS_LAUNCH(k_prefill_rows<HS_F32>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    case HS_F16: HS_LAUNCH(k_prefill_rows<HS_F16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    case HS_BF16: HS_LAUNCH(k_prefill_rows<HS_BF16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -783,18 +791,18 @@ hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *
 hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
                          int advance, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_argmax, dim3(n), dim3(1024), 0, st, logits, vocab, ld, tokens_out, len, rope_pos, advance);
+  HS_LAUNCH(k_argmax, dim3(n), dim3(1024), 0, st, logits, vocab, ld, tokens_out, len, rope_pos, advance);
   return hipGetLastError();
 }
 
 hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_advance, dim3((n + 255) / 256), dim3(256), 0, st, len, rope_pos, n);
+  HS_LAUNCH(k_advance, dim3((n + 255) / 256), dim3(256), 0, st, len, rope_pos, n);
   return hipGetLastError();
 }
 
 hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, hipStream_t st) {
-  hipLaunchKernelGGL(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw);
+  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw);
   return hipGetLastError();
 }
 

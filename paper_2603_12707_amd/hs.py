@@ -20,7 +20,9 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length")
+           "hs_kv_read", "hs_kv_set_length", "hs_model_set_timing", "hs_model_timing")
+
+HS_K_NAMES = ("embed", "qkv", "attn", "combine", "oproj", "gateup", "down", "head", "argmax")
 
 
 class HsError(RuntimeError):
@@ -79,6 +81,8 @@ def lib() -> ctypes.CDLL:
         "hs_kv_write": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_read": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_set_length": [P, I32, I32, I32],
+        "hs_model_set_timing": [P, I32, I32],
+        "hs_model_timing": [P, I32, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -157,6 +161,20 @@ class Model:
         f = ctypes.c_int32()
         _call("hs_model_status", self.handle, ctypes.byref(f))
         return f.value
+
+    def set_timing(self, kinds, max_launches: int) -> None:
+        mask = 0
+        for k in kinds:
+            mask |= 1 << HS_K_NAMES.index(k)
+        _call("hs_model_set_timing", self.handle, mask, max_launches)
+
+    def timing(self) -> dict:
+        n = len(HS_K_NAMES)
+        ms, cnt, dropped = (ctypes.c_double * n)(), (ctypes.c_int64 * n)(), ctypes.c_int64()
+        _call("hs_model_timing", self.handle, n, ms, cnt, ctypes.byref(dropped))
+        out = {k: (ms[i], cnt[i]) for i, k in enumerate(HS_K_NAMES) if cnt[i]}
+        out["dropped"] = dropped.value
+        return out
 
     def close(self) -> None:
         if self.handle:
