@@ -88,9 +88,13 @@ def setup(cfg: dict, n_steps_total: int):
     from workload import synth
     B = cfg["batch"]
     t = time.time()
-    w = synth.make_weights(cfg, device="cuda")
+    w = {}
+    for name in synth.weight_names(cfg):  # generate and pack one matrix at a time
+        t_row = synth.make_weight(cfg, name, device="cuda")
+        w[name] = hs.pack_matrix(t_row, cfg["dtype"]) if name.split(".")[-1] in hs.hs.PACKED else t_row
+        del t_row
     torch.cuda.synchronize()
-    log(f"weights generated in HBM: {sum(v.numel() * v.element_size() for v in w.values()) / 1e9:.2f} GB "
+    log(f"weights generated and packed in HBM: {sum(v.numel() * v.element_size() for v in w.values()) / 1e9:.2f} GB "
         f"in {time.time() - t:.1f} s")
     if "kv_len" in cfg:  # layer stack fed from a synthetic cache
         lens = synth.kv_lengths(cfg)
@@ -99,7 +103,7 @@ def setup(cfg: dict, n_steps_total: int):
         n_v, s_text = synth.request_lengths(cfg)
         lens = [a + b for a, b in zip(n_v, s_text)]
     caps = [n + n_steps_total for n in lens]
-    model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps))
+    model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True)
     kv = hs.KVCache(model, n_v, caps)
     first = torch.empty(B, dtype=torch.int32, device="cuda")
     t = time.time()
@@ -122,15 +126,15 @@ def setup(cfg: dict, n_steps_total: int):
     return w, model, kv, first, lens
 
 
-def cpu_baseline(cfg: dict, w_gpu: dict, ctx: int, n_tokens: int = 2) -> dict:
+def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
     """The oracle, single-threaded on one host core, decoding n_tokens for one
-    request of the workload from a synthetic cache of ctx positions."""
-    import torch
-
+    request of the workload from a synthetic cache of ctx positions.  Its
+    row-major weights come from the same seeded generator (run on the GPU for
+    speed; the generator is bit-identical on CPU and GPU)."""
     from oracle import oracle as O
     from workload import synth
     t = time.time()
-    w_cpu = {k: v.cpu() for k, v in w_gpu.items()}
+    w_cpu = {n: synth.make_weight(cfg, n, device="cuda").cpu() for n in synth.weight_names(cfg)}
     model = O.Model(cfg, w_cpu)
     seq = model.new_seq(ctx + n_tokens)
     for layer in range(cfg["n_layers"]):
@@ -270,7 +274,8 @@ def main() -> int:
         "profiled_ms_per_step": round(prof_elapsed / n_prof * 1e3, 4),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, w, lens_start[0])
+        del w
+        out["cpu_baseline"] = cpu_baseline(cfg, lens_start[0])
     print(json.dumps(out), flush=True)
     return 0
 

@@ -75,12 +75,13 @@ typedef struct hs_config {
   int32_t dtype;
 } hs_config;
 
-/* One decoder layer's weights, device pointers, row-major [out, in]
- * (nn.Linear layout), all in the model dtype:
- *   attn_norm, mlp_norm      [d]
- *   wq [n_h*d_h, d]   wk, wv [n_kv*d_h, d]   (bq, bk, bv: [rows] or NULL)
- *   wo [d, n_h*d_h]   w_gate, w_up [F, d]    w_down [d, F]
- * Row-major with no padding; every row starts 16-byte aligned. */
+/* One decoder layer's weights, device pointers in the model dtype.  The
+ * projection matrices are the nn.Linear matrices [out, in] in the packed
+ * layout written by hs_pack_matrix:
+ *   wq [n_h*d_h, d]   wk, wv [n_kv*d_h, d]   wo [d, n_h*d_h]
+ *   w_gate, w_up [F, d]   w_down [d, F]
+ * the norm gains attn_norm, mlp_norm [d] and the optional biases
+ * bq, bk, bv [rows] are plain vectors. */
 typedef struct hs_layer_weights {
   const void *attn_norm;
   const void *wq, *wk, *wv;
@@ -91,8 +92,9 @@ typedef struct hs_layer_weights {
   const void *w_down;
 } hs_layer_weights;
 
-/* embed [V, d]; final_norm [d]; lm_head [V, d].  lm_head == NULL declares a
- * layer stack without a head: decode then produces no tokens or logits. */
+/* embed [V, d] row-major (rows are gathered); final_norm [d]; lm_head [V, d]
+ * packed by hs_pack_matrix.  lm_head == NULL declares a layer stack without a
+ * head: decode then produces no tokens or logits. */
 typedef struct hs_weights {
   const void *embed;
   const void *final_norm;
@@ -114,6 +116,20 @@ const char *hs_last_error(void);
  * s_text = capacity - n_v it is also the size hs_kv_alloc lays out for one
  * request.  Pure host arithmetic; either output pointer may be NULL. */
 int hs_kv_bytes(const hs_config *cfg, int64_t n_v, int64_t s_text, uint64_t *kv_bytes, uint64_t *emb_bytes);
+
+/* Packed weight layout.  Decode streams every weight byte once per token, so
+ * each projection matrix is stored in the order the GEMM reads it: the
+ * row-major [rows, cols] matrix is cut into tiles of 16 rows; a tile is a
+ * sequence of k-blocks of 256 bytes per row (128 elements for 16-bit dtypes,
+ * 64 for fp32); k-block kb of tile t is four 1 KB sub-blocks s, and 16-byte
+ * slot l = 16 * q + i of sub-block s holds the 16-byte chunk
+ * c = 16 * kb + 4 * s + q of row 16 * t + i.  Rows past `rows` and chunks past
+ * `cols` are zero.  cols must be a multiple of 8 (16-bit) or 4 (fp32).
+ * hs_packed_bytes gives the size; hs_pack_matrix converts src (row-major,
+ * device) into dst (device, hs_packed_bytes long, 16-byte aligned),
+ * asynchronously on the stream. */
+int hs_packed_bytes(int32_t dtype, int64_t rows, int64_t cols, uint64_t *bytes);
+int hs_pack_matrix(int32_t dtype, const void *src, int64_t rows, int64_t cols, void *dst, hs_stream_t stream);
 
 /* Validates cfg, records the caller-owned weight pointers (they must outlive
  * the model) and allocates the workspaces for decode batches of up to

@@ -9,8 +9,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhs.so")
-SOURCES = [os.path.join(CSRC, "hs_api.cpp"), os.path.join(CSRC, "hs_kernels.hip")]
-DEPS = SOURCES + [os.path.join(CSRC, "hs_internal.h"), os.path.join(ROOT, "include", "hs.h")]
+SOURCES = [os.path.join(CSRC, f) for f in ("hs_api.cpp", "hs_gemm.hip", "hs_attn.hip", "hs_misc.hip")]
+DEPS = SOURCES + [os.path.join(CSRC, "hs_internal.h"), os.path.join(CSRC, "hs_device.h"),
+                  os.path.join(ROOT, "include", "hs.h")]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -31,14 +32,17 @@ def hipcc() -> str:
 def build(verbose: bool = False) -> str:
     """Compiles libhs.so; always recompiles."""
     tmp = LIB + ".tmp"
-    objs = []
+    objs, procs = [], []
     for src in SOURCES:
         obj = os.path.join(CSRC, os.path.basename(src) + ".o")
         cmd = [hipcc()] + [f for f in FLAGS if f != "-shared"] + ["-c", "-x", "hip", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.check_call(cmd)
+        procs.append((subprocess.Popen(cmd), cmd))
         objs.append(obj)
+    for p, cmd in procs:
+        if p.wait() != 0:
+            raise subprocess.CalledProcessError(p.returncode, cmd)
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)

@@ -154,7 +154,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
-    HIP_TRY(timed(m, HS_K_QKV, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, (nh + 2 * nkv) * hd / 32, st); }));
+    HIP_TRY(timed(m, HS_K_QKV, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, st); }));
 
     AttnArgs a{};
     a.q = m->q;
@@ -184,7 +184,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     o.x = m->attn;
     o.resid = m->x;
     o.ld_resid = d;
-    HIP_TRY(timed(m, HS_K_OPROJ, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, (d + 15) / 16, st); }));
+    HIP_TRY(timed(m, HS_K_OPROJ, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st); }));
 
     GemmArgs u{};
     u.w[0] = W.w_gate;
@@ -197,7 +197,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     u.eps = c.rms_eps;
     u.out = m->act;
     u.ld_out = F;
-    HIP_TRY(timed(m, HS_K_GATEUP, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, (F + 15) / 16, st); }));
+    HIP_TRY(timed(m, HS_K_GATEUP, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, st); }));
 
     GemmArgs dn{};
     dn.w[0] = W.w_down;
@@ -207,7 +207,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     dn.x = m->act;
     dn.resid = m->x;
     dn.ld_resid = d;
-    HIP_TRY(timed(m, HS_K_DOWN, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, (d + 15) / 16, st); }));
+    HIP_TRY(timed(m, HS_K_DOWN, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, st); }));
   }
   return HS_OK;
 }
@@ -225,7 +225,7 @@ int run_head(hs_model *m, const float *x_rows, int ncols, float *logits, hipStre
   g.eps = c.rms_eps;
   g.out = logits;
   g.ld_out = c.vocab;
-  HIP_TRY(timed(m, HS_K_HEAD, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, (c.vocab + 31) / 32, st); }));
+  HIP_TRY(timed(m, HS_K_HEAD, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, st); }));
   return HS_OK;
 }
 
@@ -248,6 +248,25 @@ int hs_kv_bytes(const hs_config *cfg, int64_t n_v, int64_t s_text, uint64_t *kv_
     return fail(HS_E_INVALID, "hs_kv_bytes: size overflows 64 bits");
   if (kv_bytes) *kv_bytes = kv;
   if (emb_bytes) *emb_bytes = emb;
+  return HS_OK;
+}
+
+int hs_packed_bytes(int32_t dtype, int64_t rows, int64_t cols, uint64_t *bytes) {
+  if (!bytes || dtype < HS_F32 || dtype > HS_BF16 || rows <= 0 || cols <= 0)
+    return fail(HS_E_INVALID, "hs_packed_bytes: bad argument");
+  if (cols % (16 / dtype_bytes(dtype))) return fail(HS_E_INVALID, "hs_packed_bytes: cols must fill 16-byte chunks");
+  *bytes = (uint64_t)packed_elems(dtype, rows, cols) * dtype_bytes(dtype);
+  return HS_OK;
+}
+
+int hs_pack_matrix(int32_t dtype, const void *src, int64_t rows, int64_t cols, void *dst, hs_stream_t stream) {
+  uint64_t bytes;
+  int rc = hs_packed_bytes(dtype, rows, cols, &bytes);
+  if (rc) return rc;
+  if (!src || !dst || ((uintptr_t)src | (uintptr_t)dst) % 16)
+    return fail(HS_E_INVALID, "hs_pack_matrix: NULL or misaligned pointer");
+  if (cols > INT32_MAX) return fail(HS_E_INVALID, "hs_pack_matrix: cols too large");
+  HIP_TRY(launch_pack(dtype, src, rows, cols, dst, (hipStream_t)stream));
   return HS_OK;
 }
 

@@ -1,0 +1,172 @@
+// hs_device.h — device-side helpers shared by the gfx950 kernels of libhs:
+// storage dtypes and their round-to-nearest-even conversions, 16-byte chunk
+// (un)packing, the MFMA tile update and DPP/shuffle reductions.
+#pragma once
+
+#include "hs_internal.h"
+
+#include <cmath>
+
+// every launch carries the timing hook's events (null when untimed)
+#define HS_LAUNCH(kernel, grid, block, shmem, stream, ...)                                                        \
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, hs::g_launch_events.start, hs::g_launch_events.stop, \
+                        0, __VA_ARGS__)
+
+namespace hs {
+namespace dev {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// ---------------------------------------------------------------------------
+// storage dtypes
+// ---------------------------------------------------------------------------
+template <int DT>
+struct Ty;
+template <>
+struct Ty<HS_F32> {
+  using S = float;
+  static constexpr int CE = 4;  // elements per 16-byte chunk
+};
+template <>
+struct Ty<HS_F16> {
+  using S = uint16_t;
+  static constexpr int CE = 8;
+};
+template <>
+struct Ty<HS_BF16> {
+  using S = uint16_t;
+  static constexpr int CE = 8;
+};
+
+__device__ __forceinline__ float f16_to_f32(uint32_t u) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)u);
+}
+__device__ __forceinline__ uint32_t f32_to_f16(float f) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);  // v_cvt_f16_f32, round to nearest even
+}
+__device__ __forceinline__ float bf16_to_f32(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x7FFFFFu)) return (u >> 16) | 0x40u;
+  u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest even
+  return u >> 16;
+}
+
+template <int DT>
+__device__ __forceinline__ float ld_elem(const void *p, int64_t i) {
+  if constexpr (DT == HS_F32) return ((const float *)p)[i];
+  else if constexpr (DT == HS_F16) return f16_to_f32(((const uint16_t *)p)[i]);
+  else return bf16_to_f32(((const uint16_t *)p)[i]);
+}
+
+// R(.): store an fp32 value in the storage dtype
+template <int DT>
+__device__ __forceinline__ void st_elem(void *p, int64_t i, float v) {
+  if constexpr (DT == HS_F32) ((float *)p)[i] = v;
+  else if constexpr (DT == HS_F16) ((uint16_t *)p)[i] = (uint16_t)f32_to_f16(v);
+  else ((uint16_t *)p)[i] = (uint16_t)f32_to_bf16(v);
+}
+
+// 16-byte chunk -> CE floats
+template <int DT>
+__device__ __forceinline__ void unpack(u32x4 w, float *f) {
+  if constexpr (DT == HS_F32) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(w[e]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (DT == HS_F16) {
+        f[2 * e] = f16_to_f32(w[e] & 0xFFFFu);
+        f[2 * e + 1] = f16_to_f32(w[e] >> 16);
+      } else {
+        f[2 * e] = bf16_to_f32(w[e] & 0xFFFFu);
+        f[2 * e + 1] = bf16_to_f32(w[e] >> 16);
+      }
+    }
+  }
+}
+
+// CE floats -> 16-byte chunk, rounding to the storage dtype
+template <int DT>
+__device__ __forceinline__ u32x4 pack(const float *f) {
+  u32x4 w;
+  if constexpr (DT == HS_F32) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = __float_as_uint(f[e]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (DT == HS_F16) w[e] = f32_to_f16(f[2 * e]) | (f32_to_f16(f[2 * e + 1]) << 16);
+      else w[e] = f32_to_bf16(f[2 * e]) | (f32_to_bf16(f[2 * e + 1]) << 16);
+    }
+  }
+  return w;
+}
+
+// One 16x16 output tile += A(16 x k) * B(k x 16) over the k values held in a
+// 16-byte chunk per lane.  Lane l supplies row (A) / column (B) l % 16 and the
+// k sub-range of lane group l / 16; A and B use the same k mapping, so the
+// order of k inside the contraction is immaterial.
+template <int DT>
+__device__ __forceinline__ f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+  if constexpr (DT == HS_F16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
+  } else if constexpr (DT == HS_BF16) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  } else {
+    f32x4 av = __builtin_bit_cast(f32x4, a), bv = __builtin_bit_cast(f32x4, b);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bv[e], c, 0, 0, 0);
+    return c;
+  }
+}
+
+__device__ __forceinline__ u32x4 ld16(const void *p) { return *(const u32x4 *)p; }
+__device__ __forceinline__ u32x4 ld16_stream(const void *p) {
+  return __builtin_nontemporal_load((const u32x4 *)p);
+}
+
+// ---------------------------------------------------------------------------
+// cross-lane reductions (DPP within 16-lane rows, then across rows)
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int DPP_QUAD_1032 = 0xB1;    // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_2301 = 0x4E;    // quad_perm [2,3,0,1]
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
+constexpr int DPP_ROW_MIRROR = 0x140;
+
+// sum over aligned groups of N lanes (N = 8, 16, 32, 64); every lane gets it
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  v += dpp<DPP_QUAD_1032>(v);
+  v += dpp<DPP_QUAD_2301>(v);
+  v += dpp<DPP_ROW_HALF_MIRROR>(v);
+  if constexpr (N >= 16) v += dpp<DPP_ROW_MIRROR>(v);
+  if constexpr (N >= 32) v += __shfl_xor(v, 16);
+  if constexpr (N >= 64) v += __shfl_xor(v, 32);
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) { return group_sum<64>(v); }
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp<DPP_QUAD_1032>(v));
+  v = fmaxf(v, dpp<DPP_QUAD_2301>(v));
+  v = fmaxf(v, dpp<DPP_ROW_HALF_MIRROR>(v));
+  v = fmaxf(v, dpp<DPP_ROW_MIRROR>(v));
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+
+
+}  // namespace dev
+}  // namespace hs

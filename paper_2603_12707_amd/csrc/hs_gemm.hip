@@ -1,0 +1,406 @@
+// hs_gemm.hip — weight-streaming MFMA GEMM of the decode step (gfx950) and the
+// packing of weight matrices into the layout it streams.
+//
+// Decode reads every weight byte once per generated token (§2; Eq. 5 of §4.3
+// models decode time as the streamed weight bytes over HBM bandwidth), so the
+// GEMM is organised as one sequential pass over a packed copy of each matrix:
+// a 16-row x 256-byte tile slice is stored as 1 KB in MFMA lane order, so that
+// every wave-wide load instruction reads 1 KB of contiguous HBM.
+#include "hs_device.h"
+
+namespace hs {
+namespace {
+
+using namespace dev;
+
+// ---------------------------------------------------------------------------
+// packed layout
+// ---------------------------------------------------------------------------
+// A row-major [N, K] matrix becomes tiles of 16 rows; each tile is a sequence
+// of k-blocks of 16 chunks (16 x CE elements, 256 bytes per row); k-block kb
+// of tile t is four 1 KB sub-blocks s, and lane l = 16 * lq + li of sub-block
+// s holds the 16-byte chunk kc = 16 * kb + 4 * s + lq of row 16 * t + li.
+// Rows past N and chunks past K are zero.
+template <int DT>
+__global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_t N, int K, int nkb,
+                                              int64_t total) {
+  constexpr int CE = Ty<DT>::CE;
+  using S = typename Ty<DT>::S;
+  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int lane = (int)(i & 63), s = (int)((i >> 6) & 3);
+    const int64_t rest = i >> 8;
+    const int kb = (int)(rest % nkb);
+    const int64_t tile = rest / nkb;
+    const int64_t row = tile * 16 + (lane & 15);
+    const int kc = kb * 16 + s * 4 + (lane >> 4);
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (row < N && (int64_t)kc * CE < K) v = ld16((const S *)src + row * K + (int64_t)kc * CE);
+    *(u32x4 *)((S *)dst + i * CE) = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// row tiles
+// ---------------------------------------------------------------------------
+// The q/k/v epilogue pairs rows i and i + d_h/2 of one head (the two halves
+// RoPE rotates together); SwiGLU pairs row j of the gate and of the up
+// projection; the other epilogues take R consecutive tiles.
+template <int EPI, int R>
+__device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int *row0) {
+  if constexpr (EPI == EPI_QKV) {
+    const int hd = a.head_dim, gph = hd / 32;
+    int m = 0, rem = g;
+    if (rem >= a.n_heads * gph) {
+      rem -= a.n_heads * gph;
+      m = 1;
+      if (rem >= a.n_kv * gph) {
+        rem -= a.n_kv * gph;
+        m = 2;
+      }
+    }
+    const int head = rem / gph, i0 = (rem % gph) * 16;
+    mat[0] = mat[1] = m;
+    row0[0] = head * hd + i0;
+    row0[1] = head * hd + i0 + hd / 2;
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    mat[0] = 0;
+    mat[1] = 1;
+    row0[0] = row0[1] = 16 * g;
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      mat[r] = 0;
+      row0[r] = 16 * (R * g + r);
+    }
+  }
+}
+
+template <int DT, int EPI, int R>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat, const int *row0, const f32x4 *v,
+                                              int col, int rr) {
+  constexpr int B = DT == HS_F32 ? 4 : 2;
+  if constexpr (EPI == EPI_STORE) {
+    float *o = (float *)a.out + (int64_t)col * a.ld_out;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = row0[r] + rr + e;
+        if (row < a.rows[mat[r]]) o[row] = v[r][e];
+      }
+  } else if constexpr (EPI == EPI_RESID) {
+    float *x = a.resid + (int64_t)col * a.ld_resid;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = row0[r] + rr + e;
+        if (row < a.rows[mat[r]]) x[row] += v[r][e];
+      }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    void *o = (char *)a.out + (int64_t)col * a.ld_out * B;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j = row0[0] + rr + e;
+      if (j < a.rows[0]) {
+        const float g = v[0][e], u = v[1][e];
+        st_elem<DT>(o, j, g / (1.0f + expf(-g)) * u);
+      }
+    }
+  } else {  // EPI_QKV
+    const int m = mat[0], hd = a.head_dim, half = hd >> 1;
+    const int head = row0[0] / hd, i0 = row0[0] - head * hd;
+    int req, pos;
+    if (a.prefill_req < 0) {
+      req = col;
+      pos = a.kv_len[col];
+    } else {
+      req = a.prefill_req;
+      pos = col;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = i0 + rr + e;  // frequency pair, < d_h / 2
+      float v1 = v[0][e], v2 = v[1][e];
+      if (a.bias[m]) {
+        v1 += ld_elem<DT>(a.bias[m], head * hd + i);
+        v2 += ld_elem<DT>(a.bias[m], head * hd + i + half);
+      }
+      float o1 = v1, o2 = v2;
+      if (m < 2) {
+        int p;
+        if (a.prefill_req < 0) p = a.rope_pos[col];
+        else if (!a.rope_m3) p = col;
+        else p = a.rope_pos[(i < a.sec0 ? 0 : (i < a.sec1 ? 1 : 2)) * a.ncols + col];
+        p = min(max(p, 0), a.rope_max - 1);
+        const float cs = a.rope_tab[((int64_t)p * half + i) * 2], sn = a.rope_tab[((int64_t)p * half + i) * 2 + 1];
+        o1 = v1 * cs - v2 * sn;
+        o2 = v2 * cs + v1 * sn;
+      }
+      if (m == 0) {
+        void *q = (char *)a.out + ((int64_t)col * a.ld_out + head * hd) * B;
+        st_elem<DT>(q, i, o1);
+        st_elem<DT>(q, i + half, o2);
+      } else {
+        const int cap = a.kv_cap[req];
+        if (pos < cap) {
+          const int64_t off =
+              a.kv_base[req] + ((int64_t)((a.layer * 2 + (m == 2 ? 1 : 0)) * a.n_kv + head) * cap + pos) * hd;
+          st_elem<DT>(a.kv, off + i, o1);
+          st_elem<DT>(a.kv, off + i + half, o2);
+        }
+      }
+    }
+  }
+}
+
+// Sum over the 64 * NW threads of a work group; every thread gets it.
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float *s_part) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) s_part[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) t += s_part[w];
+  return t;
+}
+
+// Y[c][n] = sum_k X[c][k] W[n][k] over R row tiles and NT column tiles of 16.
+//
+// The NW waves of a work group split the packed k-blocks round robin, so that
+// together they read consecutive kilobytes; each wave keeps U k-blocks of
+// loads in flight (non-temporal: every weight byte is read once per step).
+// X comes from the activation rows in global memory (L2-resident), from the
+// fp32 residual stream normalised on the fly (PRO_NORM, XS = 0), or, when the
+// work group's columns are few (XS = 1), from a copy normalised once into LDS.
+// The waves' partial tiles are summed in a fixed order through LDS and handed
+// to the epilogue.
+template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
+__global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
+  using S = typename Ty<DT>::S;
+  constexpr int CE = Ty<DT>::CE;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 15, lq = lane >> 4;
+  const int col0 = blockIdx.y * 16 * NT;
+  const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4;
+
+  int mat[R], row0[R];
+  tile_map<EPI, R>(a, blockIdx.x, mat, row0);
+  const S *wp[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    wp[r] = row0[r] < a.rows[mat[r]] ? (const S *)a.w[mat[r]] + ((int64_t)(row0[r] >> 4) * nkb * 256 + lane) * CE
+                                     : nullptr;
+
+  __shared__ float s_rsq[16 * NT];
+  __shared__ float s_part[NW];
+  extern __shared__ __align__(16) unsigned char s_x[];  // XS: normalised activations [nst][K]
+  const int nst = min(a.ncols - col0, 16 * NT);
+  if constexpr (PRO == PRO_NORM && XS == 1) {
+    const float *x = (const float *)a.x;
+    for (int c = 0; c < nst; ++c) {
+      const float *xr = x + (int64_t)(col0 + c) * K;
+      float ss = 0.f;
+      for (int k = threadIdx.x * 4; k < K; k += 256 * NW) {
+        const f32x4 v = *(const f32x4 *)(xr + k);
+        ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+      }
+      const float rs = 1.0f / sqrtf(block_sum<NW>(ss, s_part) / (float)K + a.eps);
+      for (int k = threadIdx.x * 4; k < K; k += 256 * NW) {
+        const f32x4 v = *(const f32x4 *)(xr + k);
+        float h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) h[e] = v[e] * rs * ld_elem<DT>(a.gain, k + e);
+        if constexpr (DT == HS_F32) {
+          *(f32x4 *)((float *)s_x + (int64_t)c * K + k) = f32x4{h[0], h[1], h[2], h[3]};
+        } else {
+          uint32_t w0, w1;
+          if constexpr (DT == HS_F16) {
+            w0 = f32_to_f16(h[0]) | (f32_to_f16(h[1]) << 16);
+            w1 = f32_to_f16(h[2]) | (f32_to_f16(h[3]) << 16);
+          } else {
+            w0 = f32_to_bf16(h[0]) | (f32_to_bf16(h[1]) << 16);
+            w1 = f32_to_bf16(h[2]) | (f32_to_bf16(h[3]) << 16);
+          }
+          uint32_t *dst = (uint32_t *)((uint16_t *)s_x + (int64_t)c * K + k);
+          dst[0] = w0;
+          dst[1] = w1;
+        }
+      }
+    }
+    __syncthreads();
+  } else if constexpr (PRO == PRO_NORM) {
+    const float *x = (const float *)a.x;
+    for (int c = wave; c < 16 * NT; c += NW) {
+      const int col = col0 + c;
+      float ss = 0.f;
+      if (col < a.ncols) {
+        const float *xr = x + (int64_t)col * K;
+        for (int k = lane * 4; k < K; k += 256) {
+          const f32x4 v = *(const f32x4 *)(xr + k);
+          ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+        }
+      }
+      ss = wave_sum(ss);
+      if (lane == 0) s_rsq[c] = 1.0f / sqrtf(ss / (float)K + a.eps);
+    }
+    __syncthreads();
+  }
+
+  auto load_x = [&](int t, int kc) -> u32x4 {
+    const int c = 16 * t + li, col = col0 + c;
+    if (col >= a.ncols || kc >= kchunks) return u32x4{0u, 0u, 0u, 0u};
+    if constexpr (PRO == PRO_PLAIN) {
+      return ld16((const S *)a.x + (int64_t)col * K + (int64_t)kc * CE);
+    } else if constexpr (XS == 1) {
+      return *(const u32x4 *)((const S *)s_x + (int64_t)c * K + (int64_t)kc * CE);
+    } else {
+      const float *xr = (const float *)a.x + (int64_t)col * K + (int64_t)kc * CE;
+      const float rs = s_rsq[c];
+      float xv[CE], gv[CE], h[CE];
+      unpack<HS_F32>(ld16(xr), xv);
+      if constexpr (CE == 8) unpack<HS_F32>(ld16(xr + 4), xv + 4);
+      unpack<DT>(ld16((const S *)a.gain + (int64_t)kc * CE), gv);
+#pragma unroll
+      for (int e = 0; e < CE; ++e) h[e] = xv[e] * rs * gv[e];
+      return pack<DT>(h);
+    }
+  };
+
+  f32x4 acc[R][NT];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kb0 = wave; kb0 < nkb; kb0 += NW * U) {
+    u32x4 wa[U][R][4], xb[U][NT][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = kb0 + u * NW;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          wa[u][r][s] = (wp[r] && kb < nkb) ? ld16_stream(wp[r] + (int64_t)(kb * 4 + s) * 64 * CE)
+                                            : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) xb[u][t][s] = load_x(t, (kb0 + u * NW) * 16 + s * 4 + lq);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(wa[u][r][s], xb[u][t][s], acc[r][t]);
+  }
+
+  __shared__ f32x4 s_red[NW][R][NT][64];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) s_red[wave][r][t][lane] = acc[r][t];
+  __syncthreads();
+  for (int item = threadIdx.x; item < NT * 64; item += 64 * NW) {
+    const int t = item >> 6, ln = item & 63;
+    f32x4 v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      v[r] = s_red[0][r][t][ln];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) v[r] += s_red[w][r][t][ln];
+    }
+    const int col = col0 + 16 * t + (ln & 15);
+    if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launch shapes
+// ---------------------------------------------------------------------------
+constexpr int XS_MAX_BYTES = 32 * 1024;  // LDS for normalised activations
+
+template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
+hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_t st) {
+  const dim3 grid(n_groups, (a.ncols + 16 * NT - 1) / (16 * NT));
+  HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI>), grid, dim3(64 * NW), shmem, st, a);
+  return hipGetLastError();
+}
+
+// Launch shape per epilogue: the paired-tile epilogues (q/k/v, SwiGLU) and
+// the LM head take 4 waves; the residual projections, whose matrices have
+// few row tiles, take 8 waves per tile so that enough loads are in flight.
+template <int DT, int PRO, int EPI>
+hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
+  constexpr int R = (EPI == EPI_QKV || EPI == EPI_SWIGLU) ? 2 : 1;
+  constexpr int NW = EPI == EPI_RESID ? 8 : 4;
+  // one work group per R row tiles (q/k/v: per pair of RoPE half-tiles)
+  const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 32
+                                      : (a.rows[0] + 16 * (EPI == EPI_SWIGLU ? 1 : R) - 1) /
+                                            (16 * (EPI == EPI_SWIGLU ? 1 : R));
+  const int tiles = (a.ncols + 15) / 16;
+  const int b = DT == HS_F32 ? 4 : 2;
+  if (tiles <= 1) {
+    if constexpr (PRO == PRO_NORM) {
+      const size_t xs = (size_t)a.ncols * a.K * b;
+      if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, 4, PRO, 1, EPI>(a, n_groups, xs, st);
+    }
+    if (EPI == EPI_RESID && a.K > 4096) return gemm_launch<DT, R, 1, NW, 2, PRO, 0, EPI>(a, n_groups, 0, st);
+    return gemm_launch<DT, R, 1, NW, 4, PRO, 0, EPI>(a, n_groups, 0, st);
+  }
+  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 2, PRO, 0, EPI>(a, n_groups, 0, st);
+  return gemm_launch<DT, R, 4, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
+}
+
+template <int DT>
+hipError_t gemm_dt(int pro, int epi, const GemmArgs &a, hipStream_t st) {
+  if (pro == PRO_NORM && epi == EPI_QKV) return gemm_shape<DT, PRO_NORM, EPI_QKV>(a, st);
+  if (pro == PRO_NORM && epi == EPI_SWIGLU) return gemm_shape<DT, PRO_NORM, EPI_SWIGLU>(a, st);
+  if (pro == PRO_NORM && epi == EPI_STORE) return gemm_shape<DT, PRO_NORM, EPI_STORE>(a, st);
+  if (pro == PRO_PLAIN && epi == EPI_RESID) return gemm_shape<DT, PRO_PLAIN, EPI_RESID>(a, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st) {
+  if (a.ncols <= 0 || a.rows[0] <= 0) return hipSuccess;
+  switch (dtype) {
+    case HS_F32: return gemm_dt<HS_F32>(pro, epi, a, st);
+    case HS_F16: return gemm_dt<HS_F16>(pro, epi, a, st);
+    case HS_BF16: return gemm_dt<HS_BF16>(pro, epi, a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+int64_t packed_elems(int dtype, int64_t rows, int64_t cols) {
+  const int ce = dtype == HS_F32 ? 4 : 8;
+  const int64_t nkb = (cols / ce + 15) / 16;
+  return ((rows + 15) / 16) * nkb * 256 * ce;
+}
+
+hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, hipStream_t st) {
+  const int ce = dtype == HS_F32 ? 4 : 8;
+  const int nkb = (int)((cols / ce + 15) / 16);
+  const int64_t total = ((rows + 15) / 16) * nkb * 256;
+  if (total <= 0) return hipSuccess;
+  const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
+  switch (dtype) {
+    case HS_F32: HS_LAUNCH(k_pack<HS_F32>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
+    case HS_F16: HS_LAUNCH(k_pack<HS_F16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
+    case HS_BF16: HS_LAUNCH(k_pack<HS_BF16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace hs

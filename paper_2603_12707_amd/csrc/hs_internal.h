@@ -80,7 +80,9 @@ struct LaunchEvents {
 };
 extern thread_local LaunchEvents g_launch_events;
 
-hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, int n_groups, hipStream_t st);
+hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st);
+hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, hipStream_t st);
+int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
 hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);
 hipError_t launch_combine(int dtype, int head_dim, int nq, const AttnArgs &a, hipStream_t st);
 hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x,

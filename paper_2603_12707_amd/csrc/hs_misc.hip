@@ -1,0 +1,162 @@
+// hs_misc.hip — embedding gather, prefill input rows, greedy selection and
+// length bookkeeping kernels of the decode engine (gfx950).
+#include "hs_device.h"
+
+namespace hs {
+
+thread_local LaunchEvents g_launch_events;
+
+namespace {
+
+using namespace dev;
+
+// ---------------------------------------------------------------------------
+// embeddings, selection, bookkeeping
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void k_embed(const void *E, int V, int d, const int *tok, float *x, int *status) {
+  const int b = blockIdx.x;
+  int t = tok[b];
+  if (t < 0 || t >= V) {
+    if (threadIdx.x == 0) atomicOr(status, 1);
+    t = 0;
+  }
+  for (int k = threadIdx.x; k < d; k += 256) x[(int64_t)b * d + k] = ld_elem<DT>(E, (int64_t)t * d + k);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_prefill_rows(const void *emb, int n_v, const void *E, int V, int d,
+                                                      const int *ids, float *x, int *status) {
+  const int r = blockIdx.x;
+  const void *src;
+  int64_t row;
+  if (r < n_v) {
+    src = emb;
+    row = r;
+  } else {
+    int t = ids[r - n_v];
+    if (t < 0 || t >= V) {
+      if (threadIdx.x == 0) atomicOr(status, 1);
+      t = 0;
+    }
+    src = E;
+    row = t;
+  }
+  for (int k = threadIdx.x; k < d; k += 256) x[(int64_t)r * d + k] = ld_elem<DT>(src, row * d + k);
+}
+
+// Greedy selection: largest logit, lowest index among equals (NaN never wins).
+__global__ __launch_bounds__(1024) void k_argmax(const float *logits, int V, int ld, int *out, int *len, int *rope,
+                                                 int advance) {
+  const int b = blockIdx.x;
+  const float *lg = logits + (int64_t)b * ld;
+  float bv = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int i = threadIdx.x; i < V; i += 1024) {
+    const float v = lg[i];
+    if (v > bv) {
+      bv = v;
+      bi = i;
+    }
+  }
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(bv, off);
+    const int oi = __shfl_xor(bi, off);
+    if (ov > bv || (ov == bv && oi < bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  __shared__ float s_v[16];
+  __shared__ int s_i[16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    s_v[wave] = bv;
+    s_i[wave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < 16; ++w)
+      if (s_v[w] > bv || (s_v[w] == bv && s_i[w] < bi)) {
+        bv = s_v[w];
+        bi = s_i[w];
+      }
+    out[b] = bi == 0x7FFFFFFF ? 0 : bi;
+    if (advance) {
+      len[b] += 1;
+      rope[b] += 1;
+    }
+  }
+}
+
+__global__ void k_advance(int *len, int *rope, int n) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < n) {
+    len[b] += 1;
+    rope[b] += 1;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int req, int s_ctx, const int *pos_thw) {
+  int mx = s_ctx - 1;
+  if (pos_thw) {
+    mx = 0x80000000;
+    for (int i = threadIdx.x; i < 3 * s_ctx; i += 256) mx = max(mx, pos_thw[i]);
+    for (int off = 32; off >= 1; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+    __shared__ int s_mx[4];
+    if ((threadIdx.x & 63) == 0) s_mx[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    mx = max(max(s_mx[0], s_mx[1]), max(s_mx[2], s_mx[3]));
+  }
+  if (threadIdx.x == 0) {
+    len[req] = s_ctx;
+    rope[req] = mx + 1;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x, int *status,
+                        hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  switch (dtype) {
+    case HS_F32: HS_LAUNCH(k_embed<HS_F32>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_F16: HS_LAUNCH(k_embed<HS_F16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_BF16: HS_LAUNCH(k_embed<HS_BF16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *embed, int vocab, int d,
+                               const int *ids, int s_text, float *x, int *status, hipStream_t st) {
+  const int rows = n_v + s_text;
+  if (rows <= 0) return hipSuccess;
+  switch (dtype) {
+    case HS_F32: HS_LAUNCH(k_prefill_rows<HS_F32>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    case HS_F16: HS_LAUNCH(k_prefill_rows<HS_F16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    case HS_BF16: HS_LAUNCH(k_prefill_rows<HS_BF16>, dim3(rows), dim3(256), 0, st, emb, n_v, embed, vocab, d, ids, x, status); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
+                         int advance, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  HS_LAUNCH(k_argmax, dim3(n), dim3(1024), 0, st, logits, vocab, ld, tokens_out, len, rope_pos, advance);
+  return hipGetLastError();
+}
+
+hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  HS_LAUNCH(k_advance, dim3((n + 255) / 256), dim3(256), 0, st, len, rope_pos, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, hipStream_t st) {
+  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw);
+  return hipGetLastError();
+}
+
+}  // namespace hs

@@ -20,7 +20,11 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length", "hs_model_set_timing", "hs_model_timing")
+           "hs_kv_read", "hs_kv_set_length", "hs_model_set_timing", "hs_model_timing", "hs_packed_bytes",
+           "hs_pack_matrix")
+
+# projection matrices the library reads in its packed layout
+PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
 
 HS_K_NAMES = ("embed", "qkv", "attn", "combine", "oproj", "gateup", "down", "head", "argmax")
 
@@ -82,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "hs_kv_read": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_set_length": [P, I32, I32, I32],
         "hs_model_set_timing": [P, I32, I32],
+        "hs_packed_bytes": [I32, I64, I64, ctypes.POINTER(U64)],
+        "hs_pack_matrix": [I32, P, I64, I64, P, P],
         "hs_model_timing": [P, I32, P, P, P],
     }
     for name, args in sig.items():
@@ -128,12 +134,55 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-class Model:
-    """A model over caller-owned device weight tensors named as in the
-    workload generator (embed, layers.{i}.wq, ..., final_norm, lm_head)."""
+_DT = {"f32": HS_F32, "f16": HS_F16, "bf16": HS_BF16}
 
-    def __init__(self, cfg: dict, weights: dict, max_batch: int, max_ctx: int):
+
+def _is_packed(name: str) -> bool:
+    return name.split(".")[-1] in PACKED
+
+
+def hs_packed_bytes(dtype: str, rows: int, cols: int) -> int:
+    out = ctypes.c_uint64()
+    _call("hs_packed_bytes", _DT[dtype], rows, cols, ctypes.byref(out))
+    return out.value
+
+
+def pack_matrix(t, dtype: str):
+    """Packed copy (uint8 device tensor) of a row-major [rows, cols] device
+    matrix, written by hs_pack_matrix on the current stream."""
+    import torch
+    assert t.is_cuda and t.dim() == 2 and t.is_contiguous()
+    rows, cols = t.shape
+    out = torch.empty(hs_packed_bytes(dtype, rows, cols), dtype=torch.uint8, device=t.device)
+    _call("hs_pack_matrix", _DT[dtype], _ptr(t), rows, cols, _ptr(out), _stream())
+    return out
+
+
+def pack_weights(cfg: dict, weights: dict, free_source: bool = False) -> dict:
+    """Returns the weight dict with every projection matrix packed; vectors
+    and the embedding table pass through.  With free_source the row-major
+    matrices are removed from `weights` as they are packed."""
+    out = {}
+    for name in list(weights):
+        if _is_packed(name):
+            out[name] = pack_matrix(weights[name], cfg["dtype"])
+            if free_source:
+                del weights[name]
+        else:
+            out[name] = weights[name]
+    return out
+
+
+class Model:
+    """A model over device weight tensors named as in the workload generator
+    (embed, layers.{i}.wq, ..., final_norm, lm_head).  Row-major projection
+    matrices are packed on construction unless packed=True says they already
+    are."""
+
+    def __init__(self, cfg: dict, weights: dict, max_batch: int, max_ctx: int, packed: bool = False):
         self.cfg = cfg
+        if not packed:
+            weights = pack_weights(cfg, weights)
         self._w = weights  # keeps the tensors alive
         L = cfg["n_layers"]
         self._layers = (hs_layer_weights * L)()
