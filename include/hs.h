@@ -193,7 +193,7 @@ int hs_model_status(hs_model *m, int32_t *flags);
 #define HS_K_EMBED 0   /* token embedding gather */
 #define HS_K_QKV 1     /* RMSNorm + q/k/v projection + RoPE + KV append */
 #define HS_K_ATTN 2    /* split-K attention over the KV cache */
-#define HS_K_COMBINE 3 /* split combine */
+#define HS_K_COMBINE 3 /* combine of the attention splits */
 #define HS_K_OPROJ 4   /* output projection + residual */
 #define HS_K_GATEUP 5  /* RMSNorm + gate/up projection + SwiGLU */
 #define HS_K_DOWN 6    /* down projection + residual */

@@ -34,6 +34,7 @@ int fail(int code, const char *fmt, ...) {
 int dtype_bytes(int dt) { return dt == HS_F32 ? 4 : 2; }
 
 // Runs one launcher, attaching a timing event pair when its kind is timed.
+// Every launcher passed here launches exactly one kernel.
 template <typename F>
 hipError_t timed(hs_model *m, int kind, F &&launch) {
   const bool on = (m->timing_mask >> kind) & 1;
@@ -90,15 +91,20 @@ int check_config(const hs_config *c) {
   return HS_OK;
 }
 
-// Positions per attention split: the smallest power of two >= s_min that
-// keeps (queries x KV heads x splits) within a few thousand work groups.
-void split_policy(int nq, int n_kv, int max_len, int s_min, int *S, int *n_split) {
-  int s = s_min;
-  while (s < ATTN_SMAX && (int64_t)nq * n_kv * ((max_len + s - 1) / s) > 8192) s *= 2;
+// Attention splits: one work group per (query, KV head) covers all positions
+// unless there are too few such pairs to give every CU a work group; then the
+// positions are cut into up to that many splits of at least ATTN_MIN_SPLIT
+// positions each (S, the positions per split, is a multiple of 64).
+void split_policy(int nq, int n_kv, int max_len, int *S, int *n_split) {
+  const int64_t pairs = (int64_t)nq * n_kv;
+  const int want = (int)std::max<int64_t>(1, (256 + pairs - 1) / pairs);
+  const int most = std::max(1, max_len / ATTN_MIN_SPLIT);
+  int ns = std::min(std::min(want, most), ATTN_MAX_SPLITS);
+  int s = (max_len + ns - 1) / ns;
+  s = (s + 63) / 64 * 64;
   *S = s;
-  *n_split = std::max(1, (max_len + s - 1) / s);
+  *n_split = (max_len + s - 1) / s;
 }
-constexpr int PREFILL_SMIN = 256;
 
 int64_t kv_request_elems(const hs_config &c, int cap) {
   return 2ll * c.n_layers * c.n_kv_heads * (int64_t)c.head_dim * cap;
@@ -174,7 +180,7 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     a.scale = (float)(1.0 / std::sqrt((double)hd));
     a.out = m->attn;
     HIP_TRY(timed(m, HS_K_ATTN, [&] { return launch_attention(c.dtype, hd, nh / nkv, ncols, a, st); }));
-    HIP_TRY(timed(m, HS_K_COMBINE, [&] { return launch_combine(c.dtype, hd, ncols, a, st); }));
+    if (n_split > 1) HIP_TRY(timed(m, HS_K_COMBINE, [&] { return launch_combine(c.dtype, hd, ncols, a, st); }));
 
     GemmArgs o{};
     o.w[0] = W.wo;
@@ -276,6 +282,8 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   int rc = check_config(cfg);
   if (rc) return rc;
   if (!w || !w->embed || !w->layers) return fail(HS_E_INVALID, "hs_model_create: missing embed/layers");
+  if (((uintptr_t)w->embed | (uintptr_t)w->lm_head) % 16)
+    return fail(HS_E_INVALID, "hs_model_create: embed and lm_head must be 16-byte aligned");
   if (w->lm_head && !w->final_norm) return fail(HS_E_INVALID, "hs_model_create: lm_head without final_norm");
   if (max_batch <= 0 || max_ctx <= 0) return fail(HS_E_INVALID, "hs_model_create: max_batch/max_ctx must be > 0");
   for (int l = 0; l < cfg->n_layers; ++l) {
@@ -306,19 +314,13 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   // <= max_ctx rows, can ask for
   int64_t entries = 0;
   for (int nq = 1; nq <= max_batch; ++nq) {
-    int S, ns, prev_ns = -1, prev_S = -1;
-    for (int len = 1; len <= max_ctx; ++len) {
-      split_policy(nq, c.n_kv_heads, len, ATTN_SMIN, &S, &ns);
-      if (ns == prev_ns && S == prev_S) continue;
-      prev_ns = ns;
-      prev_S = S;
-      entries = std::max(entries, (int64_t)nq * nh * ns);
-    }
-  }
-  for (int r = 1; r <= max_ctx; ++r) {
     int S, ns;
-    split_policy(r, c.n_kv_heads, r, PREFILL_SMIN, &S, &ns);
-    entries = std::max(entries, (int64_t)r * nh * ns);
+    for (int len = 1; len <= max_ctx; len += std::max(1, len / 64)) {
+      split_policy(nq, c.n_kv_heads, len, &S, &ns);
+      if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
+    }
+    split_policy(nq, c.n_kv_heads, max_ctx, &S, &ns);
+    if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
   }
   m->part_entries = entries;
 
@@ -331,8 +333,8 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {&m->attn, (size_t)rows * nh * hd * b},
       {&m->act, (size_t)rows * c.ffn_dim * b},
       {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
-      {(void **)&m->part_o, (size_t)entries * hd * 4},
-      {(void **)&m->part_ml, (size_t)entries * 2 * 4},
+      {(void **)&m->part_o, (size_t)std::max<int64_t>(entries, 1) * hd * 4},
+      {(void **)&m->part_ml, (size_t)std::max<int64_t>(entries, 1) * 2 * 4},
       {(void **)&m->rope_tab, (size_t)max_ctx * (hd / 2) * 2 * 4},
       {(void **)&m->status, 4},
   };
@@ -490,15 +492,14 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
   if (s_ctx <= 0) return fail(HS_E_INVALID, "hs_prefill_embeddings: empty context");
   if ((n_v > 0 && !emb) || (s_text > 0 && !text_ids))
     return fail(HS_E_INVALID, "hs_prefill_embeddings: missing embedding rows or text ids");
+  if (((uintptr_t)emb) % 16) return fail(HS_E_INVALID, "hs_prefill_embeddings: emb must be 16-byte aligned");
   if (c.rope_kind == HS_ROPE_M3 && !pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: M-RoPE needs pos_thw");
   if (c.rope_kind == HS_ROPE_1D && pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: 1-D RoPE takes no pos_thw");
   if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "hs_prefill_embeddings: request %d is not empty", req);
   if (s_ctx > kv->cap[req])
     return fail(HS_E_CAPACITY, "hs_prefill_embeddings: context %d exceeds capacity %d", s_ctx, kv->cap[req]);
-  int S, ns;
-  split_policy(s_ctx, c.n_kv_heads, s_ctx, PREFILL_SMIN, &S, &ns);
-  if ((int64_t)s_ctx * c.n_heads * ns > m->part_entries)
-    return fail(HS_E_INVALID, "hs_prefill_embeddings: attention workspace too small");
+  // prefill: every row is its own query, so one split per (row, KV head)
+  const int S = s_ctx, ns = 1;
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
   int rc = run_layers(m, kv, s_ctx, req, pos_thw, S, ns, st);
@@ -532,8 +533,8 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
       return fail(HS_E_CAPACITY, "hs_decode_step: request %d is full (%d positions)", b, kv->cap[b]);
   }
   int S, ns;
-  split_policy(B, c.n_kv_heads, kv->max_cap, ATTN_SMIN, &S, &ns);
-  if ((int64_t)B * c.n_heads * ns > m->part_entries)
+  split_policy(B, c.n_kv_heads, kv->max_cap, &S, &ns);
+  if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "hs_decode_step: attention workspace too small");
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(timed(m, HS_K_EMBED, [&] { return launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st); }));

@@ -171,8 +171,9 @@ __device__ __forceinline__ float block_sum(float v, float *s_part) {
 // Y[c][n] = sum_k X[c][k] W[n][k] over R row tiles and NT column tiles of 16.
 //
 // The NW waves of a work group split the packed k-blocks round robin, so that
-// together they read consecutive kilobytes; each wave keeps U k-blocks of
-// loads in flight (non-temporal: every weight byte is read once per step).
+// together they read consecutive kilobytes; each wave keeps two groups of U
+// k-blocks of loads in flight (non-temporal: every weight byte is read once
+// per step).
 // X comes from the activation rows in global memory (L2-resident), from the
 // fp32 residual stream normalised on the fly (PRO_NORM, XS = 0), or, when the
 // work group's columns are few (XS = 1), from a copy normalised once into LDS.
@@ -195,22 +196,52 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     wp[r] = row0[r] < a.rows[mat[r]] ? (const S *)a.w[mat[r]] + ((int64_t)(row0[r] >> 4) * nkb * 256 + lane) * CE
                                      : nullptr;
 
+  // weight loads of one group of U k-blocks (k-blocks kb0, kb0 + NW, ...)
+  auto load_w = [&](u32x4 (&wv)[U][R][4], int kb0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = kb0 + u * NW;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          wv[u][r][s] = (wp[r] && kb < nkb) ? ld16_stream(wp[r] + (int64_t)(kb * 4 + s) * 64 * CE)
+                                            : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  // the first group is issued before the prologue so that its HBM latency
+  // overlaps the normalisation of the activations
+  u32x4 wcur[U][R][4], wnxt[U][R][4];
+  load_w(wcur, wave);
+
   __shared__ float s_rsq[16 * NT];
   __shared__ float s_part[NW];
   extern __shared__ __align__(16) unsigned char s_x[];  // XS: normalised activations [nst][K]
   const int nst = min(a.ncols - col0, 16 * NT);
   if constexpr (PRO == PRO_NORM && XS == 1) {
+    // one pass over each staged column: its x values stay in registers
+    // between the sum of squares and the scaling
     const float *x = (const float *)a.x;
+    constexpr int PER = 8;  // float4 per thread and pass (K <= 8 * 4 * 64 * NW)
     for (int c = 0; c < nst; ++c) {
       const float *xr = x + (int64_t)(col0 + c) * K;
+      f32x4 xv[PER];
       float ss = 0.f;
-      for (int k = threadIdx.x * 4; k < K; k += 256 * NW) {
-        const f32x4 v = *(const f32x4 *)(xr + k);
-        ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int k = (u * 64 * NW + threadIdx.x) * 4;
+        xv[u] = k < K ? *(const f32x4 *)(xr + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+        ss += xv[u][0] * xv[u][0] + xv[u][1] * xv[u][1] + xv[u][2] * xv[u][2] + xv[u][3] * xv[u][3];
+      }
+      for (int k0 = PER * 256 * NW; k0 < K; k0 += 256 * NW) {  // columns longer than one pass
+        const int k = k0 + threadIdx.x * 4;
+        if (k < K) {
+          const f32x4 v = *(const f32x4 *)(xr + k);
+          ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+        }
       }
       const float rs = 1.0f / sqrtf(block_sum<NW>(ss, s_part) / (float)K + a.eps);
-      for (int k = threadIdx.x * 4; k < K; k += 256 * NW) {
-        const f32x4 v = *(const f32x4 *)(xr + k);
+      auto put = [&](int k, f32x4 v) {
         float h[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) h[e] = v[e] * rs * ld_elem<DT>(a.gain, k + e);
@@ -229,6 +260,15 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
           dst[0] = w0;
           dst[1] = w1;
         }
+      };
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int k = (u * 64 * NW + threadIdx.x) * 4;
+        if (k < K) put(k, xv[u]);
+      }
+      for (int k0 = PER * 256 * NW; k0 < K; k0 += 256 * NW) {
+        const int k = k0 + threadIdx.x * 4;
+        if (k < K) put(k, *(const f32x4 *)(xr + k));
       }
     }
     __syncthreads();
@@ -276,24 +316,18 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // software pipeline: activations of this group, weights of the next
+  // group, then the MFMAs of this group (which wait only for the former)
   for (int kb0 = wave; kb0 < nkb; kb0 += NW * U) {
-    u32x4 wa[U][R][4], xb[U][NT][4];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kb = kb0 + u * NW;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-          wa[u][r][s] = (wp[r] && kb < nkb) ? ld16_stream(wp[r] + (int64_t)(kb * 4 + s) * 64 * CE)
-                                            : u32x4{0u, 0u, 0u, 0u};
-    }
+    u32x4 xb[U][NT][4];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int t = 0; t < NT; ++t) xb[u][t][s] = load_x(t, (kb0 + u * NW) * 16 + s * 4 + lq);
+    const bool more = kb0 + NW * U < nkb;
+    if (more) load_w(wnxt, kb0 + NW * U);
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -301,7 +335,15 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int r = 0; r < R; ++r)
 #pragma unroll
-          for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(wa[u][r][s], xb[u][t][s], acc[r][t]);
+          for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(wcur[u][r][s], xb[u][t][s], acc[r][t]);
+    if (more) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int s = 0; s < 4; ++s) wcur[u][r][s] = wnxt[u][r][s];
+    }
   }
 
   __shared__ f32x4 s_red[NW][R][NT][64];
@@ -343,6 +385,10 @@ template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   constexpr int R = (EPI == EPI_QKV || EPI == EPI_SWIGLU) ? 2 : 1;
   constexpr int NW = EPI == EPI_RESID ? 8 : 4;
+  // k-blocks per pipelined group at one column tile: two for single row
+  // tiles; one for paired tiles, whose registers would otherwise halve the
+  // resident work groups
+  constexpr int U1 = R == 2 ? 1 : 2;
   // one work group per R row tiles (q/k/v: per pair of RoPE half-tiles)
   const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 32
                                       : (a.rows[0] + 16 * (EPI == EPI_SWIGLU ? 1 : R) - 1) /
@@ -352,12 +398,11 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   if (tiles <= 1) {
     if constexpr (PRO == PRO_NORM) {
       const size_t xs = (size_t)a.ncols * a.K * b;
-      if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, 4, PRO, 1, EPI>(a, n_groups, xs, st);
+      if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
     }
-    if (EPI == EPI_RESID && a.K > 4096) return gemm_launch<DT, R, 1, NW, 2, PRO, 0, EPI>(a, n_groups, 0, st);
-    return gemm_launch<DT, R, 1, NW, 4, PRO, 0, EPI>(a, n_groups, 0, st);
+    return gemm_launch<DT, R, 1, NW, U1, PRO, 0, EPI>(a, n_groups, 0, st);
   }
-  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 2, PRO, 0, EPI>(a, n_groups, 0, st);
+  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
   return gemm_launch<DT, R, 4, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
 }
 

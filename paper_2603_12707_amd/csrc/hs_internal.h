@@ -50,9 +50,11 @@ struct GemmArgs {
 
 enum { PRO_PLAIN = 0, PRO_NORM = 1 };
 
-// attention: positions per split are a power of two in [ATTN_SMIN, ATTN_SMAX]
-constexpr int ATTN_SMAX = 1024;
-constexpr int ATTN_SMIN = 64;
+// attention work groups: waves per work group, and the fewest positions a
+// split is cut down to when the GPU would otherwise be under-filled
+constexpr int ATTN_WAVES = 4;
+constexpr int ATTN_MIN_SPLIT = 128;
+constexpr int ATTN_MAX_SPLITS = 256;
 enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
 struct AttnArgs {

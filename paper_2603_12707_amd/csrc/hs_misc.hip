@@ -13,6 +13,33 @@ using namespace dev;
 // ---------------------------------------------------------------------------
 // embeddings, selection, bookkeeping
 // ---------------------------------------------------------------------------
+// Copies one embedding row (model dtype) into the fp32 residual stream, one
+// 16-byte chunk per thread and step, all loads issued before the stores.
+template <int DT>
+__device__ __forceinline__ void copy_row(const void *__restrict__ src, float *__restrict__ dst, int d) {
+  constexpr int CE = Ty<DT>::CE;
+  using S = typename Ty<DT>::S;
+  constexpr int PER = 4;  // chunks per thread per pass
+  for (int base = 0; base < d; base += 256 * CE * PER) {
+    u32x4 v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int k = base + (u * 256 + threadIdx.x) * CE;
+      v[u] = k < d ? ld16((const S *)src + k) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int k = base + (u * 256 + threadIdx.x) * CE;
+      if (k < d) {
+        float f[CE];
+        unpack<DT>(v[u], f);
+#pragma unroll
+        for (int e = 0; e < CE; e += 4) *(f32x4 *)(dst + k + e) = f32x4{f[e], f[e + 1], f[e + 2], f[e + 3]};
+      }
+    }
+  }
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_embed(const void *E, int V, int d, const int *tok, float *x, int *status) {
   const int b = blockIdx.x;
@@ -21,7 +48,8 @@ __global__ __launch_bounds__(256) void k_embed(const void *E, int V, int d, cons
     if (threadIdx.x == 0) atomicOr(status, 1);
     t = 0;
   }
-  for (int k = threadIdx.x; k < d; k += 256) x[(int64_t)b * d + k] = ld_elem<DT>(E, (int64_t)t * d + k);
+  constexpr int B = DT == HS_F32 ? 4 : 2;
+  copy_row<DT>((const char *)E + (int64_t)t * d * B, x + (int64_t)b * d, d);
 }
 
 template <int DT>
@@ -42,22 +70,32 @@ __global__ __launch_bounds__(256) void k_prefill_rows(const void *emb, int n_v, 
     src = E;
     row = t;
   }
-  for (int k = threadIdx.x; k < d; k += 256) x[(int64_t)r * d + k] = ld_elem<DT>(src, row * d + k);
+  constexpr int B = DT == HS_F32 ? 4 : 2;
+  copy_row<DT>((const char *)src + row * d * B, x + (int64_t)r * d, d);
 }
 
 // Greedy selection: largest logit, lowest index among equals (NaN never wins).
-__global__ __launch_bounds__(1024) void k_argmax(const float *logits, int V, int ld, int *out, int *len, int *rope,
-                                                 int advance) {
+// Each thread scans indices i = tid + 1024 k in order, eight loads at a time.
+__global__ __launch_bounds__(1024) void k_argmax(const float *__restrict__ logits, int V, int ld, int *out, int *len,
+                                                 int *rope, int advance) {
   const int b = blockIdx.x;
   const float *lg = logits + (int64_t)b * ld;
   float bv = -INFINITY;
   int bi = 0x7FFFFFFF;
-  for (int i = threadIdx.x; i < V; i += 1024) {
-    const float v = lg[i];
-    if (v > bv) {
-      bv = v;
-      bi = i;
+  constexpr int PER = 8;
+  for (int base = 0; base < V; base += 1024 * PER) {
+    float v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = base + u * 1024 + threadIdx.x;
+      v[u] = i < V ? lg[i] : -INFINITY;
     }
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      if (v[u] > bv) {
+        bv = v[u];
+        bi = base + u * 1024 + threadIdx.x;
+      }
   }
   for (int off = 32; off >= 1; off >>= 1) {
     const float ov = __shfl_xor(bv, off);
