@@ -87,6 +87,15 @@ def stored_traffic(workload: str, kernel: str):
     return float(val.group(1))
 
 
+DEFAULT_WARMUP, DEFAULT_STEPS = 8, 120
+
+
+def steps_after_context(warmup: int, steps: int) -> int:
+    """Decode steps a bench run appends after the context: warm-up, the timed
+    region, the event-timed region and the per-kernel breakdown."""
+    return warmup + 2 * steps + min(10, steps)
+
+
 def setup(cfg: dict, n_steps_total: int):
     import torch
 
@@ -165,8 +174,8 @@ def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=120)
-    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--steps", type=int, default=DEFAULT_STEPS)
+    ap.add_argument("--warmup", type=int, default=DEFAULT_WARMUP)
     ap.add_argument("--workload", default="llava7b_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -186,7 +195,7 @@ def main() -> int:
     B = cfg["batch"]
     torch.cuda.set_device(0)
     n_prof = min(10, args.steps)
-    w, model, kv, first, lens0 = setup(cfg, args.warmup + 2 * args.steps + n_prof)
+    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps))
 
     tin = first.clone()
     tout = torch.empty_like(tin)

@@ -1,0 +1,193 @@
+"""GPU checks of the C ABI that need no oracle arithmetic: bit-exact KV
+indexing, the packed weight layout, error paths, and the seeded generator's
+CPU/GPU identity."""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import small_cfg
+from workload import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _model(cfg, max_batch=4, max_ctx=64):
+    import paper_2603_12707_amd as hs
+    w = {k: v.cuda() for k, v in synth.make_weights(cfg).items()}
+    return hs.Model(cfg, w, max_batch, max_ctx)
+
+
+def _layout_offset(cfg, caps, req, layer, sel, head, pos):
+    """Element offset of a cache row by the layout documented in hs.h."""
+    L, nkv, hd = cfg["n_layers"], cfg["n_kv_heads"], cfg["head_dim"]
+    base = sum(2 * L * nkv * hd * c for c in caps[:req])
+    return base + (((layer * 2 + sel) * nkv + head) * caps[req] + pos) * hd
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_kv_write_read_follow_documented_layout(dtype):
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype=dtype, n_layers=2, n_heads=4, n_kv_heads=2, head_dim=64)
+    model = _model(cfg)
+    caps = [7, 13, 5]
+    kv = hs.KVCache(model, [0, 3, 5], caps)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    flat = kv.buf.view(tdt)
+    assert flat.numel() * flat.element_size() == sum(hs.hs_kv_bytes(cfg, 0, c)[0] for c in caps)
+    flat.zero_()
+    rng = np.random.default_rng(0)
+    for req, cap in enumerate(caps):
+        for layer in range(2):
+            for sel in (0, 1):
+                for head in range(2):
+                    pos0 = int(rng.integers(0, cap))
+                    n = int(rng.integers(1, cap - pos0 + 1))
+                    rows = torch.from_numpy(rng.standard_normal((n, 64)).astype(np.float32)).to(tdt)
+                    src = rows.cuda() if (req + layer + sel + head) % 2 else rows
+                    kv.write(req, layer, sel, head, pos0, src)
+                    off = _layout_offset(cfg, caps, req, layer, sel, head, pos0)
+                    got = flat[off:off + n * 64].view(n, 64).cpu()
+                    assert torch.equal(got.view(torch.int16 if dtype != "f32" else torch.int32),
+                                       rows.view(torch.int16 if dtype != "f32" else torch.int32))
+                    back = torch.empty_like(rows)
+                    kv.read(req, layer, sel, head, pos0, n, back)
+                    assert torch.equal(back, rows)
+    with pytest.raises(hs.HsError) as e:
+        kv.write(0, 0, 0, 0, 5, torch.zeros(3, 64, dtype=tdt))  # past capacity 7
+    assert e.value.code == hs.HS_E_INVALID
+    with pytest.raises(hs.HsError):
+        kv.write(0, 2, 0, 0, 0, torch.zeros(1, 64, dtype=tdt))  # layer out of range
+
+
+def test_decode_appends_exactly_one_row_per_layer_and_head():
+    """After prefill, a decode step changes the cache only at position len_b
+    of every (request, layer, K|V, head); every other byte stays as it was."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="bf16", n_layers=2, n_heads=4, n_kv_heads=2, head_dim=64)
+    model = _model(cfg)
+    n_v, s_text = [4, 0, 9], [3, 6, 1]
+    caps = [12, 9, 16]
+    kv = hs.KVCache(model, n_v, caps)
+    kv.buf.fill_(0x5A)  # sentinel in every unwritten byte
+    for r in range(3):
+        emb = synth.vision_rows(cfg, r, n_v[r]).cuda() if n_v[r] else None
+        kv.prefill(r, emb, synth.text_ids(cfg, r, s_text[r]).cuda())
+    torch.cuda.synchronize()
+    before = kv.buf.clone()
+    lens = kv.lengths()
+    assert lens == [7, 6, 10]
+    tin = torch.tensor([1, 2, 3], dtype=torch.int32, device="cuda")
+    tout = torch.empty(3, dtype=torch.int32, device="cuda")
+    kv.decode(tin, tout)
+    torch.cuda.synchronize()
+    after = kv.buf
+    changed = torch.zeros_like(before, dtype=torch.bool)
+    b = 2  # bytes per element
+    for r in range(3):
+        for layer in range(2):
+            for sel in (0, 1):
+                for head in range(2):
+                    off = _layout_offset(cfg, caps, r, layer, sel, head, lens[r]) * b
+                    changed[off:off + 64 * b] = True
+                    # the appended row was written (no sentinel pattern left)
+                    assert not torch.all(after[off:off + 64 * b] == 0x5A)
+    assert torch.equal(after[~changed], before[~changed])
+    assert kv.lengths() == [8, 7, 11]
+
+
+@pytest.mark.parametrize("dtype,rows,cols", [("f16", 37, 136), ("bf16", 16, 128), ("f32", 5, 68), ("f16", 300, 1000)])
+def test_pack_matrix_follows_documented_layout(dtype, rows, cols):
+    import paper_2603_12707_amd as hs
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    src = torch.randn(rows, cols, generator=torch.Generator().manual_seed(1)).to(tdt)
+    packed = hs.pack_matrix(src.cuda(), dtype).cpu()
+    ce = 16 // src.element_size()
+    nkb = (cols // ce + 15) // 16
+    tiles = (rows + 15) // 16
+    assert packed.numel() == tiles * nkb * 256 * ce * src.element_size()
+    p = packed.view(tdt).view(tiles, nkb, 4, 64, ce)
+    # expected by the formula in hs.h: slot l = 16 q + i of sub-block s of
+    # k-block kb of tile t holds chunk 16 kb + 4 s + q of row 16 t + i
+    exp = torch.zeros(tiles * 16, nkb * 16 * ce, dtype=tdt)
+    exp[:rows, :cols] = src
+    exp = exp.view(tiles, 16, nkb, 4, 4, ce)  # [t][i][kb][s][q][e]
+    exp = exp.permute(0, 2, 3, 4, 1, 5).reshape(tiles, nkb, 4, 64, ce)
+    assert torch.equal(p.view(torch.int16 if dtype != "f32" else torch.int32),
+                       exp.view(torch.int16 if dtype != "f32" else torch.int32))
+
+
+def test_error_paths():
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="f16", n_layers=1)
+    model = _model(cfg, max_batch=2, max_ctx=32)
+    kv = hs.KVCache(model, [2, 0], [6, 5])
+    tin = torch.zeros(2, dtype=torch.int32, device="cuda")
+    tout = torch.zeros(2, dtype=torch.int32, device="cuda")
+    with pytest.raises(hs.HsError) as e:
+        kv.decode(tin, tout)                      # decode before prefill
+    assert e.value.code == hs.HS_E_STATE
+    emb = synth.vision_rows(cfg, 0, 2).cuda()
+    ids = synth.text_ids(cfg, 0, 3).cuda()
+    kv.prefill(0, emb, ids)
+    with pytest.raises(hs.HsError) as e:
+        kv.prefill(0, emb, ids)                   # prefill twice
+    assert e.value.code == hs.HS_E_STATE
+    with pytest.raises(hs.HsError) as e:
+        kv.prefill(1, None, synth.text_ids(cfg, 1, 6).cuda())  # context 6 > capacity 5
+    assert e.value.code == hs.HS_E_CAPACITY
+    with pytest.raises(hs.HsError) as e:
+        kv.prefill(2, None, ids)                  # request out of range
+    assert e.value.code == hs.HS_E_INVALID
+    kv.prefill(1, None, synth.text_ids(cfg, 1, 4).cuda())
+    with pytest.raises(hs.HsError) as e:
+        kv.decode(tin, tin)                       # aliasing token buffers
+    assert e.value.code == hs.HS_E_INVALID
+    kv.decode(tin, tout)                          # lengths 5, 4 -> 6, 5 (request 1 full)
+    with pytest.raises(hs.HsError) as e:
+        kv.decode(tout, tin)
+    assert e.value.code == hs.HS_E_CAPACITY
+    assert kv.lengths() == [6, 5]
+    small = torch.empty(10, dtype=torch.uint8, device="cuda")
+    with pytest.raises(hs.HsError) as e:
+        hs.KVCache(model, [0], [4], buf=small)    # buffer too small
+    assert e.value.code == hs.HS_E_BUFFER
+    with pytest.raises(hs.HsError) as e:
+        hs.KVCache(model, [0], [33])              # capacity > max_ctx
+    assert e.value.code == hs.HS_E_INVALID
+
+
+def test_out_of_range_token_is_flagged_and_read_as_zero():
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="f16", n_layers=1)
+    model = _model(cfg, max_batch=2, max_ctx=32)
+    outs = []
+    for tok in (0, cfg["vocab"] + 5):
+        kv = hs.KVCache(model, [0, 0], [8, 8])
+        for r in range(2):
+            kv.prefill(r, None, synth.text_ids(cfg, 7, 4).cuda())
+        logits = torch.empty(2, cfg["vocab"], device="cuda")
+        tout = torch.empty(2, dtype=torch.int32, device="cuda")
+        kv.decode(torch.tensor([tok, tok], dtype=torch.int32, device="cuda"), tout, logits)
+        outs.append(logits.cpu())
+        assert model.status() == (0 if tok == 0 else 1)
+    assert torch.equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "f32"])
+def test_generator_is_bit_identical_on_cpu_and_gpu(dtype):
+    """The seeded inputs the oracle and the GPU use are the same bits
+    whichever device produced them."""
+    for name, shape, mean in (("layers.3.wq", (96, 1000), None), ("layers.0.attn_norm", (777,), 1.0),
+                              ("req.5.vision", (13, 384), None)):
+        std = 1.0 if "vision" in name else 0.02
+        a = synth.normal(0, name, shape, std, dtype, "cpu", mean=mean)
+        b = synth.normal(0, name, shape, std, dtype, "cuda", mean=mean).cpu()
+        iv = torch.int16 if dtype != "f32" else torch.int32
+        assert torch.equal(a.view(iv), b.view(iv)), name
+    a = synth.uniform_int(0, "req.1.text", 5000, 0, 152063, "cpu")
+    b = synth.uniform_int(0, "req.1.text", 5000, 0, 152063, "cuda").cpu()
+    assert torch.equal(a, b)

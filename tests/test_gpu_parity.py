@@ -120,3 +120,50 @@ def test_long_context_many_splits():
     cfg = small_cfg(n_layers=1, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=512, vocab=512)
     near = _run_pair(cfg, [1100], [37], 3, extra_cap=400)
     assert near == 0
+
+
+def test_batch_invariance():
+    """A request's logits do not depend on the other requests of its batch
+    (the property that lets decode shard by request across GPUs)."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
+    n_v, s_text = [30, 3, 70, 0, 12], [5, 40, 2, 9, 200]
+    caps = [n + s + 3 for n, s in zip(n_v, s_text)]
+    pair = Pair(cfg, max_batch=5, max_ctx=max(caps))
+    out = {}
+    for batch in ([2], [0, 1, 2, 3, 4]):
+        kv = hs.KVCache(pair.gpu, [n_v[r] for r in batch], [caps[r] for r in batch])
+        for i, r in enumerate(batch):
+            emb, ids, _ = pair.request_inputs(r, n_v[r], s_text[r])
+            kv.prefill(i, emb.cuda() if n_v[r] else None, ids.cuda())
+        logits = torch.empty(len(batch), cfg["vocab"], device="cuda")
+        tout = torch.empty(len(batch), dtype=torch.int32, device="cuda")
+        kv.decode(torch.full((len(batch),), 11, dtype=torch.int32, device="cuda"), tout, logits)
+        out[len(batch)] = logits[batch.index(2)].cpu().numpy()
+        kv.close()
+    assert rel_err(out[5], out[1]) <= 1e-3
+
+
+@pytest.mark.parametrize("rope_kind", [0, 1])
+def test_prefill_then_decode_matches_longer_prefill(rope_kind):
+    """prefill(s + 1) last-row logits agree with prefill(s) followed by one
+    decode step of token s (a property that holds at any size)."""
+    import paper_2603_12707_amd as hs
+    extra = dict(rope_kind=1, mrope_section=(8, 12, 12), rope_theta=1e6) if rope_kind else {}
+    cfg = small_cfg(dtype="f16", n_heads=6, n_kv_heads=3, head_dim=64, **extra)
+    n_v, s_text = 50, 9
+    pair = Pair(cfg, max_batch=1, max_ctx=80)
+    emb, ids, pos = pair.request_inputs(0, n_v, s_text)
+    a = hs.KVCache(pair.gpu, [n_v], [80])
+    pos_short = None if pos is None else pos[:, :-1].contiguous()
+    a.prefill(0, emb.cuda(), ids[:-1].cuda(), None if pos is None else pos_short.cuda())
+    la = torch.empty(1, cfg["vocab"], device="cuda")
+    tout = torch.empty(1, dtype=torch.int32, device="cuda")
+    if rope_kind:  # the decode position must be the one the longer prefill gives the last token
+        assert int(pos[0, -1]) == int(pos_short.max()) + 1
+    a.decode(ids[-1:].cuda(), tout, la)
+    b = hs.KVCache(pair.gpu, [n_v], [80])
+    lb = torch.empty(cfg["vocab"], device="cuda")
+    b.prefill(0, emb.cuda(), ids.cuda(), None if pos is None else pos.cuda(), last_logits=lb)
+    torch.cuda.synchronize()
+    assert rel_err(la[0].cpu().numpy(), lb.cpu().numpy()) <= 2e-3
