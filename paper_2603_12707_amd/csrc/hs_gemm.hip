@@ -154,18 +154,29 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
   }
 }
 
-// Sum over the 64 * NW threads of a work group; every thread gets it.
+// fp64 sum over the 64 lanes of a wave; every lane gets it.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// fp64 sum over the 64 * NW threads of a work group; every thread gets it.
 template <int NW>
-__device__ __forceinline__ float block_sum(float v, float *s_part) {
+__device__ __forceinline__ double block_sum(double v, double *s_part) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  v = wave_sum(v);
+  v = wave_sum_f64(v);
   __syncthreads();
   if (lane == 0) s_part[wave] = v;
   __syncthreads();
-  float t = 0.f;
+  double t = 0.0;
 #pragma unroll
   for (int w = 0; w < NW; ++w) t += s_part[w];
   return t;
+}
+
+__device__ __forceinline__ double sumsq_f64(f32x4 v) {
+  return (double)v[0] * v[0] + (double)v[1] * v[1] + (double)v[2] * v[2] + (double)v[3] * v[3];
 }
 
 // Y[c][n] = sum_k X[c][k] W[n][k] over R row tiles and NT column tiles of 16.
@@ -215,7 +226,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   load_w(wcur, wave);
 
   __shared__ float s_rsq[16 * NT];
-  __shared__ float s_part[NW];
+  __shared__ double s_part[NW];
   extern __shared__ __align__(16) unsigned char s_x[];  // XS: normalised activations [nst][K]
   const int nst = min(a.ncols - col0, 16 * NT);
   if constexpr (PRO == PRO_NORM && XS == 1) {
@@ -226,21 +237,18 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     for (int c = 0; c < nst; ++c) {
       const float *xr = x + (int64_t)(col0 + c) * K;
       f32x4 xv[PER];
-      float ss = 0.f;
+      double ss = 0.0;
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
         const int k = (u * 64 * NW + threadIdx.x) * 4;
         xv[u] = k < K ? *(const f32x4 *)(xr + k) : f32x4{0.f, 0.f, 0.f, 0.f};
-        ss += xv[u][0] * xv[u][0] + xv[u][1] * xv[u][1] + xv[u][2] * xv[u][2] + xv[u][3] * xv[u][3];
+        ss += sumsq_f64(xv[u]);
       }
       for (int k0 = PER * 256 * NW; k0 < K; k0 += 256 * NW) {  // columns longer than one pass
         const int k = k0 + threadIdx.x * 4;
-        if (k < K) {
-          const f32x4 v = *(const f32x4 *)(xr + k);
-          ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
-        }
+        if (k < K) ss += sumsq_f64(*(const f32x4 *)(xr + k));
       }
-      const float rs = 1.0f / sqrtf(block_sum<NW>(ss, s_part) / (float)K + a.eps);
+      const float rs = (float)(1.0 / sqrt(block_sum<NW>(ss, s_part) / (double)K + (double)a.eps));
       auto put = [&](int k, f32x4 v) {
         float h[4];
 #pragma unroll
@@ -276,16 +284,13 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     const float *x = (const float *)a.x;
     for (int c = wave; c < 16 * NT; c += NW) {
       const int col = col0 + c;
-      float ss = 0.f;
+      double ss = 0.0;
       if (col < a.ncols) {
         const float *xr = x + (int64_t)col * K;
-        for (int k = lane * 4; k < K; k += 256) {
-          const f32x4 v = *(const f32x4 *)(xr + k);
-          ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
-        }
+        for (int k = lane * 4; k < K; k += 256) ss += sumsq_f64(*(const f32x4 *)(xr + k));
       }
-      ss = wave_sum(ss);
-      if (lane == 0) s_rsq[c] = 1.0f / sqrtf(ss / (float)K + a.eps);
+      ss = wave_sum_f64(ss);
+      if (lane == 0) s_rsq[c] = (float)(1.0 / sqrt(ss / (double)K + (double)a.eps));
     }
     __syncthreads();
   }
@@ -310,11 +315,21 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     }
   };
 
+  // The MFMAs of one k-group accumulate in fp32 from zero; with ACC64 each
+  // group's tile is then added into fp64 accumulators, so that fp32 rounding
+  // only ever acts on sums of 4 * U * 32 products.
+  constexpr bool ACC64 = NT <= 2;
   f32x4 acc[R][NT];
+  double acc64[ACC64 ? R : 1][ACC64 ? NT : 1][4];
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NT; ++t) {
+      acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (ACC64)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc64[r][t][e] = 0.0;
+    }
 
   // software pipeline: activations of this group, weights of the next
   // group, then the MFMAs of this group (which wait only for the former)
@@ -336,6 +351,16 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         for (int r = 0; r < R; ++r)
 #pragma unroll
           for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(wcur[u][r][s], xb[u][t][s], acc[r][t]);
+    if constexpr (ACC64) {
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc64[r][t][e] += (double)acc[r][t][e];
+          acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
     if (more) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
@@ -346,20 +371,39 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     }
   }
 
-  __shared__ f32x4 s_red[NW][R][NT][64];
+  // fixed-order sum of the waves' partial tiles through LDS
+  __shared__ __align__(16) unsigned char s_red_raw[NW * R * NT * 64 * (ACC64 ? 32 : 16)];
+  double *s_red64 = (double *)s_red_raw;  // [NW][R][NT][4][64]
+  f32x4 *s_red = (f32x4 *)s_red_raw;      // [NW][R][NT][64]
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) s_red[wave][r][t][lane] = acc[r][t];
+    for (int t = 0; t < NT; ++t) {
+      if constexpr (ACC64) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s_red64[(((wave * R + r) * NT + t) * 4 + e) * 64 + lane] = acc64[r][t][e];
+      } else {
+        s_red[((wave * R + r) * NT + t) * 64 + lane] = acc[r][t];
+      }
+    }
   __syncthreads();
   for (int item = threadIdx.x; item < NT * 64; item += 64 * NW) {
     const int t = item >> 6, ln = item & 63;
     f32x4 v[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      v[r] = s_red[0][r][t][ln];
+      if constexpr (ACC64) {
+        double sum[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-      for (int w = 1; w < NW; ++w) v[r] += s_red[w][r][t][ln];
+        for (int w = 0; w < NW; ++w)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sum[e] += s_red64[(((w * R + r) * NT + t) * 4 + e) * 64 + ln];
+        v[r] = f32x4{(float)sum[0], (float)sum[1], (float)sum[2], (float)sum[3]};
+      } else {
+        v[r] = s_red[((0 * R + r) * NT + t) * 64 + ln];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) v[r] += s_red[((w * R + r) * NT + t) * 64 + ln];
+      }
     }
     const int col = col0 + 16 * t + (ln & 15);
     if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
