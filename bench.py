@@ -59,11 +59,6 @@ def step_bytes(cfg: dict, lens: list) -> int:
     return L * per_layer + wb["head"] + B * d * b + sum(kv_row * (n + 1) for n in lens) + B * kv_row
 
 
-def hs_kinds():
-    from paper_2603_12707_amd.hs import HS_K_NAMES
-    return HS_K_NAMES
-
-
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
     for rel in ("paper_2603_12707_amd/csrc/hs_gemm.hip", "paper_2603_12707_amd/csrc/hs_device.h",
@@ -91,9 +86,9 @@ DEFAULT_WARMUP, DEFAULT_STEPS = 8, 120
 
 
 def steps_after_context(warmup: int, steps: int) -> int:
-    """Decode steps a bench run appends after the context: warm-up, the timed
-    region, the event-timed region and the per-kernel breakdown."""
-    return warmup + 2 * steps + min(10, steps)
+    """Positions a bench run needs after the context: warm-up, the timed region,
+    and one spare position that kernel replays rewrite."""
+    return warmup + steps + 1
 
 
 def setup(cfg: dict, n_steps_total: int):
@@ -194,7 +189,6 @@ def main() -> int:
     cfg = configs.get(args.workload)
     B = cfg["batch"]
     torch.cuda.set_device(0)
-    n_prof = min(10, args.steps)
     w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps))
 
     tin = first.clone()
@@ -211,8 +205,7 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
 
-    # timed region: K steps bracketed by device synchronisation, no events
-    # attached (an event pair on a launch delays the next dispatch by ~10 us)
+    # timed region: K steps bracketed by device synchronisation
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
@@ -220,29 +213,31 @@ def main() -> int:
     elapsed = time.perf_counter() - t0
     lens_after = kv.lengths()
 
-    # kernel region: the same number of steps again, with a HIP event pair on
-    # every launch of the dominant kernel (gate/up projection), recorded on
-    # the stream the library launches on
+    # dominant kernel (gate/up projection): replayed back to back over every
+    # layer's weights, HIP events around the batch on the stream the library
+    # launches on (torch's current stream)
     dominant = "gateup"
-    model.set_timing([dominant], cfg["n_layers"] * args.steps)
+    reps = 4 * cfg["n_layers"]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    kv.replay(dominant, cfg["n_layers"])  # warm
+    ev0.record()
+    kv.replay(dominant, reps)
+    ev1.record()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    timed_elapsed = time.perf_counter() - t1
-    tim = model.timing()
-    model.set_timing([], 0)
+    dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
 
-    # per-kernel breakdown over a few more steps (every kind timed)
-    model.set_timing(list(hs_kinds()), 400 * n_prof)
-    t2 = time.perf_counter()
-    for _ in range(n_prof):
-        step()
-    torch.cuda.synchronize()
-    prof_elapsed = time.perf_counter() - t2
-    breakdown = model.timing()
-    model.set_timing([], 0)
+    # per-kernel breakdown, the same way for every replayable kind
+    breakdown = {}
+    for kind in ("qkv", "attn", "combine", "oproj", "gateup", "down", "head"):
+        try:
+            kv.replay(kind, 1)
+        except Exception:  # combine: single split; head: no LM head
+            continue
+        ev0.record()
+        kv.replay(kind, cfg["n_layers"])
+        ev1.record()
+        torch.cuda.synchronize()
+        breakdown[kind] = ev0.elapsed_time(ev1) / cfg["n_layers"] * 1e3  # us per launch
 
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
@@ -258,19 +253,14 @@ def main() -> int:
     gbs = total_bytes / elapsed / 1e9
     assert lens_after == [n + args.steps for n in lens_start], (lens_after[:4], lens_start[:4])
 
-    dom_ms, dom_n = tim[dominant]
-    dom_avg_s = dom_ms / dom_n / 1e3
     dom_bytes = weight_bytes(cfg)[dominant]
     achieved = dom_bytes / dom_avg_s / 1e9
     traffic = stored_traffic(args.workload, dominant)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "k_gemm (RMSNorm + gate/up projection + SwiGLU)",
-                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": dom_n}
-    kernels = {k: {"avg_us": round(v[0] / v[1] * 1e3, 2), "launches_per_step": v[1] / n_prof,
-                   "ms_per_step": round(v[0] / n_prof, 4)}
-               for k, v in breakdown.items() if k != "dropped"}
-    kernel_ms = sum(v[0] for k, v in breakdown.items() if k != "dropped") / n_prof
+                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps}
+    kernels = {k: round(v, 2) for k, v in breakdown.items()}
 
     out = {
         "metric": METRIC,
@@ -293,10 +283,7 @@ def main() -> int:
         "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
         "bytes_per_step": total_bytes // args.steps,
         "roofline": roofline,
-        "kernels": kernels,
-        "kernel_ms_per_step": round(kernel_ms, 4),
-        "ms_per_step_dominant_timed": round(timed_elapsed / args.steps * 1e3, 4),
-        "ms_per_step_all_timed": round(prof_elapsed / n_prof * 1e3, 4),
+        "kernel_us": kernels,
     }
     if not args.no_cpu_baseline:
         del w

@@ -187,7 +187,7 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
  * id was replaced by 0).  Synchronises the device. */
 int hs_model_status(hs_model *m, int32_t *flags);
 
-/* ---- per-kernel timing (measurement hook) ---- */
+/* ---- kernel replay (measurement hook) ---- */
 
 /* Kernel kinds of one decode step, in launch order within a layer. */
 #define HS_K_EMBED 0   /* token embedding gather */
@@ -201,18 +201,16 @@ int hs_model_status(hs_model *m, int32_t *flags);
 #define HS_K_ARGMAX 8  /* greedy selection and length advance */
 #define HS_K_COUNT 9
 
-/* Attaches a HIP start/stop event pair to every later launch (on the call's
- * stream) of the kinds in kind_mask (bit k = kind k), up to max_launches
- * launches; launches beyond that run untimed and are counted as dropped.
- * kind_mask 0 switches timing off and releases the events.  Event creation
- * happens here, never inside the timed calls. */
-int hs_model_set_timing(hs_model *m, int32_t kind_mask, int32_t max_launches);
-
-/* Synchronises the device, adds up the elapsed time of every timed launch per
- * kind into total_ms[n_kinds] (milliseconds) and launches[n_kinds], returns
- * the number of dropped launches in *dropped (may be NULL), and resets the
- * accumulators. */
-int hs_model_timing(hs_model *m, int32_t n_kinds, double *total_ms, int64_t *launches, int64_t *dropped);
+/* Launches `count` kernels of one kind back to back on the stream, in the
+ * launch configuration of this handle's decode step, cycling over the layers
+ * (layer i % n_layers), so that a caller can time one kernel with events
+ * around the batch.  Only for measurement between decode steps: the replayed
+ * kernels read and rewrite the step's workspaces (and q/k/v rewrites the
+ * K/V rows at each request's next position, which the next step rewrites
+ * again); lengths do not change.  Kinds: HS_K_QKV, HS_K_ATTN, HS_K_COMBINE
+ * (HS_E_STATE when the batch runs attention in one split), HS_K_OPROJ,
+ * HS_K_GATEUP, HS_K_DOWN, HS_K_HEAD.  Same state checks as hs_decode_step. */
+int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_stream_t stream);
 
 /* ---- test and fill hooks (synchronous) ---- */
 

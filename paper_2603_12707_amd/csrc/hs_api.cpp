@@ -33,34 +33,6 @@ int fail(int code, const char *fmt, ...) {
 
 int dtype_bytes(int dt) { return dt == HS_F32 ? 4 : 2; }
 
-// Runs one launcher, attaching a timing event pair when its kind is timed.
-// Every launcher passed here launches exactly one kernel.
-template <typename F>
-hipError_t timed(hs_model *m, int kind, F &&launch) {
-  const bool on = (m->timing_mask >> kind) & 1;
-  if (on && m->ev_used < (int)m->ev_start.size()) {
-    g_launch_events.start = m->ev_start[m->ev_used];
-    g_launch_events.stop = m->ev_stop[m->ev_used];
-    m->ev_kind[m->ev_used++] = kind;
-  } else if (on) {
-    m->ev_dropped++;
-  }
-  const hipError_t e = launch();
-  g_launch_events = LaunchEvents{};
-  return e;
-}
-
-void release_events(hs_model *m) {
-  for (hipEvent_t e : m->ev_start) (void)hipEventDestroy(e);
-  for (hipEvent_t e : m->ev_stop) (void)hipEventDestroy(e);
-  m->ev_start.clear();
-  m->ev_stop.clear();
-  m->ev_kind.clear();
-  m->ev_used = 0;
-  m->ev_dropped = 0;
-  m->timing_mask = 0;
-}
-
 // Light checks needed by the size formula alone.
 bool shape_ok(const hs_config *c) {
   return c && c->n_layers > 0 && c->n_kv_heads > 0 && c->head_dim > 0 && c->d_model > 0 && c->dtype >= HS_F32 &&
@@ -112,19 +84,25 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
 
 void free_model(hs_model *m) {
   if (!m) return;
-  release_events(m);
   void *ptrs[] = {m->x, m->q, m->attn, m->act, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
 }
 
-// Runs every decoder layer over ncols activation rows held in m->x.
-int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *rope_pos, int S, int n_split,
-               hipStream_t st) {
-  const hs_config &c = m->cfg;
-  const int d = c.d_model, hd = c.head_dim, nh = c.n_heads, nkv = c.n_kv_heads, F = c.ffn_dim;
-  for (int l = 0; l < c.n_layers; ++l) {
+// The launches of one pass over ncols activation rows held in m->x: decode
+// (one row per request, prefill_req < 0) or prefill (one row per position of
+// request prefill_req).  Each member launches one kernel.
+struct Step {
+  hs_model *m;
+  hs_kv *kv;
+  int ncols, prefill_req;
+  const int *rope_pos;
+  int S, n_split;
+  hipStream_t st;
+
+  hipError_t qkv(int l) const {
+    const hs_config &c = m->cfg;
     const hs_layer_weights &W = m->layers[l];
     GemmArgs g{};
     g.w[0] = W.wq;
@@ -135,18 +113,18 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
       g.bias[1] = W.bk;
       g.bias[2] = W.bv;
     }
-    g.rows[0] = nh * hd;
-    g.rows[1] = g.rows[2] = nkv * hd;
-    g.K = d;
+    g.rows[0] = c.n_heads * c.head_dim;
+    g.rows[1] = g.rows[2] = c.n_kv_heads * c.head_dim;
+    g.K = c.d_model;
     g.ncols = ncols;
     g.x = m->x;
     g.gain = W.attn_norm;
     g.eps = c.rms_eps;
     g.out = m->q;
-    g.ld_out = nh * hd;
-    g.head_dim = hd;
-    g.n_heads = nh;
-    g.n_kv = nkv;
+    g.ld_out = c.n_heads * c.head_dim;
+    g.head_dim = c.head_dim;
+    g.n_heads = c.n_heads;
+    g.n_kv = c.n_kv_heads;
     g.kv = kv->buf;
     g.kv_base = kv->d_base;
     g.kv_cap = kv->d_cap;
@@ -160,78 +138,118 @@ int run_layers(hs_model *m, hs_kv *kv, int ncols, int prefill_req, const int *ro
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
-    HIP_TRY(timed(m, HS_K_QKV, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, st); }));
+    return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, st);
+  }
 
+  AttnArgs attn_args(int l) const {
+    const hs_config &c = m->cfg;
     AttnArgs a{};
     a.q = m->q;
-    a.ld_q = nh * hd;
+    a.ld_q = c.n_heads * c.head_dim;
     a.kv = kv->buf;
     a.kv_base = kv->d_base;
     a.kv_cap = kv->d_cap;
     a.kv_len = kv->d_len;
     a.layer = l;
-    a.n_heads = nh;
-    a.n_kv = nkv;
+    a.n_heads = c.n_heads;
+    a.n_kv = c.n_kv_heads;
     a.prefill_req = prefill_req;
     a.S = S;
     a.n_split = n_split;
     a.part_o = m->part_o;
     a.part_ml = m->part_ml;
-    a.scale = (float)(1.0 / std::sqrt((double)hd));
+    a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
     a.out = m->attn;
-    HIP_TRY(timed(m, HS_K_ATTN, [&] { return launch_attention(c.dtype, hd, nh / nkv, ncols, a, st); }));
-    if (n_split > 1) HIP_TRY(timed(m, HS_K_COMBINE, [&] { return launch_combine(c.dtype, hd, ncols, a, st); }));
+    return a;
+  }
 
+  hipError_t attn(int l) const {
+    const hs_config &c = m->cfg;
+    return launch_attention(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
+  }
+
+  hipError_t combine(int l) const {  // launches nothing with a single split
+    const hs_config &c = m->cfg;
+    return launch_combine(c.dtype, c.head_dim, ncols, attn_args(l), st);
+  }
+
+  hipError_t residual(const void *w, int K, const void *x) const {
+    const hs_config &c = m->cfg;
     GemmArgs o{};
-    o.w[0] = W.wo;
-    o.rows[0] = d;
-    o.K = nh * hd;
+    o.w[0] = w;
+    o.rows[0] = c.d_model;
+    o.K = K;
     o.ncols = ncols;
-    o.x = m->attn;
+    o.x = x;
     o.resid = m->x;
-    o.ld_resid = d;
-    HIP_TRY(timed(m, HS_K_OPROJ, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st); }));
+    o.ld_resid = c.d_model;
+    return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st);
+  }
 
+  hipError_t oproj(int l) const { return residual(m->layers[l].wo, m->cfg.n_heads * m->cfg.head_dim, m->attn); }
+
+  hipError_t gateup(int l) const {
+    const hs_config &c = m->cfg;
+    const hs_layer_weights &W = m->layers[l];
     GemmArgs u{};
     u.w[0] = W.w_gate;
     u.w[1] = W.w_up;
-    u.rows[0] = u.rows[1] = F;
-    u.K = d;
+    u.rows[0] = u.rows[1] = c.ffn_dim;
+    u.K = c.d_model;
     u.ncols = ncols;
     u.x = m->x;
     u.gain = W.mlp_norm;
     u.eps = c.rms_eps;
     u.out = m->act;
-    u.ld_out = F;
-    HIP_TRY(timed(m, HS_K_GATEUP, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, st); }));
-
-    GemmArgs dn{};
-    dn.w[0] = W.w_down;
-    dn.rows[0] = d;
-    dn.K = F;
-    dn.ncols = ncols;
-    dn.x = m->act;
-    dn.resid = m->x;
-    dn.ld_resid = d;
-    HIP_TRY(timed(m, HS_K_DOWN, [&] { return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, dn, st); }));
+    u.ld_out = c.ffn_dim;
+    return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, st);
   }
-  return HS_OK;
-}
 
-// Final RMSNorm + LM head over ncols rows starting at x_rows -> logits.
-int run_head(hs_model *m, const float *x_rows, int ncols, float *logits, hipStream_t st) {
+  hipError_t down(int l) const { return residual(m->layers[l].w_down, m->cfg.ffn_dim, m->act); }
+
+  // final RMSNorm + LM head over ncols rows starting at x_rows
+  hipError_t head(const float *x_rows, float *logits) const {
+    const hs_config &c = m->cfg;
+    GemmArgs g{};
+    g.w[0] = m->w.lm_head;
+    g.rows[0] = c.vocab;
+    g.K = c.d_model;
+    g.ncols = ncols;
+    g.x = x_rows;
+    g.gain = m->w.final_norm;
+    g.eps = c.rms_eps;
+    g.out = logits;
+    g.ld_out = c.vocab;
+    return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, st);
+  }
+
+  int layers() const {
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      HIP_TRY(qkv(l));
+      HIP_TRY(attn(l));
+      if (n_split > 1) HIP_TRY(combine(l));
+      HIP_TRY(oproj(l));
+      HIP_TRY(gateup(l));
+      HIP_TRY(down(l));
+    }
+    return HS_OK;
+  }
+};
+
+// The decode pass of a handle (checks that every request can take a step).
+int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out) {
   const hs_config &c = m->cfg;
-  GemmArgs g{};
-  g.w[0] = m->w.lm_head;
-  g.rows[0] = c.vocab;
-  g.K = c.d_model;
-  g.ncols = ncols;
-  g.x = x_rows;
-  g.gain = m->w.final_norm;
-  g.eps = c.rms_eps;
-  g.out = logits;
-  g.ld_out = c.vocab;
-  HIP_TRY(timed(m, HS_K_HEAD, [&] { return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, st); }));
+  const int B = kv->batch;
+  if (B > m->max_batch) return fail(HS_E_INVALID, "decode: batch %d exceeds max_batch %d", B, m->max_batch);
+  for (int b = 0; b < B; ++b) {
+    if (!kv->ready[b]) return fail(HS_E_STATE, "decode: request %d is not prefilled", b);
+    if (kv->len[b] >= kv->cap[b]) return fail(HS_E_CAPACITY, "decode: request %d is full (%d positions)", b, kv->cap[b]);
+  }
+  int S, ns;
+  split_policy(B, c.n_kv_heads, kv->max_cap, &S, &ns);
+  if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
+    return fail(HS_E_INVALID, "decode: attention workspace too small");
+  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, st};
   return HS_OK;
 }
 
@@ -378,48 +396,6 @@ int hs_model_status(hs_model *m, int32_t *flags) {
   return HS_OK;
 }
 
-int hs_model_set_timing(hs_model *m, int32_t kind_mask, int32_t max_launches) {
-  if (!m) return fail(HS_E_INVALID, "hs_model_set_timing: NULL model");
-  if (kind_mask < 0 || kind_mask >= (1 << HS_K_COUNT) || max_launches < 0)
-    return fail(HS_E_INVALID, "hs_model_set_timing: bad mask or launch count");
-  HIP_TRY(hipDeviceSynchronize());
-  release_events(m);
-  if (!kind_mask) return HS_OK;
-  m->ev_start.resize(max_launches, nullptr);
-  m->ev_stop.resize(max_launches, nullptr);
-  m->ev_kind.resize(max_launches, -1);
-  for (int i = 0; i < max_launches; ++i) {
-    if (hipEventCreate(&m->ev_start[i]) != hipSuccess || hipEventCreate(&m->ev_stop[i]) != hipSuccess) {
-      release_events(m);
-      return fail(HS_E_DEVICE, "hs_model_set_timing: hipEventCreate failed");
-    }
-  }
-  m->timing_mask = kind_mask;
-  return HS_OK;
-}
-
-int hs_model_timing(hs_model *m, int32_t n_kinds, double *total_ms, int64_t *launches, int64_t *dropped) {
-  if (!m || !total_ms || !launches || n_kinds < 0) return fail(HS_E_INVALID, "hs_model_timing: bad argument");
-  HIP_TRY(hipDeviceSynchronize());
-  for (int k = 0; k < n_kinds; ++k) {
-    total_ms[k] = 0.0;
-    launches[k] = 0;
-  }
-  for (int i = 0; i < m->ev_used; ++i) {
-    float ms = 0.f;
-    HIP_TRY(hipEventElapsedTime(&ms, m->ev_start[i], m->ev_stop[i]));
-    const int k = m->ev_kind[i];
-    if (k >= 0 && k < n_kinds) {
-      total_ms[k] += ms;
-      launches[k] += 1;
-    }
-  }
-  if (dropped) *dropped = m->ev_dropped;
-  m->ev_used = 0;
-  m->ev_dropped = 0;
-  return HS_OK;
-}
-
 int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *capacity, void *dev_buf,
                 uint64_t buf_bytes, hs_kv **out) {
   if (!out) return fail(HS_E_INVALID, "hs_kv_alloc: out is NULL");
@@ -502,11 +478,13 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
   const int S = s_ctx, ns = 1;
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
-  int rc = run_layers(m, kv, s_ctx, req, pos_thw, S, ns, st);
+  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, st};
+  int rc = pre.layers();
   if (rc) return rc;
   float *lg = last_logits ? last_logits : m->logits;
-  rc = run_head(m, m->x + (int64_t)(s_ctx - 1) * c.d_model, 1, lg, st);
-  if (rc) return rc;
+  Step last = pre;
+  last.ncols = 1;
+  HIP_TRY(last.head(m->x + (int64_t)(s_ctx - 1) * c.d_model, lg));
   HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, 1, first_token, nullptr, nullptr, 0, st));
   HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, req, s_ctx, pos_thw, st));
   kv->len[req] = s_ctx;
@@ -520,37 +498,58 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
   if (!tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_in is NULL");
   const hs_config &c = m->cfg;
   const int B = kv->batch;
-  if (B > m->max_batch) return fail(HS_E_INVALID, "hs_decode_step: batch %d exceeds max_batch %d", B, m->max_batch);
   if (m->w.lm_head) {
     if (!tokens_out) return fail(HS_E_INVALID, "hs_decode_step: tokens_out is NULL");
     if (tokens_out == tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_out aliases tokens_in");
   } else if (logits) {
     return fail(HS_E_INVALID, "hs_decode_step: model has no LM head, logits must be NULL");
   }
-  for (int b = 0; b < B; ++b) {
-    if (!kv->ready[b]) return fail(HS_E_STATE, "hs_decode_step: request %d is not prefilled", b);
-    if (kv->len[b] >= kv->cap[b])
-      return fail(HS_E_CAPACITY, "hs_decode_step: request %d is full (%d positions)", b, kv->cap[b]);
-  }
-  int S, ns;
-  split_policy(B, c.n_kv_heads, kv->max_cap, &S, &ns);
-  if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
-    return fail(HS_E_INVALID, "hs_decode_step: attention workspace too small");
   hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(timed(m, HS_K_EMBED, [&] { return launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st); }));
-  int rc = run_layers(m, kv, B, -1, kv->d_rope, S, ns, st);
+  Step step;
+  int rc = decode_step_args(m, kv, st, &step);
+  if (rc) return rc;
+  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st));
+  rc = step.layers();
   if (rc) return rc;
   if (hidden_out)
     HIP_TRY(hipMemcpyAsync(hidden_out, m->x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
   if (m->w.lm_head) {
     float *lg = logits ? logits : m->logits;
-    rc = run_head(m, m->x, B, lg, st);
-    if (rc) return rc;
-    HIP_TRY(timed(m, HS_K_ARGMAX, [&] { return launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st); }));
+    HIP_TRY(step.head(m->x, lg));
+    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st));
   } else {
-    HIP_TRY(timed(m, HS_K_ARGMAX, [&] { return launch_advance(kv->d_len, kv->d_rope, B, st); }));
+    HIP_TRY(launch_advance(kv->d_len, kv->d_rope, B, st));
   }
   for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  return HS_OK;
+}
+
+int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_stream_t stream) {
+  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_replay_kernels: model/handle mismatch");
+  if (count < 0) return fail(HS_E_INVALID, "hs_replay_kernels: negative count");
+  hipStream_t st = (hipStream_t)stream;
+  Step step;
+  int rc = decode_step_args(m, kv, st, &step);
+  if (rc) return rc;
+  const int L = m->cfg.n_layers;
+  if (kind == HS_K_HEAD && !m->w.lm_head) return fail(HS_E_STATE, "hs_replay_kernels: model has no LM head");
+  if (kind == HS_K_COMBINE && step.n_split <= 1)
+    return fail(HS_E_STATE, "hs_replay_kernels: this batch runs attention in one split");
+  for (int i = 0; i < count; ++i) {
+    const int l = i % L;
+    hipError_t e;
+    switch (kind) {
+      case HS_K_QKV: e = step.qkv(l); break;
+      case HS_K_ATTN: e = step.attn(l); break;
+      case HS_K_COMBINE: e = step.combine(l); break;
+      case HS_K_OPROJ: e = step.oproj(l); break;
+      case HS_K_GATEUP: e = step.gateup(l); break;
+      case HS_K_DOWN: e = step.down(l); break;
+      case HS_K_HEAD: e = step.head(m->x, m->logits); break;
+      default: return fail(HS_E_INVALID, "hs_replay_kernels: kind %d cannot be replayed", kind);
+    }
+    HIP_TRY(e);
+  }
   return HS_OK;
 }
 

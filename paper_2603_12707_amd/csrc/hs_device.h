@@ -7,10 +7,8 @@
 
 #include <cmath>
 
-// every launch carries the timing hook's events (null when untimed)
-#define HS_LAUNCH(kernel, grid, block, shmem, stream, ...)                                                        \
-  hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, hs::g_launch_events.start, hs::g_launch_events.stop, \
-                        0, __VA_ARGS__)
+#define HS_LAUNCH(kernel, grid, block, shmem, stream, ...) \
+  hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__)
 
 namespace hs {
 namespace dev {

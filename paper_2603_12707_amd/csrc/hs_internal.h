@@ -2,7 +2,6 @@
 // kernel launchers.  Not part of the C ABI.
 #pragma once
 
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -75,13 +74,6 @@ struct AttnArgs {
   void *out;       // combined output, model dtype [nq][n_heads * head_dim]
 };
 
-// Event pair attached to the next kernel launch (per-kernel timing hook);
-// both null for an ordinary launch.
-struct LaunchEvents {
-  hipEvent_t start = nullptr, stop = nullptr;
-};
-extern thread_local LaunchEvents g_launch_events;
-
 hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st);
 hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, hipStream_t st);
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
@@ -117,12 +109,6 @@ struct hs_model {
   float *part_ml = nullptr;
   float *rope_tab = nullptr; // [max_ctx][d_h / 2][2]
   int *status = nullptr;
-  // per-kernel timing (measurement hook)
-  int timing_mask = 0;
-  std::vector<hipEvent_t> ev_start, ev_stop;
-  std::vector<int> ev_kind;
-  int ev_used = 0;
-  int64_t ev_dropped = 0;
 };
 
 struct hs_kv {

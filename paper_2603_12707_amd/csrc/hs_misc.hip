@@ -3,9 +3,6 @@
 #include "hs_device.h"
 
 namespace hs {
-
-thread_local LaunchEvents g_launch_events;
-
 namespace {
 
 using namespace dev;

@@ -20,8 +20,7 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length", "hs_model_set_timing", "hs_model_timing", "hs_packed_bytes",
-           "hs_pack_matrix")
+           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -85,10 +84,9 @@ def lib() -> ctypes.CDLL:
         "hs_kv_write": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_read": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_set_length": [P, I32, I32, I32],
-        "hs_model_set_timing": [P, I32, I32],
+        "hs_replay_kernels": [P, P, I32, I32, P],
         "hs_packed_bytes": [I32, I64, I64, ctypes.POINTER(U64)],
         "hs_pack_matrix": [I32, P, I64, I64, P, P],
-        "hs_model_timing": [P, I32, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -211,20 +209,6 @@ class Model:
         _call("hs_model_status", self.handle, ctypes.byref(f))
         return f.value
 
-    def set_timing(self, kinds, max_launches: int) -> None:
-        mask = 0
-        for k in kinds:
-            mask |= 1 << HS_K_NAMES.index(k)
-        _call("hs_model_set_timing", self.handle, mask, max_launches)
-
-    def timing(self) -> dict:
-        n = len(HS_K_NAMES)
-        ms, cnt, dropped = (ctypes.c_double * n)(), (ctypes.c_int64 * n)(), ctypes.c_int64()
-        _call("hs_model_timing", self.handle, n, ms, cnt, ctypes.byref(dropped))
-        out = {k: (ms[i], cnt[i]) for i, k in enumerate(HS_K_NAMES) if cnt[i]}
-        out["dropped"] = dropped.value
-        return out
-
     def close(self) -> None:
         if self.handle:
             _call("hs_model_free", self.handle)
@@ -282,6 +266,10 @@ class KVCache:
 
     def read(self, req: int, layer: int, kv_sel: int, head: int, pos0: int, n: int, out) -> None:
         _call("hs_kv_read", self.handle, req, layer, kv_sel, head, pos0, n, _ptr(out), int(out.is_cuda))
+
+    def replay(self, kind: str, count: int) -> None:
+        """Launches `count` kernels of one kind back to back (measurement)."""
+        _call("hs_replay_kernels", self.model.handle, self.handle, HS_K_NAMES.index(kind), count, _stream())
 
     def set_length(self, req: int, length: int, rope_pos: int) -> None:
         _call("hs_kv_set_length", self.handle, req, length, rope_pos)
