@@ -63,12 +63,26 @@ int check_config(const hs_config *c) {
   return HS_OK;
 }
 
-// Attention splits: one work group per (query, KV head) covers all positions
-// unless there are too few such pairs to give every CU a work group; then the
+// Attention work decomposition for nq queries of at most max_len positions.
+// One work group per (query, KV head) covers all positions unless there are
+// too few such pairs to give every CU a work group.  Query-head groups of at
+// most two then first widen the work group to ATTN_WAVES_WIDE waves (one
+// split as long as every wave keeps two load blocks or fewer), otherwise the
 // positions are cut into up to that many splits of at least ATTN_MIN_SPLIT
 // positions each (S, the positions per split, is a multiple of 64).
-void split_policy(int nq, int n_kv, int max_len, int *S, int *n_split) {
+void split_policy(int nq, int n_kv, int group, int max_len, int *S, int *n_split, int *waves) {
   const int64_t pairs = (int64_t)nq * n_kv;
+  *waves = ATTN_WAVES;
+  if (group <= 2 && pairs < 256) {
+    const int per_wg = ATTN_WAVES_WIDE * 4 * 8 * 2;  // waves x positions per load x block x 2 blocks
+    *waves = ATTN_WAVES_WIDE;
+    const int ns = std::min((max_len + per_wg - 1) / per_wg, ATTN_MAX_SPLITS);
+    int s = (max_len + ns - 1) / ns;
+    s = (s + 63) / 64 * 64;
+    *S = s;
+    *n_split = (max_len + s - 1) / s;
+    return;
+  }
   const int want = (int)std::max<int64_t>(1, (256 + pairs - 1) / pairs);
   const int most = std::max(1, max_len / ATTN_MIN_SPLIT);
   int ns = std::min(std::min(want, most), ATTN_MAX_SPLITS);
@@ -98,7 +112,7 @@ struct Step {
   hs_kv *kv;
   int ncols, prefill_req;
   const int *rope_pos;
-  int S, n_split;
+  int S, n_split, waves;
   hipStream_t st;
 
   hipError_t qkv(int l) const {
@@ -156,6 +170,7 @@ struct Step {
     a.prefill_req = prefill_req;
     a.S = S;
     a.n_split = n_split;
+    a.waves = waves;
     a.part_o = m->part_o;
     a.part_ml = m->part_ml;
     a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
@@ -245,11 +260,11 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out) {
     if (!kv->ready[b]) return fail(HS_E_STATE, "decode: request %d is not prefilled", b);
     if (kv->len[b] >= kv->cap[b]) return fail(HS_E_CAPACITY, "decode: request %d is full (%d positions)", b, kv->cap[b]);
   }
-  int S, ns;
-  split_policy(B, c.n_kv_heads, kv->max_cap, &S, &ns);
+  int S, ns, waves;
+  split_policy(B, c.n_kv_heads, c.n_heads / c.n_kv_heads, kv->max_cap, &S, &ns, &waves);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
-  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, st};
+  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, waves, st};
   return HS_OK;
 }
 
@@ -331,13 +346,14 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   // decode batch <= max_batch with capacities <= max_ctx, or any prefill of
   // <= max_ctx rows, can ask for
   int64_t entries = 0;
+  const int group = c.n_heads / c.n_kv_heads;
   for (int nq = 1; nq <= max_batch; ++nq) {
-    int S, ns;
+    int S, ns, waves;
     for (int len = 1; len <= max_ctx; len += std::max(1, len / 64)) {
-      split_policy(nq, c.n_kv_heads, len, &S, &ns);
+      split_policy(nq, c.n_kv_heads, group, len, &S, &ns, &waves);
       if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
     }
-    split_policy(nq, c.n_kv_heads, max_ctx, &S, &ns);
+    split_policy(nq, c.n_kv_heads, group, max_ctx, &S, &ns, &waves);
     if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
   }
   m->part_entries = entries;
@@ -478,7 +494,7 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
   const int S = s_ctx, ns = 1;
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
-  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, st};
+  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, ATTN_WAVES, st};
   int rc = pre.layers();
   if (rc) return rc;
   float *lg = last_logits ? last_logits : m->logits;

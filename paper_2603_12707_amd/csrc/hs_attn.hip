@@ -21,7 +21,7 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
   return m_part == -INFINITY ? 0.f : expf(m_part - m_all);
 }
 
-// One work group = (split, KV head j, query).  Each of its ATTN_WAVES waves walks
+// One work group = (split, KV head j, query).  Each of its NW waves walks
 // its share of the split's positions (LPT lanes per position, one 16-byte
 // chunk of the K row and of the V row per lane); loads are issued a block of
 // UB position groups ahead of their use (double-buffered), and every position
@@ -29,13 +29,12 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
 // groups are merged with lane shuffles, the waves through LDS.  With a single
 // split the work group writes the normalised output, otherwise the split's
 // unnormalised partial o, its max m and its sum l.
-template <int DT, int HD, int G>
-__global__ __launch_bounds__(64 * ATTN_WAVES) void k_attn(AttnArgs a) {
+template <int DT, int HD, int G, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   using S = typename Ty<DT>::S;
   constexpr int CE = Ty<DT>::CE;
   constexpr int LPT = HD / CE;
   constexpr int TPW = 64 / LPT;           // positions per wave-wide load
-  constexpr int NW = ATTN_WAVES;
   constexpr int STEP = NW * TPW;          // positions per work-group iteration
   constexpr int UB = G <= 2 ? 8 : 4;      // iterations per block of loads
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
@@ -204,13 +203,20 @@ __global__ __launch_bounds__(HD) void k_combine(AttnArgs a) {
 
 template <int DT, int HD>
 hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
-  const dim3 grid(a.n_split, a.n_kv, nq), block(64 * ATTN_WAVES);
+  const dim3 grid(a.n_split, a.n_kv, nq);
+  const bool wide = a.waves == ATTN_WAVES_WIDE;
   switch (group) {
-    case 1: HS_LAUNCH((k_attn<DT, HD, 1>), grid, block, 0, st, a); break;
-    case 2: HS_LAUNCH((k_attn<DT, HD, 2>), grid, block, 0, st, a); break;
-    case 4: HS_LAUNCH((k_attn<DT, HD, 4>), grid, block, 0, st, a); break;
-    case 7: HS_LAUNCH((k_attn<DT, HD, 7>), grid, block, 0, st, a); break;
-    case 8: HS_LAUNCH((k_attn<DT, HD, 8>), grid, block, 0, st, a); break;
+    case 1:
+      if (wide) HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES_WIDE>), grid, dim3(64 * ATTN_WAVES_WIDE), 0, st, a);
+      else HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a);
+      break;
+    case 2:
+      if (wide) HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES_WIDE>), grid, dim3(64 * ATTN_WAVES_WIDE), 0, st, a);
+      else HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a);
+      break;
+    case 4: HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
+    case 7: HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
+    case 8: HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -6,6 +6,7 @@
 #include "hs_internal.h"
 
 #include <cmath>
+#include <type_traits>
 
 #define HS_LAUNCH(kernel, grid, block, shmem, stream, ...) \
   hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__)
@@ -128,6 +129,32 @@ __device__ __forceinline__ f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
 __device__ __forceinline__ u32x4 ld16(const void *p) { return *(const u32x4 *)p; }
 __device__ __forceinline__ u32x4 ld16_stream(const void *p) {
   return __builtin_nontemporal_load((const u32x4 *)p);
+}
+
+// ---------------------------------------------------------------------------
+// raw buffer reads
+// ---------------------------------------------------------------------------
+// A buffer resource covers the byte range [base, base + bytes); a read at an
+// offset past it returns zeros without touching memory.  Loads that may fall
+// outside their data therefore need no branch, which keeps the compiler's
+// count of outstanding loads exact (a branch around a load makes it wait for
+// all of them).  Ranges stay below BUF_OOB, the offset used for "no data".
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t BUF_OOB = 0x80000000u;
+constexpr int BUF_WORD3 = 0x00020000;  // raw access, 32-bit data format
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, BUF_WORD3);
+}
+__device__ __forceinline__ u32x4 bld16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+// non-temporal: data read once per step (the weight stream)
+__device__ __forceinline__ u32x4 bld16_stream(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2));
+}
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 bld8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
 // ---------------------------------------------------------------------------

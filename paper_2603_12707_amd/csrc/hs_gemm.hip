@@ -179,138 +179,198 @@ __device__ __forceinline__ double sumsq_f64(f32x4 v) {
   return (double)v[0] * v[0] + (double)v[1] * v[1] + (double)v[2] * v[2] + (double)v[3] * v[3];
 }
 
+// Normalised activations h = x * rs * gain for the 4 consecutive k values of
+// one float4 of x, rounded to the storage dtype and written to the LDS copy.
+template <int DT>
+__device__ __forceinline__ void put_h(unsigned char *s_x, int64_t at, f32x4 v, float rs, const float *g) {
+  float h[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) h[e] = v[e] * rs * g[e];
+  if constexpr (DT == HS_F32) {
+    *(f32x4 *)((float *)s_x + at) = f32x4{h[0], h[1], h[2], h[3]};
+  } else {
+    uint32_t w0, w1;
+    if constexpr (DT == HS_F16) {
+      w0 = f32_to_f16(h[0]) | (f32_to_f16(h[1]) << 16);
+      w1 = f32_to_f16(h[2]) | (f32_to_f16(h[3]) << 16);
+    } else {
+      w0 = f32_to_bf16(h[0]) | (f32_to_bf16(h[1]) << 16);
+      w1 = f32_to_bf16(h[2]) | (f32_to_bf16(h[3]) << 16);
+    }
+    *(u32x2 *)((uint16_t *)s_x + at) = u32x2{w0, w1};
+  }
+}
+
+// 4 gain values starting at element k (k a multiple of 4)
+template <int DT>
+__device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
+  if constexpr (DT == HS_F32) {
+    const u32x4 v = bld16(gr, ok ? (uint32_t)k * 4u : BUF_OOB);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) g[e] = __uint_as_float(v[e]);
+  } else {
+    const u32x2 v = bld8(gr, ok ? (uint32_t)k * 2u : BUF_OOB);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      g[2 * e] = DT == HS_F16 ? f16_to_f32(v[e] & 0xFFFFu) : bf16_to_f32(v[e] & 0xFFFFu);
+      g[2 * e + 1] = DT == HS_F16 ? f16_to_f32(v[e] >> 16) : bf16_to_f32(v[e] >> 16);
+    }
+  }
+}
+
 // Y[c][n] = sum_k X[c][k] W[n][k] over R row tiles and NT column tiles of 16.
 //
 // The NW waves of a work group split the packed k-blocks round robin, so that
-// together they read consecutive kilobytes; each wave keeps two groups of U
-// k-blocks of loads in flight (non-temporal: every weight byte is read once
-// per step).
-// X comes from the activation rows in global memory (L2-resident), from the
-// fp32 residual stream normalised on the fly (PRO_NORM, XS = 0), or, when the
-// work group's columns are few (XS = 1), from a copy normalised once into LDS.
-// The waves' partial tiles are summed in a fixed order through LDS and handed
-// to the epilogue.
+// together they read consecutive kilobytes.  Each wave keeps a ring of two
+// groups of U k-blocks of weight loads in flight (non-temporal: every weight
+// byte is read once per step); a group is refilled as soon as its MFMAs are
+// issued.  The loads are raw buffer reads whose ranges end where the data
+// ends, so that no load sits behind a branch; the ring runs a whole number
+// of rounds, and groups past the wave's last k-block read zeros.
+// X comes from a copy in LDS (XS = 1: the work group's columns are few; with
+// PRO_NORM the copy holds the normalised activations, with the first column's
+// x requested before the weights), from the activation rows in global memory
+// (PRO_PLAIN, XS = 0), or from the fp32 residual stream normalised on the fly
+// (PRO_NORM, XS = 0).  The waves' partial tiles are summed in a fixed order
+// through LDS and handed to the epilogue.
 template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
 __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   using S = typename Ty<DT>::S;
   constexpr int CE = Ty<DT>::CE;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int SB = (int)sizeof(S);
+  constexpr int D = 2;  // groups of weight loads in flight per wave
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lq = lane >> 4;
   const int col0 = blockIdx.y * 16 * NT;
   const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4;
+  const int nst = min(a.ncols - col0, 16 * NT);
 
   int mat[R], row0[R];
   tile_map<EPI, R>(a, blockIdx.x, mat, row0);
-  const S *wp[R];
+  // one range per row tile: its packed k-blocks (4 KB each); empty past the matrix
+  rsrc_t wr[R];
 #pragma unroll
   for (int r = 0; r < R; ++r)
-    wp[r] = row0[r] < a.rows[mat[r]] ? (const S *)a.w[mat[r]] + ((int64_t)(row0[r] >> 4) * nkb * 256 + lane) * CE
-                                     : nullptr;
-
-  // weight loads of one group of U k-blocks (k-blocks kb0, kb0 + NW, ...)
-  auto load_w = [&](u32x4 (&wv)[U][R][4], int kb0) {
+    wr[r] = make_rsrc((const S *)a.w[mat[r]] + (int64_t)(row0[r] >> 4) * nkb * 256 * CE,
+                      row0[r] < a.rows[mat[r]] ? (uint32_t)nkb * 4096u : 0u);
+  // group g of this wave: k-blocks wave + (g * U + u) * NW
+  auto load_w = [&](u32x4 (&wv)[U][R][4], int g) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kb = kb0 + u * NW;
+      const int kb = wave + (g * U + u) * NW;
+      const uint32_t off = kb < nkb ? (uint32_t)kb * 4096u + (uint32_t)lane * 16u : BUF_OOB;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-          wv[u][r][s] = (wp[r] && kb < nkb) ? ld16_stream(wp[r] + (int64_t)(kb * 4 + s) * 64 * CE)
-                                            : u32x4{0u, 0u, 0u, 0u};
+        for (int r = 0; r < R; ++r) wv[u][r][s] = bld16_stream(wr[r], off + s * 1024u);
     }
   };
-  // the first group is issued before the prologue so that its HBM latency
-  // overlaps the normalisation of the activations
-  u32x4 wcur[U][R][4], wnxt[U][R][4];
-  load_w(wcur, wave);
 
+  const rsrc_t gr = make_rsrc(a.gain, PRO == PRO_NORM ? (uint32_t)K * SB : 0u);
+  // x of the work group's columns: fp32 residual rows (PRO_NORM) or activation rows
+  const rsrc_t xr = PRO == PRO_NORM ? make_rsrc((const float *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * 4u)
+                                    : make_rsrc((const S *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * SB);
   __shared__ float s_rsq[16 * NT];
   __shared__ double s_part[NW];
-  extern __shared__ __align__(16) unsigned char s_x[];  // XS: normalised activations [nst][K]
-  const int nst = min(a.ncols - col0, 16 * NT);
+  extern __shared__ __align__(16) unsigned char s_x[];  // XS: activations [nst][K]
+
+  // requested before the weights so that the prologue waits for them alone
+  constexpr int PER = 4;
+  f32x4 xv[PER];
+  float gv[PER][4];
+  u32x4 xc[PER];
+  if constexpr (XS == 1 && PRO == PRO_NORM) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int k = (u * 64 * NW + (int)threadIdx.x) * 4;
+      xv[u] = __builtin_bit_cast(f32x4, bld16(xr, k < K ? (uint32_t)k * 4u : BUF_OOB));
+      gain4<DT>(gr, k, k < K, gv[u]);
+    }
+  } else if constexpr (XS == 1) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = u * 64 * NW + (int)threadIdx.x;  // 16-byte chunk of the staged rows
+      xc[u] = bld16(xr, i < nst * kchunks ? (uint32_t)i * 16u : BUF_OOB);
+    }
+  }
+
+  u32x4 w[D][U][R][4];
+#pragma unroll
+  for (int d = 0; d < D; ++d) load_w(w[d], d);
+
   if constexpr (PRO == PRO_NORM && XS == 1) {
-    // one pass over each staged column: its x values stay in registers
-    // between the sum of squares and the scaling
-    const float *x = (const float *)a.x;
-    constexpr int PER = 8;  // float4 per thread and pass (K <= 8 * 4 * 64 * NW)
-    for (int c = 0; c < nst; ++c) {
-      const float *xr = x + (int64_t)(col0 + c) * K;
-      f32x4 xv[PER];
+    // one pass over each staged column; the first column's x (already
+    // requested) stays in registers between its sum of squares and its
+    // scaling, in the same straight-line code as its loads
+    auto stage = [&](int c) {
       double ss = 0.0;
 #pragma unroll
-      for (int u = 0; u < PER; ++u) {
-        const int k = (u * 64 * NW + threadIdx.x) * 4;
-        xv[u] = k < K ? *(const f32x4 *)(xr + k) : f32x4{0.f, 0.f, 0.f, 0.f};
-        ss += sumsq_f64(xv[u]);
-      }
-      for (int k0 = PER * 256 * NW; k0 < K; k0 += 256 * NW) {  // columns longer than one pass
-        const int k = k0 + threadIdx.x * 4;
-        if (k < K) ss += sumsq_f64(*(const f32x4 *)(xr + k));
-      }
+      for (int u = 0; u < PER; ++u) ss += sumsq_f64(xv[u]);
+      for (int k = (PER * 64 * NW + (int)threadIdx.x) * 4; k < K; k += 256 * NW)  // columns longer than one pass
+        ss += sumsq_f64(__builtin_bit_cast(f32x4, bld16(xr, (uint32_t)(c * K + k) * 4u)));
       const float rs = (float)(1.0 / sqrt(block_sum<NW>(ss, s_part) / (double)K + (double)a.eps));
-      auto put = [&](int k, f32x4 v) {
-        float h[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) h[e] = v[e] * rs * ld_elem<DT>(a.gain, k + e);
-        if constexpr (DT == HS_F32) {
-          *(f32x4 *)((float *)s_x + (int64_t)c * K + k) = f32x4{h[0], h[1], h[2], h[3]};
-        } else {
-          uint32_t w0, w1;
-          if constexpr (DT == HS_F16) {
-            w0 = f32_to_f16(h[0]) | (f32_to_f16(h[1]) << 16);
-            w1 = f32_to_f16(h[2]) | (f32_to_f16(h[3]) << 16);
-          } else {
-            w0 = f32_to_bf16(h[0]) | (f32_to_bf16(h[1]) << 16);
-            w1 = f32_to_bf16(h[2]) | (f32_to_bf16(h[3]) << 16);
-          }
-          uint32_t *dst = (uint32_t *)((uint16_t *)s_x + (int64_t)c * K + k);
-          dst[0] = w0;
-          dst[1] = w1;
-        }
-      };
 #pragma unroll
       for (int u = 0; u < PER; ++u) {
-        const int k = (u * 64 * NW + threadIdx.x) * 4;
-        if (k < K) put(k, xv[u]);
+        const int k = (u * 64 * NW + (int)threadIdx.x) * 4;
+        if (k < K) put_h<DT>(s_x, (int64_t)c * K + k, xv[u], rs, gv[u]);
       }
-      for (int k0 = PER * 256 * NW; k0 < K; k0 += 256 * NW) {
-        const int k = k0 + threadIdx.x * 4;
-        if (k < K) put(k, *(const f32x4 *)(xr + k));
+      for (int k = (PER * 64 * NW + (int)threadIdx.x) * 4; k < K; k += 256 * NW) {
+        float g[4];
+        gain4<DT>(gr, k, true, g);
+        put_h<DT>(s_x, (int64_t)c * K + k,
+                  __builtin_bit_cast(f32x4, bld16(xr, (uint32_t)(c * K + k) * 4u)), rs, g);
       }
+    };
+    stage(0);
+    for (int c = 1; c < nst; ++c) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int k = (u * 64 * NW + (int)threadIdx.x) * 4;
+        xv[u] = __builtin_bit_cast(f32x4, bld16(xr, k < K ? (uint32_t)(c * K + k) * 4u : BUF_OOB));
+      }
+      stage(c);
     }
     __syncthreads();
+  } else if constexpr (XS == 1) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = u * 64 * NW + (int)threadIdx.x;
+      if (i < nst * kchunks) *(u32x4 *)(s_x + (int64_t)i * 16) = xc[u];
+    }
+    for (int i = PER * 64 * NW + (int)threadIdx.x; i < nst * kchunks; i += 64 * NW)
+      *(u32x4 *)(s_x + (int64_t)i * 16) = bld16(xr, (uint32_t)i * 16u);
+    __syncthreads();
   } else if constexpr (PRO == PRO_NORM) {
-    const float *x = (const float *)a.x;
     for (int c = wave; c < 16 * NT; c += NW) {
-      const int col = col0 + c;
       double ss = 0.0;
-      if (col < a.ncols) {
-        const float *xr = x + (int64_t)col * K;
-        for (int k = lane * 4; k < K; k += 256) ss += sumsq_f64(*(const f32x4 *)(xr + k));
-      }
+      if (c < nst)
+        for (int k = lane * 4; k < K; k += 256)
+          ss += sumsq_f64(__builtin_bit_cast(f32x4, bld16(xr, (uint32_t)(c * K + k) * 4u)));
       ss = wave_sum_f64(ss);
       if (lane == 0) s_rsq[c] = (float)(1.0 / sqrt(ss / (double)K + (double)a.eps));
     }
     __syncthreads();
   }
 
+  // chunk kc of column 16 t + li of the work group; zero past the data
   auto load_x = [&](int t, int kc) -> u32x4 {
-    const int c = 16 * t + li, col = col0 + c;
-    if (col >= a.ncols || kc >= kchunks) return u32x4{0u, 0u, 0u, 0u};
-    if constexpr (PRO == PRO_PLAIN) {
-      return ld16((const S *)a.x + (int64_t)col * K + (int64_t)kc * CE);
-    } else if constexpr (XS == 1) {
-      return *(const u32x4 *)((const S *)s_x + (int64_t)c * K + (int64_t)kc * CE);
+    const int c = 16 * t + li;
+    const bool ok = c < nst && kc < kchunks;
+    if constexpr (XS == 1) {
+      const u32x4 v = *(const u32x4 *)((const S *)s_x + (ok ? (int64_t)c * K + (int64_t)kc * CE : 0));
+      return ok ? v : u32x4{0u, 0u, 0u, 0u};
+    } else if constexpr (PRO == PRO_PLAIN) {
+      return bld16(xr, ok ? (uint32_t)(c * K + kc * CE) * SB : BUF_OOB);
     } else {
-      const float *xr = (const float *)a.x + (int64_t)col * K + (int64_t)kc * CE;
+      const uint32_t xo = ok ? (uint32_t)(c * K + kc * CE) * 4u : BUF_OOB;
       const float rs = s_rsq[c];
-      float xv[CE], gv[CE], h[CE];
-      unpack<HS_F32>(ld16(xr), xv);
-      if constexpr (CE == 8) unpack<HS_F32>(ld16(xr + 4), xv + 4);
-      unpack<DT>(ld16((const S *)a.gain + (int64_t)kc * CE), gv);
+      float xe[CE], ge[CE], h[CE];
+      unpack<HS_F32>(bld16(xr, xo), xe);
+      if constexpr (CE == 8) unpack<HS_F32>(bld16(xr, xo + 16u), xe + 4);
+      unpack<DT>(bld16(gr, ok ? (uint32_t)kc * 16u : BUF_OOB), ge);
 #pragma unroll
-      for (int e = 0; e < CE; ++e) h[e] = xv[e] * rs * gv[e];
+      for (int e = 0; e < CE; ++e) h[e] = xe[e] * rs * ge[e];
       return pack<DT>(h);
     }
   };
@@ -331,43 +391,40 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         for (int e = 0; e < 4; ++e) acc64[r][t][e] = 0.0;
     }
 
-  // software pipeline: activations of this group, weights of the next
-  // group, then the MFMAs of this group (which wait only for the former)
-  for (int kb0 = wave; kb0 < nkb; kb0 += NW * U) {
-    u32x4 xb[U][NT][4];
+  const int nblk = wave < nkb ? (nkb - 1 - wave) / NW + 1 : 0;  // k-blocks of this wave
+  const int ng = (nblk + U - 1) / U;
+  for (int g0 = 0; g0 < ng; g0 += D) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int t = 0; t < NT; ++t) xb[u][t][s] = load_x(t, (kb0 + u * NW) * 16 + s * 4 + lq);
-    const bool more = kb0 + NW * U < nkb;
-    if (more) load_w(wnxt, kb0 + NW * U);
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int r = 0; r < R; ++r)
-#pragma unroll
-          for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(wcur[u][r][s], xb[u][t][s], acc[r][t]);
-    if constexpr (ACC64) {
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc64[r][t][e] += (double)acc[r][t][e];
-          acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-    }
-    if (more) {
+    for (int d = 0; d < D; ++d) {
+      const int g = g0 + d;
+      u32x4 xb[U][NT][4];
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) xb[u][t][s] = load_x(t, (wave + (g * U + u) * NW) * 16 + s * 4 + lq);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[r][t] = mma<DT>(w[d][u][r][s], xb[u][t][s], acc[r][t]);
+      if constexpr (ACC64) {
+#pragma unroll
         for (int r = 0; r < R; ++r)
 #pragma unroll
-          for (int s = 0; s < 4; ++s) wcur[u][r][s] = wnxt[u][r][s];
+          for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc64[r][t][e] += (double)acc[r][t][e];
+            acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+      }
+      load_w(w[d], g + D);
+      // keep the next group's MFMAs (which wait for its loads) below this refill
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -395,14 +452,14 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       if constexpr (ACC64) {
         double sum[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-        for (int w = 0; w < NW; ++w)
+        for (int w2 = 0; w2 < NW; ++w2)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sum[e] += s_red64[(((w * R + r) * NT + t) * 4 + e) * 64 + ln];
+          for (int e = 0; e < 4; ++e) sum[e] += s_red64[(((w2 * R + r) * NT + t) * 4 + e) * 64 + ln];
         v[r] = f32x4{(float)sum[0], (float)sum[1], (float)sum[2], (float)sum[3]};
       } else {
         v[r] = s_red[((0 * R + r) * NT + t) * 64 + ln];
 #pragma unroll
-        for (int w = 1; w < NW; ++w) v[r] += s_red[((w * R + r) * NT + t) * 64 + ln];
+        for (int w2 = 1; w2 < NW; ++w2) v[r] += s_red[((w2 * R + r) * NT + t) * 64 + ln];
       }
     }
     const int col = col0 + 16 * t + (ln & 15);
@@ -432,7 +489,7 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   // k-blocks per pipelined group at one column tile: two for single row
   // tiles; one for paired tiles, whose registers would otherwise halve the
   // resident work groups
-  constexpr int U1 = R == 2 ? 1 : 2;
+  constexpr int U1 = (R == 2 || NW == 8) ? 1 : 2;
   // one work group per R row tiles (q/k/v: per pair of RoPE half-tiles)
   const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 32
                                       : (a.rows[0] + 16 * (EPI == EPI_SWIGLU ? 1 : R) - 1) /
@@ -440,10 +497,8 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   const int tiles = (a.ncols + 15) / 16;
   const int b = DT == HS_F32 ? 4 : 2;
   if (tiles <= 1) {
-    if constexpr (PRO == PRO_NORM) {
-      const size_t xs = (size_t)a.ncols * a.K * b;
-      if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
-    }
+    const size_t xs = (size_t)a.ncols * a.K * b;
+    if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
     return gemm_launch<DT, R, 1, NW, U1, PRO, 0, EPI>(a, n_groups, 0, st);
   }
   if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
