@@ -64,30 +64,22 @@ int check_config(const hs_config *c) {
 }
 
 // Attention work decomposition for nq queries of at most max_len positions.
-// One work group per (query, KV head) covers all positions unless there are
-// too few such pairs to give every CU a work group.  Query-head groups of at
-// most two then first widen the work group to ATTN_WAVES_WIDE waves (one
-// split as long as every wave keeps two load blocks or fewer), otherwise the
-// positions are cut into up to that many splits of at least ATTN_MIN_SPLIT
-// positions each (S, the positions per split, is a multiple of 64).
-void split_policy(int nq, int n_kv, int group, int max_len, int *S, int *n_split, int *waves) {
+// A work group covers one (query, KV head) and S consecutive positions.  The
+// positions of a pair are cut into splits until there are about two work
+// groups per CU, but no further than one batch of K/V loads per wave (round =
+// ATTN_WAVES x positions per wave-wide load x attn_batch(group)); S is a
+// multiple of the positions one work-group iteration covers.  Many pairs keep
+// one split each.
+void split_policy(int nq, int n_kv, int group, int head_dim, int dtype, int max_len, int *S, int *n_split) {
+  const int ce = dtype == HS_F32 ? 4 : 8;
+  const int step = ATTN_WAVES * (64 * ce / head_dim);
+  const int round = step * attn_batch(group);
   const int64_t pairs = (int64_t)nq * n_kv;
-  *waves = ATTN_WAVES;
-  if (group <= 2 && pairs < 256) {
-    const int per_wg = ATTN_WAVES_WIDE * 4 * 8 * 2;  // waves x positions per load x block x 2 blocks
-    *waves = ATTN_WAVES_WIDE;
-    const int ns = std::min((max_len + per_wg - 1) / per_wg, ATTN_MAX_SPLITS);
-    int s = (max_len + ns - 1) / ns;
-    s = (s + 63) / 64 * 64;
-    *S = s;
-    *n_split = (max_len + s - 1) / s;
-    return;
-  }
-  const int want = (int)std::max<int64_t>(1, (256 + pairs - 1) / pairs);
-  const int most = std::max(1, max_len / ATTN_MIN_SPLIT);
-  int ns = std::min(std::min(want, most), ATTN_MAX_SPLITS);
+  const int want = (int)std::max<int64_t>(1, (512 + pairs - 1) / pairs);
+  const int by_round = std::max(1, (max_len + round - 1) / round);
+  const int ns = std::min(std::min(want, by_round), ATTN_MAX_SPLITS);
   int s = (max_len + ns - 1) / ns;
-  s = (s + 63) / 64 * 64;
+  s = (s + step - 1) / step * step;
   *S = s;
   *n_split = (max_len + s - 1) / s;
 }
@@ -112,7 +104,7 @@ struct Step {
   hs_kv *kv;
   int ncols, prefill_req;
   const int *rope_pos;
-  int S, n_split, waves;
+  int S, n_split;
   hipStream_t st;
 
   hipError_t qkv(int l) const {
@@ -170,7 +162,6 @@ struct Step {
     a.prefill_req = prefill_req;
     a.S = S;
     a.n_split = n_split;
-    a.waves = waves;
     a.part_o = m->part_o;
     a.part_ml = m->part_ml;
     a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
@@ -260,11 +251,11 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out) {
     if (!kv->ready[b]) return fail(HS_E_STATE, "decode: request %d is not prefilled", b);
     if (kv->len[b] >= kv->cap[b]) return fail(HS_E_CAPACITY, "decode: request %d is full (%d positions)", b, kv->cap[b]);
   }
-  int S, ns, waves;
-  split_policy(B, c.n_kv_heads, c.n_heads / c.n_kv_heads, kv->max_cap, &S, &ns, &waves);
+  int S, ns;
+  split_policy(B, c.n_kv_heads, c.n_heads / c.n_kv_heads, c.head_dim, c.dtype, kv->max_cap, &S, &ns);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
-  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, waves, st};
+  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, st};
   return HS_OK;
 }
 
@@ -348,12 +339,12 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   int64_t entries = 0;
   const int group = c.n_heads / c.n_kv_heads;
   for (int nq = 1; nq <= max_batch; ++nq) {
-    int S, ns, waves;
+    int S, ns;
     for (int len = 1; len <= max_ctx; len += std::max(1, len / 64)) {
-      split_policy(nq, c.n_kv_heads, group, len, &S, &ns, &waves);
+      split_policy(nq, c.n_kv_heads, group, hd, c.dtype, len, &S, &ns);
       if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
     }
-    split_policy(nq, c.n_kv_heads, group, max_ctx, &S, &ns, &waves);
+    split_policy(nq, c.n_kv_heads, group, hd, c.dtype, max_ctx, &S, &ns);
     if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
   }
   m->part_entries = entries;
@@ -494,7 +485,7 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
   const int S = s_ctx, ns = 1;
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
-  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, ATTN_WAVES, st};
+  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, st};
   int rc = pre.layers();
   if (rc) return rc;
   float *lg = last_logits ? last_logits : m->logits;

@@ -23,20 +23,25 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
 
 // One work group = (split, KV head j, query).  Each of its NW waves walks
 // its share of the split's positions (LPT lanes per position, one 16-byte
-// chunk of the K row and of the V row per lane); loads are issued a block of
-// UB position groups ahead of their use (double-buffered), and every position
-// group keeps an online softmax for the G query heads of KV head j.  The
-// groups are merged with lane shuffles, the waves through LDS.  With a single
-// split the work group writes the normalised output, otherwise the split's
-// unnormalised partial o, its max m and its sum l.
+// chunk of the K row and of the V row per lane), requesting the chunks of UB
+// position groups at once; the split policy sizes splits so that one such
+// batch usually covers a wave's share.  Every position group keeps an online
+// softmax for the G query heads of KV head j.  The groups are merged with
+// lane shuffles, the waves through LDS.  With a single split the work group
+// writes the normalised output; otherwise every split writes its unnormalised
+// partial o, its max m and its sum l, a split past the query's positions
+// writing the neutral (o = 0, m = -inf, l = 0).
+// K/V are read through buffer ranges that end at the split's last position,
+// so that no load sits behind a branch.
 template <int DT, int HD, int G, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   using S = typename Ty<DT>::S;
   constexpr int CE = Ty<DT>::CE;
+  constexpr int SB = (int)sizeof(S);
   constexpr int LPT = HD / CE;
   constexpr int TPW = 64 / LPT;           // positions per wave-wide load
   constexpr int STEP = NW * TPW;          // positions per work-group iteration
-  constexpr int UB = G <= 2 ? 8 : 4;      // iterations per block of loads
+  constexpr int UB = attn_batch(G);       // iterations per batch of loads
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
   int req, L;
   if (a.prefill_req < 0) {
@@ -49,14 +54,26 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   const int cap = a.kv_cap[req];
   L = min(L, cap);
   const int t0 = split * a.S;
-  if (t0 >= L) return;
+  const int64_t qh = (int64_t)qi * a.n_heads + j * G;  // first (query, head) row of this group
+  if (t0 >= L) {
+    for (int idx = threadIdx.x; idx < G * HD; idx += 64 * NW) {
+      const int h = idx / HD, e = idx - h * HD;
+      a.part_o[((qh + h) * a.n_split + split) * HD + e] = 0.f;
+      if (e == 0) {
+        a.part_ml[((qh + h) * a.n_split + split) * 2] = -INFINITY;
+        a.part_ml[((qh + h) * a.n_split + split) * 2 + 1] = 0.f;
+      }
+    }
+    return;
+  }
   const int n = min(a.S, L - t0);
-  const int ns = (L + a.S - 1) / a.S;
   const int n_it = (n + STEP - 1) / STEP;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tg = lane / LPT, c = lane % LPT;
-  const S *Kp = (const S *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2) * a.n_kv + j) * cap * HD + c * CE;
-  const S *Vp = (const S *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap * HD + c * CE;
+  const S *kbase = (const S *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+  const S *vbase = (const S *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap + t0) * HD;
+  const rsrc_t kr = make_rsrc(kbase, (uint32_t)n * HD * SB), vr = make_rsrc(vbase, (uint32_t)n * HD * SB);
 
   float qf[G][CE];
 #pragma unroll
@@ -72,25 +89,22 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
     for (int e = 0; e < CE; ++e) o[h][e] = 0.f;
   }
   for (int it0 = 0; it0 < n_it; it0 += UB) {
-    // all K and V chunks of the block are requested before any is used
-    u32x4 kr[UB], vr[UB];
+    // all K and V chunks of the batch are requested before any is used;
+    // positions past the split read zeros
+    u32x4 kc[UB], vc[UB];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int tt = (it0 + u) * STEP + wave * TPW + tg;
-      if (it0 + u < n_it && tt < n) {
-        kr[u] = ld16(Kp + (int64_t)(t0 + tt) * HD);
-        vr[u] = ld16(Vp + (int64_t)(t0 + tt) * HD);
-      } else {
-        kr[u] = vr[u] = u32x4{0u, 0u, 0u, 0u};
-      }
+      const uint32_t off = (uint32_t)((it0 + u) * STEP + wave * TPW + tg) * (HD * SB) + (uint32_t)c * 16u;
+      kc[u] = bld16_stream(kr, off);
+      vc[u] = bld16_stream(vr, off);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int tt = (it0 + u) * STEP + wave * TPW + tg;
-      const bool valid = it0 + u < n_it && tt < n;
+      const bool valid = tt < n;
       float kf[CE], vf[CE];
-      unpack<DT>(kr[u], kf);
-      unpack<DT>(vr[u], vf);
+      unpack<DT>(kc[u], kf);
+      unpack<DT>(vc[u], vf);
 #pragma unroll
       for (int h = 0; h < G; ++h) {
         float d = 0.f;
@@ -139,7 +153,6 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
     }
   __syncthreads();
 
-  const int64_t qh = (int64_t)qi * a.n_heads + j * G;  // first (query, head) row of this group
   for (int idx = threadIdx.x; idx < G * HD; idx += 64 * NW) {
     const int h = idx / HD, e = idx - h * HD;
     float M = s_m[0][h];
@@ -152,7 +165,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
       num += wt * s_o[w][h][e];
       den += wt * s_l[w][h];
     }
-    if (ns == 1) {
+    if (a.n_split == 1) {
       st_elem<DT>(a.out, (qh + h) * HD + e, num / den);
     } else {
       a.part_o[((qh + h) * a.n_split + split) * HD + e] = num;
@@ -164,59 +177,63 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   }
 }
 
-// o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s over the splits that hold
-// positions, in split order; rounded to the storage dtype.  Queries whose
-// positions fit one split were finished by the attention kernel.
-template <int DT, int HD>
+// o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s over the n_split splits
+// of one (query, head), in split order (empty splits have weight zero);
+// rounded to the storage dtype.  NSF > 0: at most NSF splits, whose partials
+// are all requested at once.
+template <int DT, int HD, int NSF>
 __global__ __launch_bounds__(HD) void k_combine(AttnArgs a) {
   const int h = blockIdx.x, qi = blockIdx.y, e = threadIdx.x;
-  int req, L;
-  if (a.prefill_req < 0) {
-    req = qi;
-    L = a.kv_len[qi] + 1;
+  const int ns = a.n_split;
+  const int64_t base = ((int64_t)qi * a.n_heads + h) * ns;
+  float num = 0.f, den = 0.f;
+  if constexpr (NSF > 0) {
+    const rsrc_t mr = make_rsrc(a.part_ml + base * 2, (uint32_t)ns * 8u);
+    const rsrc_t orr = make_rsrc(a.part_o + base * HD, (uint32_t)ns * HD * 4u);
+    float m[NSF], l[NSF], o[NSF];
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp) {
+      const u32x2 ml = bld8(mr, (uint32_t)sp * 8u);
+      m[sp] = __uint_as_float(ml[0]);
+      l[sp] = __uint_as_float(ml[1]);
+      o[sp] = __uint_as_float(bld4(orr, (uint32_t)(sp * HD + e) * 4u));
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp)
+      if (sp < ns) M = fmaxf(M, m[sp]);
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp)
+      if (sp < ns) {
+        const float w = expf(m[sp] - M);
+        den += w * l[sp];
+        num += w * o[sp];
+      }
   } else {
-    req = a.prefill_req;
-    L = qi + 1;
+    __shared__ float s_m[ATTN_MAX_SPLITS], s_w[ATTN_MAX_SPLITS];
+    for (int sp = e; sp < ns; sp += HD) s_m[sp] = a.part_ml[(base + sp) * 2];
+    __syncthreads();
+    float M = -INFINITY;
+    for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, s_m[sp]);
+    for (int sp = e; sp < ns; sp += HD) s_w[sp] = expf(s_m[sp] - M);
+    __syncthreads();
+    for (int sp = 0; sp < ns; ++sp) {
+      den += s_w[sp] * a.part_ml[(base + sp) * 2 + 1];
+      num += s_w[sp] * a.part_o[(base + sp) * HD + e];
+    }
   }
-  L = min(L, a.kv_cap[req]);
-  const int ns = (L + a.S - 1) / a.S;
-  if (ns <= 1) return;
-  const int64_t base = ((int64_t)qi * a.n_heads + h) * a.n_split;
-  __shared__ float s_m[ATTN_MAX_SPLITS], s_w[ATTN_MAX_SPLITS];
-  __shared__ float s_den;
-  for (int sp = e; sp < ns; sp += HD) s_m[sp] = a.part_ml[(base + sp) * 2];
-  __syncthreads();
-  float M = -INFINITY;
-  for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, s_m[sp]);
-  for (int sp = e; sp < ns; sp += HD) s_w[sp] = expf(s_m[sp] - M);
-  __syncthreads();
-  if (e == 0) {
-    float den = 0.f;
-    for (int sp = 0; sp < ns; ++sp) den += s_w[sp] * a.part_ml[(base + sp) * 2 + 1];
-    s_den = den;
-  }
-  float num = 0.f;
-  for (int sp = 0; sp < ns; ++sp) num += s_w[sp] * a.part_o[(base + sp) * HD + e];
-  __syncthreads();
-  st_elem<DT>(a.out, ((int64_t)qi * a.n_heads + h) * HD + e, num / s_den);
+  st_elem<DT>(a.out, ((int64_t)qi * a.n_heads + h) * HD + e, num / den);
 }
 
 template <int DT, int HD>
 hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
-  const dim3 grid(a.n_split, a.n_kv, nq);
-  const bool wide = a.waves == ATTN_WAVES_WIDE;
+  const dim3 grid(a.n_split, a.n_kv, nq), block(64 * ATTN_WAVES);
   switch (group) {
-    case 1:
-      if (wide) HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES_WIDE>), grid, dim3(64 * ATTN_WAVES_WIDE), 0, st, a);
-      else HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a);
-      break;
-    case 2:
-      if (wide) HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES_WIDE>), grid, dim3(64 * ATTN_WAVES_WIDE), 0, st, a);
-      else HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a);
-      break;
-    case 4: HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
-    case 7: HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
-    case 8: HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, dim3(64 * ATTN_WAVES), 0, st, a); break;
+    case 1: HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 2: HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 4: HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 7: HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 8: HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -229,13 +246,20 @@ hipError_t attn_dt(int head_dim, int group, int nq, const AttnArgs &a, hipStream
   return hipErrorInvalidValue;
 }
 
+template <int DT, int HD>
+hipError_t combine_hd(int nq, const AttnArgs &a, hipStream_t st) {
+  const dim3 grid(a.n_heads, nq), block(HD);
+  if (a.n_split <= 8) HS_LAUNCH((k_combine<DT, HD, 8>), grid, block, 0, st, a);
+  else if (a.n_split <= 16) HS_LAUNCH((k_combine<DT, HD, 16>), grid, block, 0, st, a);
+  else HS_LAUNCH((k_combine<DT, HD, 0>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
 template <int DT>
 hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
-  const dim3 grid(a.n_heads, nq);
-  if (head_dim == 64) HS_LAUNCH((k_combine<DT, 64>), grid, dim3(64), 0, st, a);
-  else if (head_dim == 128) HS_LAUNCH((k_combine<DT, 128>), grid, dim3(128), 0, st, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (head_dim == 64) return combine_hd<DT, 64>(nq, a, st);
+  if (head_dim == 128) return combine_hd<DT, 128>(nq, a, st);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace

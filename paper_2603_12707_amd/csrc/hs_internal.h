@@ -52,10 +52,9 @@ enum { PRO_PLAIN = 0, PRO_NORM = 1 };
 // attention work groups: waves per work group, and the fewest positions a
 // split is cut down to when the GPU would otherwise be under-filled
 constexpr int ATTN_WAVES = 4;
-// wide work groups (query-head groups of at most two) when few (query, KV
-// head) pairs must each cover many positions
-constexpr int ATTN_WAVES_WIDE = 16;
-constexpr int ATTN_MIN_SPLIT = 128;
+// position groups per batch of K/V loads of one attention wave: fewer when
+// the query-head group's accumulators take more registers
+constexpr int attn_batch(int group) { return group <= 2 ? 8 : 4; }
 constexpr int ATTN_MAX_SPLITS = 256;
 enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
@@ -71,7 +70,6 @@ struct AttnArgs {
   int prefill_req; // < 0: decode (query = request, length = len + 1); else prefill row r, length r + 1
   int S;           // positions per split
   int n_split;     // splits per (query, kv head)
-  int waves;       // waves per work group: ATTN_WAVES or ATTN_WAVES_WIDE
   float *part_o;   // [nq][n_heads][n_split][head_dim]
   float *part_ml;  // [nq][n_heads][n_split][2]
   float scale;
