@@ -174,8 +174,16 @@ struct Step {
     return launch_attention(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
   }
 
-  hipError_t combine(int l) const {  // launches nothing with a single split
+  // the split combine runs in the O projection's prologue when it fits there
+  bool combine_fused() const {
     const hs_config &c = m->cfg;
+    return gemm_combine_fusable(c.dtype, ncols, c.n_heads * c.head_dim, n_split);
+  }
+
+  // launches nothing with a single split or a fused combine
+  hipError_t combine(int l) const {
+    const hs_config &c = m->cfg;
+    if (n_split <= 1 || combine_fused()) return hipSuccess;
     return launch_combine(c.dtype, c.head_dim, ncols, attn_args(l), st);
   }
 
@@ -192,7 +200,23 @@ struct Step {
     return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st);
   }
 
-  hipError_t oproj(int l) const { return residual(m->layers[l].wo, m->cfg.n_heads * m->cfg.head_dim, m->attn); }
+  hipError_t oproj(int l) const {
+    const hs_config &c = m->cfg;
+    if (!combine_fused()) return residual(m->layers[l].wo, c.n_heads * c.head_dim, m->attn);
+    GemmArgs o{};
+    o.w[0] = m->layers[l].wo;
+    o.rows[0] = c.d_model;
+    o.K = c.n_heads * c.head_dim;
+    o.ncols = ncols;
+    o.part_o = m->part_o;
+    o.part_ml = m->part_ml;
+    o.n_split = n_split;
+    o.head_dim = c.head_dim;
+    o.n_heads = c.n_heads;
+    o.resid = m->x;
+    o.ld_resid = c.d_model;
+    return launch_gemm(c.dtype, PRO_COMBINE, EPI_RESID, o, st);
+  }
 
   hipError_t gateup(int l) const {
     const hs_config &c = m->cfg;
@@ -233,7 +257,7 @@ struct Step {
     for (int l = 0; l < m->cfg.n_layers; ++l) {
       HIP_TRY(qkv(l));
       HIP_TRY(attn(l));
-      if (n_split > 1) HIP_TRY(combine(l));
+      HIP_TRY(combine(l));
       HIP_TRY(oproj(l));
       HIP_TRY(gateup(l));
       HIP_TRY(down(l));

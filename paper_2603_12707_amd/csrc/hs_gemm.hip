@@ -280,6 +280,68 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   f32x4 xv[PER];
   float gv[PER][4];
   u32x4 xc[PER];
+  // PRO_COMBINE: float4 item i of the staged activations is elements
+  // k = 4 (i mod K/4) .. +3 of column i / (K/4), i.e. of head k / head_dim
+  constexpr int PERC = 2, NSF = COMBINE_FUSE_SPLITS;
+  struct Part {
+    f32x4 o[NSF];
+    float m[NSF], l[NSF];
+  };
+  Part cp[PRO == PRO_COMBINE ? PERC : 1];
+  const int ns = a.n_split, hd = a.head_dim;
+  const rsrc_t por = make_rsrc(a.part_o + (int64_t)col0 * a.n_heads * ns * hd,
+                               PRO == PRO_COMBINE ? (uint32_t)nst * a.n_heads * ns * hd * 4u : 0u);
+  const rsrc_t pmr = make_rsrc(a.part_ml + (int64_t)col0 * a.n_heads * ns * 2,
+                               PRO == PRO_COMBINE ? (uint32_t)nst * a.n_heads * ns * 8u : 0u);
+  auto combine_load = [&](int item, Part &p) {
+    const int c = item / (K / 4), k = (item - c * (K / 4)) * 4;
+    const int h = k / hd, e = k - h * hd;
+    const bool ok = item < nst * (K / 4);
+    const int base = (c * a.n_heads + h) * ns;
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp) {
+      const bool in = ok && sp < ns;
+      p.o[sp] = __builtin_bit_cast(f32x4, bld16(por, in ? (uint32_t)((base + sp) * hd + e) * 4u : BUF_OOB));
+      const u32x2 ml = bld8(pmr, in ? (uint32_t)(base + sp) * 8u : BUF_OOB);
+      p.m[sp] = __uint_as_float(ml[0]);
+      p.l[sp] = __uint_as_float(ml[1]);
+    }
+  };
+  // o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s in split order, rounded
+  // to the storage dtype (the arithmetic of the separate combine kernel)
+  auto combine_store = [&](int item, const Part &p) {
+    if (item >= nst * (K / 4)) return;
+    float M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp)
+      if (sp < ns) M = fmaxf(M, p.m[sp]);
+    float den = 0.f, num[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sp = 0; sp < NSF; ++sp)
+      if (sp < ns) {
+        const float w = expf(p.m[sp] - M);
+        den += w * p.l[sp];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) num[e] += w * p.o[sp][e];
+      }
+    float h[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = num[e] / den;
+    const int64_t at = (int64_t)item * 4;  // staged rows are contiguous [nst][K]
+    if constexpr (DT == HS_F32) {
+      *(f32x4 *)((float *)s_x + at) = f32x4{h[0], h[1], h[2], h[3]};
+    } else {
+      uint32_t w0, w1;
+      if constexpr (DT == HS_F16) {
+        w0 = f32_to_f16(h[0]) | (f32_to_f16(h[1]) << 16);
+        w1 = f32_to_f16(h[2]) | (f32_to_f16(h[3]) << 16);
+      } else {
+        w0 = f32_to_bf16(h[0]) | (f32_to_bf16(h[1]) << 16);
+        w1 = f32_to_bf16(h[2]) | (f32_to_bf16(h[3]) << 16);
+      }
+      *(u32x2 *)((uint16_t *)s_x + at) = u32x2{w0, w1};
+    }
+  };
   if constexpr (XS == 1 && PRO == PRO_NORM) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
@@ -287,6 +349,10 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       xv[u] = __builtin_bit_cast(f32x4, bld16(xr, k < K ? (uint32_t)k * 4u : BUF_OOB));
       gain4<DT>(gr, k, k < K, gv[u]);
     }
+  } else if constexpr (PRO == PRO_COMBINE) {
+    // split partials of the first PERC float4 items of every thread
+#pragma unroll
+    for (int i = 0; i < PERC; ++i) combine_load(i * 64 * NW + (int)threadIdx.x, cp[i]);
   } else if constexpr (XS == 1) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
@@ -330,6 +396,15 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         xv[u] = __builtin_bit_cast(f32x4, bld16(xr, k < K ? (uint32_t)(c * K + k) * 4u : BUF_OOB));
       }
       stage(c);
+    }
+    __syncthreads();
+  } else if constexpr (PRO == PRO_COMBINE) {
+#pragma unroll
+    for (int i = 0; i < PERC; ++i) combine_store(i * 64 * NW + (int)threadIdx.x, cp[i]);
+    for (int item = PERC * 64 * NW + (int)threadIdx.x; item < nst * (K / 4); item += 64 * NW) {
+      Part p;
+      combine_load(item, p);
+      combine_store(item, p);
     }
     __syncthreads();
   } else if constexpr (XS == 1) {
@@ -505,8 +580,16 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   return gemm_launch<DT, R, 4, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
 }
 
+// the combine prologue: one column tile whose activations fit the LDS copy
+template <int DT>
+hipError_t gemm_combine(const GemmArgs &a, hipStream_t st) {
+  const size_t xs = (size_t)a.ncols * a.K * (DT == HS_F32 ? 4 : 2);
+  return gemm_launch<DT, 1, 1, 8, 1, PRO_COMBINE, 1, EPI_RESID>(a, (a.rows[0] + 15) / 16, xs, st);
+}
+
 template <int DT>
 hipError_t gemm_dt(int pro, int epi, const GemmArgs &a, hipStream_t st) {
+  if (pro == PRO_COMBINE && epi == EPI_RESID) return gemm_combine<DT>(a, st);
   if (pro == PRO_NORM && epi == EPI_QKV) return gemm_shape<DT, PRO_NORM, EPI_QKV>(a, st);
   if (pro == PRO_NORM && epi == EPI_SWIGLU) return gemm_shape<DT, PRO_NORM, EPI_SWIGLU>(a, st);
   if (pro == PRO_NORM && epi == EPI_STORE) return gemm_shape<DT, PRO_NORM, EPI_STORE>(a, st);
@@ -524,6 +607,12 @@ hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream
     case HS_BF16: return gemm_dt<HS_BF16>(pro, epi, a, st);
   }
   return hipErrorInvalidValue;
+}
+
+bool gemm_combine_fusable(int dtype, int ncols, int K, int n_split) {
+  const size_t b = dtype == HS_F32 ? 4 : 2;
+  return n_split > 1 && n_split <= COMBINE_FUSE_SPLITS && ncols >= 1 && ncols <= 16 && K % 4 == 0 &&
+         (size_t)ncols * K * b <= XS_MAX_BYTES;
 }
 
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols) {

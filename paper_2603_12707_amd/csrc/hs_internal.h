@@ -21,11 +21,15 @@ struct GemmArgs {
   int rows[3];
   int K;
   int ncols;
-  // prologue: plain activations (model dtype [ncols][K]) or the fp32 residual
-  // stream [ncols][K] normalised on the fly with gain[K] and eps
+  // prologue: plain activations (model dtype [ncols][K]), the fp32 residual
+  // stream [ncols][K] normalised with gain[K] and eps, or the attention output
+  // [ncols][n_heads * head_dim] combined from n_split split partials
   const void *x;
   const void *gain;
   float eps;
+  const float *part_o;   // [ncols][n_heads][n_split][head_dim]
+  const float *part_ml;  // [ncols][n_heads][n_split][2]
+  int n_split;
   // epilogue outputs
   void *out;    // logits fp32 / SwiGLU output / q after RoPE, row stride ld_out
   int ld_out;
@@ -47,10 +51,12 @@ struct GemmArgs {
   int *status;
 };
 
-enum { PRO_PLAIN = 0, PRO_NORM = 1 };
+enum { PRO_PLAIN = 0, PRO_NORM = 1, PRO_COMBINE = 2 };
+// the attention combine runs in the projection's prologue for at most this
+// many splits (and activations that fit the prologue's LDS copy)
+constexpr int COMBINE_FUSE_SPLITS = 8;
 
-// attention work groups: waves per work group, and the fewest positions a
-// split is cut down to when the GPU would otherwise be under-filled
+// waves per attention work group
 constexpr int ATTN_WAVES = 4;
 // position groups per batch of K/V loads of one attention wave: fewer when
 // the query-head group's accumulators take more registers
@@ -77,6 +83,8 @@ struct AttnArgs {
 };
 
 hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st);
+// whether launch_gemm takes PRO_COMBINE for these shapes
+bool gemm_combine_fusable(int dtype, int ncols, int K, int n_split);
 hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, hipStream_t st);
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
 hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);

@@ -114,11 +114,14 @@ def test_column_tiles(B):
     assert near <= 2
 
 
-def test_long_context_many_splits():
-    """A context long enough for many attention splits in decode and several
-    in prefill."""
-    cfg = small_cfg(n_layers=1, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=512, vocab=512)
-    near = _run_pair(cfg, [1100], [37], 3, extra_cap=400)
+@pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
+def test_long_context_many_splits(n_v, dtype):
+    """Contexts long enough for many attention splits in decode: at most 8
+    (combined in the O projection's prologue), up to 16 (partials requested
+    at once by the combine kernel) and more (the combine's general loop)."""
+    cfg = small_cfg(n_layers=1, d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=512, vocab=512,
+                    dtype=dtype)
+    near = _run_pair(cfg, [n_v], [37], 3, extra_cap=400)
     assert near == 0
 
 
