@@ -101,7 +101,7 @@ def setup(cfg: dict, n_steps_total: int):
     w = {}
     for name in synth.weight_names(cfg):  # generate and pack one matrix at a time
         t_row = synth.make_weight(cfg, name, device="cuda")
-        w[name] = hs.pack_matrix(t_row, cfg["dtype"]) if name.split(".")[-1] in hs.hs.PACKED else t_row
+        w[name] = hs.pack_weight(cfg, name, t_row)
         del t_row
     torch.cuda.synchronize()
     log(f"weights generated and packed in HBM: {sum(v.numel() * v.element_size() for v in w.values()) / 1e9:.2f} GB "

@@ -76,12 +76,11 @@ typedef struct hs_config {
 } hs_config;
 
 /* One decoder layer's weights, device pointers in the model dtype.  The
- * projection matrices are the nn.Linear matrices [out, in] in the packed
- * layout written by hs_pack_matrix:
- *   wq [n_h*d_h, d]   wk, wv [n_kv*d_h, d]   wo [d, n_h*d_h]
- *   w_gate, w_up [F, d]   w_down [d, F]
+ * projection matrices are the nn.Linear matrices [out, in] in packed layout:
+ *   wq [n_h*d_h, d]   wk, wv [n_kv*d_h, d]      written by hs_pack_matrix_heads
+ *   wo [d, n_h*d_h]   w_gate, w_up [F, d]   w_down [d, F]   by hs_pack_matrix
  * the norm gains attn_norm, mlp_norm [d] and the optional biases
- * bq, bk, bv [rows] are plain vectors. */
+ * bq, bk, bv [rows] are plain vectors in the original row order. */
 typedef struct hs_layer_weights {
   const void *attn_norm;
   const void *wq, *wk, *wv;
@@ -130,6 +129,15 @@ int hs_kv_bytes(const hs_config *cfg, int64_t n_v, int64_t s_text, uint64_t *kv_
  * asynchronously on the stream. */
 int hs_packed_bytes(int32_t dtype, int64_t rows, int64_t cols, uint64_t *bytes);
 int hs_pack_matrix(int32_t dtype, const void *src, int64_t rows, int64_t cols, void *dst, hs_stream_t stream);
+
+/* The packed layout of a q, k or v projection, whose rows form heads of
+ * head_dim rows: as hs_pack_matrix after reordering every head's rows so that
+ * row 2 j of the head is its row j and row 2 j + 1 its row j + head_dim / 2
+ * (the pair that rotate-half RoPE turns together, so that one 16-row tile
+ * holds whole pairs).  Same size as hs_packed_bytes;
+ * head_dim must be a positive multiple of 16 that divides rows. */
+int hs_pack_matrix_heads(int32_t dtype, const void *src, int64_t rows, int64_t cols, int32_t head_dim, void *dst,
+                         hs_stream_t stream);
 
 /* Validates cfg, records the caller-owned weight pointers (they must outlive
  * the model) and allocates the workspaces for decode batches of up to

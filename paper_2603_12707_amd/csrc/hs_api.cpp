@@ -320,7 +320,22 @@ int hs_pack_matrix(int32_t dtype, const void *src, int64_t rows, int64_t cols, v
   if (!src || !dst || ((uintptr_t)src | (uintptr_t)dst) % 16)
     return fail(HS_E_INVALID, "hs_pack_matrix: NULL or misaligned pointer");
   if (cols > INT32_MAX) return fail(HS_E_INVALID, "hs_pack_matrix: cols too large");
-  HIP_TRY(launch_pack(dtype, src, rows, cols, dst, (hipStream_t)stream));
+  HIP_TRY(launch_pack(dtype, src, rows, cols, dst, 0, (hipStream_t)stream));
+  return HS_OK;
+}
+
+int hs_pack_matrix_heads(int32_t dtype, const void *src, int64_t rows, int64_t cols, int32_t head_dim, void *dst,
+                         hs_stream_t stream) {
+  uint64_t bytes;
+  int rc = hs_packed_bytes(dtype, rows, cols, &bytes);
+  if (rc) return rc;
+  if (!src || !dst || ((uintptr_t)src | (uintptr_t)dst) % 16)
+    return fail(HS_E_INVALID, "hs_pack_matrix_heads: NULL or misaligned pointer");
+  if (cols > INT32_MAX) return fail(HS_E_INVALID, "hs_pack_matrix_heads: cols too large");
+  if (head_dim <= 0 || head_dim % 16 || rows % head_dim)
+    return fail(HS_E_INVALID, "hs_pack_matrix_heads: head_dim %d must be a positive multiple of 16 dividing rows",
+                head_dim);
+  HIP_TRY(launch_pack(dtype, src, rows, cols, dst, head_dim, (hipStream_t)stream));
   return HS_OK;
 }
 

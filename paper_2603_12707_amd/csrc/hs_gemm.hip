@@ -20,10 +20,13 @@ using namespace dev;
 // of k-blocks of 16 chunks (16 x CE elements, 256 bytes per row); k-block kb
 // of tile t is four 1 KB sub-blocks s, and lane l = 16 * lq + li of sub-block
 // s holds the 16-byte chunk kc = 16 * kb + 4 * s + lq of row 16 * t + li.
-// Rows past N and chunks past K are zero.
+// Rows past N and chunks past K are zero.  With pair_hd > 0 the rows form
+// heads of pair_hd rows, and packed row 2 j of a head holds its row j,
+// packed row 2 j + 1 its row j + pair_hd / 2 (the two rows RoPE rotates
+// together end up in the same lane of an MFMA output tile).
 template <int DT>
 __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_t N, int K, int nkb,
-                                              int64_t total) {
+                                              int64_t total, int pair_hd) {
   constexpr int CE = Ty<DT>::CE;
   using S = typename Ty<DT>::S;
   for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
@@ -31,7 +34,12 @@ __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_
     const int64_t rest = i >> 8;
     const int kb = (int)(rest % nkb);
     const int64_t tile = rest / nkb;
-    const int64_t row = tile * 16 + (lane & 15);
+    int64_t row = tile * 16 + (lane & 15);
+    if (pair_hd > 0) {
+      const int64_t head = row / pair_hd;
+      const int p = (int)(row - head * pair_hd);
+      row = head * pair_hd + ((p & 1) ? pair_hd / 2 + p / 2 : p / 2);
+    }
     const int kc = kb * 16 + s * 4 + (lane >> 4);
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (row < N && (int64_t)kc * CE < K) v = ld16((const S *)src + row * K + (int64_t)kc * CE);
@@ -42,26 +50,24 @@ __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_
 // ---------------------------------------------------------------------------
 // row tiles
 // ---------------------------------------------------------------------------
-// The q/k/v epilogue pairs rows i and i + d_h/2 of one head (the two halves
-// RoPE rotates together); SwiGLU pairs row j of the gate and of the up
+// q/k/v: single tiles of the q, k, v matrices in turn (their rows packed in
+// head-paired order); SwiGLU pairs row j of the gate and of the up
 // projection; the other epilogues take R consecutive tiles.
 template <int EPI, int R>
 __device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int *row0) {
   if constexpr (EPI == EPI_QKV) {
-    const int hd = a.head_dim, gph = hd / 32;
-    int m = 0, rem = g;
-    if (rem >= a.n_heads * gph) {
-      rem -= a.n_heads * gph;
+    const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
+    int m = 0, t = g;
+    if (t >= tq) {
+      t -= tq;
       m = 1;
-      if (rem >= a.n_kv * gph) {
-        rem -= a.n_kv * gph;
+      if (t >= tk) {
+        t -= tk;
         m = 2;
       }
     }
-    const int head = rem / gph, i0 = (rem % gph) * 16;
-    mat[0] = mat[1] = m;
-    row0[0] = head * hd + i0;
-    row0[1] = head * hd + i0 + hd / 2;
+    mat[0] = m;
+    row0[0] = 16 * t;
   } else if constexpr (EPI == EPI_SWIGLU) {
     mat[0] = 0;
     mat[1] = 1;
@@ -107,9 +113,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
         st_elem<DT>(o, j, g / (1.0f + expf(-g)) * u);
       }
     }
-  } else {  // EPI_QKV
+  } else {  // EPI_QKV: packed rows rr..rr+3 of the tile are pairs (j, j + d_h/2), (j + 1, j + 1 + d_h/2)
     const int m = mat[0], hd = a.head_dim, half = hd >> 1;
-    const int head = row0[0] / hd, i0 = row0[0] - head * hd;
+    const int head = row0[0] / hd, j0 = (row0[0] - head * hd + rr) >> 1;
     int req, pos;
     if (a.prefill_req < 0) {
       req = col;
@@ -119,9 +125,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
       pos = col;
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = i0 + rr + e;  // frequency pair, < d_h / 2
-      float v1 = v[0][e], v2 = v[1][e];
+    for (int e = 0; e < 2; ++e) {
+      const int i = j0 + e;  // frequency pair, < d_h / 2
+      float v1 = v[0][2 * e], v2 = v[0][2 * e + 1];
       if (a.bias[m]) {
         v1 += ld_elem<DT>(a.bias[m], head * hd + i);
         v2 += ld_elem<DT>(a.bias[m], head * hd + i + half);
@@ -554,19 +560,20 @@ hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_
   return hipGetLastError();
 }
 
-// Launch shape per epilogue: the paired-tile epilogues (q/k/v, SwiGLU) and
-// the LM head take 4 waves; the residual projections, whose matrices have
-// few row tiles, take 8 waves per tile so that enough loads are in flight.
+// Launch shape per epilogue: q/k/v, SwiGLU (paired gate/up tiles) and the
+// LM head take 4 waves per work group, so that every work group of the grid
+// is resident at once; the residual projections, whose matrices have few row
+// tiles, take 8 waves per tile so that enough loads are in flight.
 template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
-  constexpr int R = (EPI == EPI_QKV || EPI == EPI_SWIGLU) ? 2 : 1;
+  constexpr int R = EPI == EPI_SWIGLU ? 2 : 1;
   constexpr int NW = EPI == EPI_RESID ? 8 : 4;
-  // k-blocks per pipelined group at one column tile: two for single row
-  // tiles; one for paired tiles, whose registers would otherwise halve the
-  // resident work groups
-  constexpr int U1 = (R == 2 || NW == 8) ? 1 : 2;
-  // one work group per R row tiles (q/k/v: per pair of RoPE half-tiles)
-  const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 32
+  // k-blocks per pipelined group at one column tile: two for the LM head;
+  // one elsewhere, where the registers of two would cut the resident work
+  // groups below the grid
+  constexpr int U1 = EPI == EPI_STORE ? 2 : 1;
+  // one work group per R row tiles
+  const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 16
                                       : (a.rows[0] + 16 * (EPI == EPI_SWIGLU ? 1 : R) - 1) /
                                             (16 * (EPI == EPI_SWIGLU ? 1 : R));
   const int tiles = (a.ncols + 15) / 16;
@@ -621,16 +628,17 @@ int64_t packed_elems(int dtype, int64_t rows, int64_t cols) {
   return ((rows + 15) / 16) * nkb * 256 * ce;
 }
 
-hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, hipStream_t st) {
+hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, int pair_hd,
+                       hipStream_t st) {
   const int ce = dtype == HS_F32 ? 4 : 8;
   const int nkb = (int)((cols / ce + 15) / 16);
   const int64_t total = ((rows + 15) / 16) * nkb * 256;
   if (total <= 0) return hipSuccess;
   const int grid = (int)std::min<int64_t>((total + 255) / 256, 65536);
   switch (dtype) {
-    case HS_F32: HS_LAUNCH(k_pack<HS_F32>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
-    case HS_F16: HS_LAUNCH(k_pack<HS_F16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
-    case HS_BF16: HS_LAUNCH(k_pack<HS_BF16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total); break;
+    case HS_F32: HS_LAUNCH(k_pack<HS_F32>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total, pair_hd); break;
+    case HS_F16: HS_LAUNCH(k_pack<HS_F16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total, pair_hd); break;
+    case HS_BF16: HS_LAUNCH(k_pack<HS_BF16>, dim3(grid), dim3(256), 0, st, src, dst, rows, (int)cols, nkb, total, pair_hd); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

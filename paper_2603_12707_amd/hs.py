@@ -20,7 +20,7 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix")
+           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -87,6 +87,7 @@ def lib() -> ctypes.CDLL:
         "hs_replay_kernels": [P, P, I32, I32, P],
         "hs_packed_bytes": [I32, I64, I64, ctypes.POINTER(U64)],
         "hs_pack_matrix": [I32, P, I64, I64, P, P],
+        "hs_pack_matrix_heads": [I32, P, I64, I64, I32, P, P],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -145,15 +146,31 @@ def hs_packed_bytes(dtype: str, rows: int, cols: int) -> int:
     return out.value
 
 
-def pack_matrix(t, dtype: str):
+def pack_matrix(t, dtype: str, head_dim: int = 0):
     """Packed copy (uint8 device tensor) of a row-major [rows, cols] device
-    matrix, written by hs_pack_matrix on the current stream."""
+    matrix, written on the current stream by hs_pack_matrix, or with head_dim
+    by hs_pack_matrix_heads (the q/k/v projections)."""
     import torch
     assert t.is_cuda and t.dim() == 2 and t.is_contiguous()
     rows, cols = t.shape
     out = torch.empty(hs_packed_bytes(dtype, rows, cols), dtype=torch.uint8, device=t.device)
-    _call("hs_pack_matrix", _DT[dtype], _ptr(t), rows, cols, _ptr(out), _stream())
+    if head_dim:
+        _call("hs_pack_matrix_heads", _DT[dtype], _ptr(t), rows, cols, head_dim, _ptr(out), _stream())
+    else:
+        _call("hs_pack_matrix", _DT[dtype], _ptr(t), rows, cols, _ptr(out), _stream())
     return out
+
+
+HEAD_PAIRED = ("wq", "wk", "wv")
+
+
+def pack_weight(cfg: dict, name: str, t):
+    """The tensor the model takes for weight `name`: projection matrices
+    packed (q/k/v head-paired), everything else as it is."""
+    leaf = name.split(".")[-1]
+    if leaf not in PACKED:
+        return t
+    return pack_matrix(t, cfg["dtype"], cfg["head_dim"] if leaf in HEAD_PAIRED else 0)
 
 
 def pack_weights(cfg: dict, weights: dict, free_source: bool = False) -> dict:
@@ -162,12 +179,9 @@ def pack_weights(cfg: dict, weights: dict, free_source: bool = False) -> dict:
     matrices are removed from `weights` as they are packed."""
     out = {}
     for name in list(weights):
-        if _is_packed(name):
-            out[name] = pack_matrix(weights[name], cfg["dtype"])
-            if free_source:
-                del weights[name]
-        else:
-            out[name] = weights[name]
+        out[name] = pack_weight(cfg, name, weights[name])
+        if free_source and _is_packed(name):
+            del weights[name]
     return out
 
 

@@ -120,6 +120,24 @@ def test_pack_matrix_follows_documented_layout(dtype, rows, cols):
                        exp.view(torch.int16 if dtype != "f32" else torch.int32))
 
 
+@pytest.mark.parametrize("dtype,heads,head_dim,cols", [("bf16", 3, 128, 256), ("f16", 2, 64, 136), ("f32", 4, 16, 68)])
+def test_pack_matrix_heads_pairs_rope_rows(dtype, heads, head_dim, cols):
+    """hs_pack_matrix_heads equals hs_pack_matrix of the matrix whose head
+    rows are reordered j, j + d_h/2, j + 1, j + 1 + d_h/2, ..."""
+    import paper_2603_12707_amd as hs
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    rows = heads * head_dim
+    src = torch.randn(rows, cols, generator=torch.Generator().manual_seed(2)).to(tdt)
+    half = head_dim // 2
+    order = [h * head_dim + (p // 2 if p % 2 == 0 else half + p // 2) for h in range(heads) for p in range(head_dim)]
+    paired = hs.pack_matrix(src.cuda(), dtype, head_dim).cpu()
+    plain = hs.pack_matrix(src[order].contiguous().cuda(), dtype).cpu()
+    assert torch.equal(paired, plain)
+    with pytest.raises(hs.HsError) as e:
+        hs.pack_matrix(src[:rows - 8].contiguous().cuda(), dtype, head_dim)  # rows not a whole number of heads
+    assert e.value.code == hs.HS_E_INVALID
+
+
 def test_error_paths():
     import paper_2603_12707_amd as hs
     cfg = small_cfg(dtype="f16", n_layers=1)

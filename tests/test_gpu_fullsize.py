@@ -36,7 +36,7 @@ def _weights(cfg):
     for name in synth.weight_names(cfg):
         t = synth.make_weight(cfg, name, device="cuda")
         cpu[name] = t.cpu()
-        gpu[name] = hs.pack_matrix(t, cfg["dtype"]) if name.split(".")[-1] in hs.hs.PACKED else t
+        gpu[name] = hs.pack_weight(cfg, name, t)
         del t
     torch.cuda.synchronize()
     return cpu, gpu
