@@ -90,7 +90,7 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
 
 void free_model(hs_model *m) {
   if (!m) return;
-  void *ptrs[] = {m->x, m->q, m->attn, m->act, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
+  void *ptrs[] = {m->x, m->q, m->attn, m->act, m->hnorm, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
@@ -125,6 +125,7 @@ struct Step {
     g.ncols = ncols;
     g.x = m->x;
     g.gain = W.attn_norm;
+    g.h_work = m->hnorm;
     g.eps = c.rms_eps;
     g.out = m->q;
     g.ld_out = c.n_heads * c.head_dim;
@@ -229,6 +230,7 @@ struct Step {
     u.ncols = ncols;
     u.x = m->x;
     u.gain = W.mlp_norm;
+    u.h_work = m->hnorm;
     u.eps = c.rms_eps;
     u.out = m->act;
     u.ld_out = c.ffn_dim;
@@ -247,6 +249,7 @@ struct Step {
     g.ncols = ncols;
     g.x = x_rows;
     g.gain = m->w.final_norm;
+    g.h_work = m->hnorm;
     g.eps = c.rms_eps;
     g.out = logits;
     g.ld_out = c.vocab;
@@ -396,6 +399,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {&m->q, (size_t)rows * nh * hd * b},
       {&m->attn, (size_t)rows * nh * hd * b},
       {&m->act, (size_t)rows * c.ffn_dim * b},
+      {&m->hnorm, (size_t)rows * c.d_model * b},
       {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
       {(void **)&m->part_o, (size_t)std::max<int64_t>(entries, 1) * hd * 4},
       {(void **)&m->part_ml, (size_t)std::max<int64_t>(entries, 1) * 2 * 4},

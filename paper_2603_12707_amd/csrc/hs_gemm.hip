@@ -224,6 +224,25 @@ __device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
   }
 }
 
+// RMSNorm of fp32 residual rows into the storage dtype, one work group per
+// row: h = R(x * rs * gain), rs = 1 / sqrt(mean(x^2) + eps) with the sum of
+// squares in fp64 -- the normalisation the GEMM prologue applies when it
+// stages its columns itself, done once for GEMMs over more columns.
+template <int DT>
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gain, float eps, int K, void *h) {
+  const float *xr = x + (int64_t)blockIdx.x * K;
+  __shared__ double s_part[4];
+  double ss = 0.0;
+  for (int k = threadIdx.x * 4; k < K; k += 1024) ss += sumsq_f64(*(const f32x4 *)(xr + k));
+  const float rs = (float)(1.0 / sqrt(block_sum<4>(ss, s_part) / (double)K + (double)eps));
+  for (int k = threadIdx.x * 4; k < K; k += 1024) {
+    float g[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) g[e] = ld_elem<DT>(gain, k + e);
+    put_h<DT>((unsigned char *)h, (int64_t)blockIdx.x * K + k, *(const f32x4 *)(xr + k), rs, g);
+  }
+}
+
 // Y[c][n] = sum_k X[c][k] W[n][k] over R row tiles and NT column tiles of 16.
 //
 // The NW waves of a work group split the packed k-blocks round robin, so that
@@ -235,12 +254,13 @@ __device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
 // of rounds, and groups past the wave's last k-block read zeros.
 // X comes from a copy in LDS (XS = 1: the work group's columns are few; with
 // PRO_NORM the copy holds the normalised activations, with the first column's
-// x requested before the weights), from the activation rows in global memory
-// (PRO_PLAIN, XS = 0), or from the fp32 residual stream normalised on the fly
-// (PRO_NORM, XS = 0).  The waves' partial tiles are summed in a fixed order
-// through LDS and handed to the epilogue.
+// x requested before the weights; with PRO_COMBINE the attention output
+// rebuilt from its split partials), or from the activation rows in global
+// memory (PRO_PLAIN, XS = 0), requested with the weights.  The waves' partial
+// tiles are summed in a fixed order through LDS and handed to the epilogue.
 template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
 __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
+  static_assert(PRO == PRO_PLAIN || XS == 1, "only plain activations are read from global memory");
   using S = typename Ty<DT>::S;
   constexpr int CE = Ty<DT>::CE;
   constexpr int SB = (int)sizeof(S);
@@ -277,7 +297,6 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   // x of the work group's columns: fp32 residual rows (PRO_NORM) or activation rows
   const rsrc_t xr = PRO == PRO_NORM ? make_rsrc((const float *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * 4u)
                                     : make_rsrc((const S *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * SB);
-  __shared__ float s_rsq[16 * NT];
   __shared__ double s_part[NW];
   extern __shared__ __align__(16) unsigned char s_x[];  // XS: activations [nst][K]
 
@@ -367,9 +386,36 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     }
   }
 
+  // chunk kc of column 16 t + li of the work group; zero past the data
+  auto load_x = [&](int t, int kc) -> u32x4 {
+    const int c = 16 * t + li;
+    const bool ok = c < nst && kc < kchunks;
+    if constexpr (XS == 1) {
+      const u32x4 v = *(const u32x4 *)((const S *)s_x + (ok ? (int64_t)c * K + (int64_t)kc * CE : 0));
+      return ok ? v : u32x4{0u, 0u, 0u, 0u};
+    } else {
+      return bld16(xr, ok ? (uint32_t)(c * K + kc * CE) * SB : BUF_OOB);
+    }
+  };
+
+  // activations from global memory at two column tiles or fewer travel in a
+  // ring of their own, each group's chunks requested just before its weights
+  constexpr bool XRING = XS == 0 && NT <= 2;
+  u32x4 xq[XRING ? D : 1][U][NT][4];
+  auto load_xg = [&](u32x4 (&xv)[U][NT][4], int g) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) xv[u][t][s] = load_x(t, (wave + (g * U + u) * NW) * 16 + s * 4 + lq);
+  };
   u32x4 w[D][U][R][4];
 #pragma unroll
-  for (int d = 0; d < D; ++d) load_w(w[d], d);
+  for (int d = 0; d < D; ++d) {
+    if constexpr (XRING) load_xg(xq[d], d);
+    load_w(w[d], d);
+  }
 
   if constexpr (PRO == PRO_NORM && XS == 1) {
     // one pass over each staged column; the first column's x (already
@@ -422,44 +468,13 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     for (int i = PER * 64 * NW + (int)threadIdx.x; i < nst * kchunks; i += 64 * NW)
       *(u32x4 *)(s_x + (int64_t)i * 16) = bld16(xr, (uint32_t)i * 16u);
     __syncthreads();
-  } else if constexpr (PRO == PRO_NORM) {
-    for (int c = wave; c < 16 * NT; c += NW) {
-      double ss = 0.0;
-      if (c < nst)
-        for (int k = lane * 4; k < K; k += 256)
-          ss += sumsq_f64(__builtin_bit_cast(f32x4, bld16(xr, (uint32_t)(c * K + k) * 4u)));
-      ss = wave_sum_f64(ss);
-      if (lane == 0) s_rsq[c] = (float)(1.0 / sqrt(ss / (double)K + (double)a.eps));
-    }
-    __syncthreads();
   }
 
-  // chunk kc of column 16 t + li of the work group; zero past the data
-  auto load_x = [&](int t, int kc) -> u32x4 {
-    const int c = 16 * t + li;
-    const bool ok = c < nst && kc < kchunks;
-    if constexpr (XS == 1) {
-      const u32x4 v = *(const u32x4 *)((const S *)s_x + (ok ? (int64_t)c * K + (int64_t)kc * CE : 0));
-      return ok ? v : u32x4{0u, 0u, 0u, 0u};
-    } else if constexpr (PRO == PRO_PLAIN) {
-      return bld16(xr, ok ? (uint32_t)(c * K + kc * CE) * SB : BUF_OOB);
-    } else {
-      const uint32_t xo = ok ? (uint32_t)(c * K + kc * CE) * 4u : BUF_OOB;
-      const float rs = s_rsq[c];
-      float xe[CE], ge[CE], h[CE];
-      unpack<HS_F32>(bld16(xr, xo), xe);
-      if constexpr (CE == 8) unpack<HS_F32>(bld16(xr, xo + 16u), xe + 4);
-      unpack<DT>(bld16(gr, ok ? (uint32_t)kc * 16u : BUF_OOB), ge);
-#pragma unroll
-      for (int e = 0; e < CE; ++e) h[e] = xe[e] * rs * ge[e];
-      return pack<DT>(h);
-    }
-  };
 
   // The MFMAs of one k-group accumulate in fp32 from zero; with ACC64 each
   // group's tile is then added into fp64 accumulators, so that fp32 rounding
-  // only ever acts on sums of 4 * U * 32 products.
-  constexpr bool ACC64 = NT <= 2;
+  // only ever acts on sums of 4 * U * 32 products (where the registers allow).
+  constexpr bool ACC64 = R * NT <= 2;
   f32x4 acc[R][NT];
   double acc64[ACC64 ? R : 1][ACC64 ? NT : 1][4];
 #pragma unroll
@@ -478,13 +493,12 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int g = g0 + d;
-      u32x4 xb[U][NT][4];
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int t = 0; t < NT; ++t) xb[u][t][s] = load_x(t, (wave + (g * U + u) * NW) * 16 + s * 4 + lq);
+      u32x4 xl[XRING ? 1 : U][XRING ? 1 : NT][4];
+      if constexpr (!XRING) load_xg(xl, g);
+      auto &xb = [&]() -> auto & {
+        if constexpr (XRING) return xq[d];
+        else return xl;
+      }();
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -503,6 +517,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
             acc[r][t] = f32x4{0.f, 0.f, 0.f, 0.f};
           }
       }
+      if constexpr (XRING) load_xg(xq[d], g + D);
       load_w(w[d], g + D);
       // keep the next group's MFMAs (which wait for its loads) below this refill
       __builtin_amdgcn_sched_barrier(0);
@@ -578,13 +593,20 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
                                             (16 * (EPI == EPI_SWIGLU ? 1 : R));
   const int tiles = (a.ncols + 15) / 16;
   const int b = DT == HS_F32 ? 4 : 2;
-  if (tiles <= 1) {
-    const size_t xs = (size_t)a.ncols * a.K * b;
-    if (xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
-    return gemm_launch<DT, R, 1, NW, U1, PRO, 0, EPI>(a, n_groups, 0, st);
+  const size_t xs = (size_t)a.ncols * a.K * b;
+  if (tiles <= 1 && xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
+  GemmArgs p = a;
+  if constexpr (PRO == PRO_NORM) {
+    // more columns than the prologue stages: normalise them once, then read
+    // them as plain activations
+    HS_LAUNCH(k_rmsnorm<DT>, dim3(a.ncols), dim3(256), 0, st, (const float *)a.x, a.gain, a.eps, a.K, a.h_work);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    p.x = a.h_work;
   }
-  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
-  return gemm_launch<DT, R, 4, NW, 1, PRO, 0, EPI>(a, n_groups, 0, st);
+  if (tiles <= 1) return gemm_launch<DT, R, 1, NW, U1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
+  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
+  return gemm_launch<DT, R, 4, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
 }
 
 // the combine prologue: one column tile whose activations fit the LDS copy

@@ -27,6 +27,7 @@ struct GemmArgs {
   const void *x;
   const void *gain;
   float eps;
+  void *h_work;          // PRO_NORM over many columns: normalised rows, model dtype [ncols][K]
   const float *part_o;   // [ncols][n_heads][n_split][head_dim]
   const float *part_ml;  // [ncols][n_heads][n_split][2]
   int n_split;
@@ -115,6 +116,7 @@ struct hs_model {
   void *q = nullptr;        // [max_rows][n_h * d_h] q after RoPE
   void *attn = nullptr;     // [max_rows][n_h * d_h] attention output
   void *act = nullptr;      // [max_rows][F] SwiGLU output
+  void *hnorm = nullptr;    // [max_rows][d] normalised rows for GEMMs over many columns
   float *logits = nullptr;  // [max_batch][V] (used when the caller passes no logits buffer)
   float *part_o = nullptr;
   float *part_ml = nullptr;
