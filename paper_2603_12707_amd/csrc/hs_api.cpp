@@ -67,13 +67,15 @@ int check_config(const hs_config *c) {
 // A work group covers one (query, KV head) and S consecutive positions.  The
 // positions of a pair are cut into splits until there are about two work
 // groups per CU, but no further than one batch of K/V loads per wave (round =
-// ATTN_WAVES x positions per wave-wide load x attn_batch(group)); S is a
-// multiple of the positions one work-group iteration covers.  Many pairs keep
-// one split each.
+// ATTN_WAVES x positions per wave-wide load x loads per batch; a matrix-core
+// wave takes 16 positions per tile and ATTN_MMA_BATCH tiles per batch); S is
+// a multiple of the positions one work-group iteration covers.  Many pairs
+// keep one split each.
 void split_policy(int nq, int n_kv, int group, int head_dim, int dtype, int max_len, int *S, int *n_split) {
   const int ce = dtype == HS_F32 ? 4 : 8;
-  const int step = ATTN_WAVES * (64 * ce / head_dim);
-  const int round = step * attn_batch(group);
+  const bool mma = attn_uses_mma(dtype, group);  // 16-position tiles per wave
+  const int step = ATTN_WAVES * (mma ? 16 : 64 * ce / head_dim);
+  const int round = step * (mma ? ATTN_MMA_BATCH : attn_batch(group));
   const int64_t pairs = (int64_t)nq * n_kv;
   const int want = (int)std::max<int64_t>(1, (512 + pairs - 1) / pairs);
   const int by_round = std::max(1, (max_len + round - 1) / round);

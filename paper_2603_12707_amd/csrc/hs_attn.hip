@@ -177,6 +177,181 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   }
 }
 
+// Attention for query-head groups of 4..16 heads on the matrix cores.  One
+// work group = (split, KV head j, query), as above; each wave takes tiles of 16
+// consecutive positions.  Per tile, the scores of the tile's positions for all
+// heads of the group are S^T = K Q^T (16 positions x 16 head slots, MFMA
+// 16x16x32: exact products of the stored 16-bit values, fp32 sums).  A lane
+// then holds the scores of positions 4 q .. 4 q + 3 (q = lane / 16) for head
+// lane % 16 -- exactly the B-operand layout of the 16x16x16 MFMA that updates
+// O^T (d x heads) += V^T P^T, so the online-softmax probabilities feed the
+// matrix cores from registers.  That MFMA takes 16-bit operands, so P enters
+// as the sum of two storage-dtype parts, p = hi + lo (hi = R(p), lo =
+// R(p - hi)), one MFMA each: the products with the stored V values are exact
+// and p is kept to ~16 significant bits, against fp32 in the definition (a
+// single rounding of p to bf16 doubled the error of o and, over 28 layers,
+// the error of the residual stream).  l sums hi + lo, so o stays a weighted
+// mean of the V rows.  For the V^T operand a lane loads
+// chunk c = lane % 16 of the 4 positions it covers, and output row c of d-tile
+// dt is element d = 8 c + dt, which a lane gathers from its four chunks.
+// The waves merge through LDS as in k_attn.
+template <int DT, int HD, int G, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
+  static_assert(DT != HS_F32 && G <= 16 && (HD == 64 || HD == 128), "16-bit storage, at most 16 heads per group");
+  constexpr int SB = 2;
+  constexpr int CPR = HD / 8;         // 16-byte chunks per row
+  constexpr int KK = HD / 32;         // 32-wide k steps of the scores
+  constexpr int UB = ATTN_MMA_BATCH;  // tiles per batch of loads
+  constexpr int STEP = NW * 16;       // positions per work-group iteration
+  const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
+  int req, L;
+  if (a.prefill_req < 0) {
+    req = qi;
+    L = a.kv_len[qi] + 1;
+  } else {
+    req = a.prefill_req;
+    L = qi + 1;
+  }
+  const int cap = a.kv_cap[req];
+  L = min(L, cap);
+  const int t0 = split * a.S;
+  const int64_t qh = (int64_t)qi * a.n_heads + j * G;
+  if (t0 >= L) {
+    for (int idx = threadIdx.x; idx < G * HD; idx += 64 * NW) {
+      const int h = idx / HD, e = idx - h * HD;
+      a.part_o[((qh + h) * a.n_split + split) * HD + e] = 0.f;
+      if (e == 0) {
+        a.part_ml[((qh + h) * a.n_split + split) * 2] = -INFINITY;
+        a.part_ml[((qh + h) * a.n_split + split) * 2 + 1] = 0.f;
+      }
+    }
+    return;
+  }
+  const int n = min(a.S, L - t0);
+  const int n_it = (n + STEP - 1) / STEP;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int li = lane & 15, lg = lane >> 4;
+  const uint16_t *kbase =
+      (const uint16_t *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+  const uint16_t *vbase =
+      (const uint16_t *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap + t0) * HD;
+  const rsrc_t kr = make_rsrc(kbase, (uint32_t)n * HD * SB), vr = make_rsrc(vbase, (uint32_t)n * HD * SB);
+
+  // Q^T operand: head lane % 16 of the group (zero past G), k = 32 kk + 8 q ..
+  u32x4 qb[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk)
+    qb[kk] = li < G ? ld16((const uint16_t *)a.q + (int64_t)qi * a.ld_q + (j * G + li) * HD + (kk * 4 + lg) * 8)
+                    : u32x4{0u, 0u, 0u, 0u};
+
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int it0 = 0; it0 < n_it; it0 += UB) {
+    // every K and V chunk of the batch is requested before any is used;
+    // positions past the split read zeros
+    u32x4 kc[UB][KK], vc[UB][4];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int p0 = ((it0 + u) * NW + wave) * 16;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kc[u][kk] = bld16_stream(kr, (uint32_t)((p0 + li) * HD + (kk * 4 + lg) * 8) * SB);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        vc[u][i] = bld16_stream(vr, li < CPR ? (uint32_t)((p0 + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int p0 = ((it0 + u) * NW + wave) * 16;
+      f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) sc = mma<DT>(kc[u][kk], qb[kk], sc);
+      float sv[4];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sv[i] = p0 + 4 * lg + i < n ? sc[i] * a.scale : -INFINITY;
+        tmax = fmaxf(tmax, sv[i]);
+      }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      const float mn = fmaxf(m, tmax);
+      const float corr = m == -INFINITY ? 0.f : __expf(m - mn);
+      float pr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[i] = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mn);
+      // the PV operands: p = hi + lo in the storage dtype; l sums hi + lo
+      u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u};
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr[i]) : f32_to_bf16(pr[i]);
+        const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
+        const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr[i] - hf) : f32_to_bf16(pr[i] - hf);
+        ps += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));
+        ph[i >> 1] |= hb << (16 * (i & 1));
+        pl[i >> 1] |= lb << (16 * (i & 1));
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      l = l * corr + ps;
+      m = mn;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        o[dt] *= corr;
+        // V^T rows: element dt of chunk lane % 16 of the 4 positions
+        const int w = dt >> 1, sh = 16 * (dt & 1);
+        u32x2 av;
+        av[0] = ((vc[u][0][w] >> sh) & 0xFFFFu) | (((vc[u][1][w] >> sh) & 0xFFFFu) << 16);
+        av[1] = ((vc[u][2][w] >> sh) & 0xFFFFu) | (((vc[u][3][w] >> sh) & 0xFFFFu) << 16);
+        o[dt] = mma16<DT>(av, ph, o[dt]);
+        o[dt] = mma16<DT>(av, pl, o[dt]);
+      }
+    }
+  }
+
+  __shared__ float s_m[NW][16], s_l[NW][16];
+  __shared__ float s_o[NW][16][HD + 1];
+  if (lg == 0) {
+    s_m[wave][li] = m;
+    s_l[wave][li] = l;
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d = (4 * lg + i) * 8 + dt;
+      if (d < HD) s_o[wave][li][d] = o[dt][i];
+    }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * HD; idx += 64 * NW) {
+    const int h = idx / HD, e = idx - h * HD;
+    float M = s_m[0][h];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, s_m[w][h]);
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float wt = merge_weight(s_m[w][h], M);
+      num += wt * s_o[w][h][e];
+      den += wt * s_l[w][h];
+    }
+    if (a.n_split == 1) {
+      st_elem<DT>(a.out, (qh + h) * HD + e, num / den);
+    } else {
+      a.part_o[((qh + h) * a.n_split + split) * HD + e] = num;
+      if (e == 0) {
+        a.part_ml[((qh + h) * a.n_split + split) * 2] = M;
+        a.part_ml[((qh + h) * a.n_split + split) * 2 + 1] = den;
+      }
+    }
+  }
+}
+
 // o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s over the n_split splits
 // of one (query, head), in split order (empty splits have weight zero);
 // rounded to the storage dtype.  NSF > 0: at most NSF splits, whose partials
@@ -231,9 +406,18 @@ hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
   switch (group) {
     case 1: HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES>), grid, block, 0, st, a); break;
     case 2: HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES>), grid, block, 0, st, a); break;
-    case 4: HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a); break;
-    case 7: HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a); break;
-    case 8: HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 4:
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a);
+      break;
+    case 7:
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a);
+      break;
+    case 8:
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

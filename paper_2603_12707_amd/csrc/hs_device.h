@@ -126,6 +126,23 @@ __device__ __forceinline__ f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
   }
 }
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// The 16x16x16 MFMA: lane l supplies row (A) / column (B) l % 16 and the
+// 4 k values 4 (l / 16) .. + 3 of its 8-byte operand.
+template <int DT>
+__device__ __forceinline__ f32x4 mma16(u32x2 a, u32x2 b, f32x4 c) {
+  if constexpr (DT == HS_F16) {
+    return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b), c, 0, 0,
+                                                 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, a), __builtin_bit_cast(bf16x4, b), c,
+                                                     0, 0, 0);
+  }
+}
+
 __device__ __forceinline__ u32x4 ld16(const void *p) { return *(const u32x4 *)p; }
 __device__ __forceinline__ u32x4 ld16_stream(const void *p) {
   return __builtin_nontemporal_load((const u32x4 *)p);
@@ -155,7 +172,6 @@ __device__ __forceinline__ u32x4 bld16_stream(rsrc_t r, uint32_t off) {
 __device__ __forceinline__ uint32_t bld4(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint32_t, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ u32x2 bld8(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }

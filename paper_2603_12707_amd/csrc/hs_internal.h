@@ -62,6 +62,10 @@ constexpr int ATTN_WAVES = 4;
 // position groups per batch of K/V loads of one attention wave: fewer when
 // the query-head group's accumulators take more registers
 constexpr int attn_batch(int group) { return group <= 2 ? 8 : 4; }
+// query-head groups of 4 or more in 16-bit storage run on the matrix cores,
+// in tiles of 16 positions per wave, ATTN_MMA_BATCH tiles per batch of loads
+constexpr bool attn_uses_mma(int dtype, int group) { return dtype != HS_F32 && group >= 4; }
+constexpr int ATTN_MMA_BATCH = 2;
 constexpr int ATTN_MAX_SPLITS = 256;
 enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 
