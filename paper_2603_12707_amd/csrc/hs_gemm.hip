@@ -50,24 +50,27 @@ __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_
 // ---------------------------------------------------------------------------
 // row tiles
 // ---------------------------------------------------------------------------
-// q/k/v: single tiles of the q, k, v matrices in turn (their rows packed in
-// head-paired order); SwiGLU pairs row j of the gate and of the up
-// projection; the other epilogues take R consecutive tiles.
+// q/k/v: R consecutive tiles of the q, k, v matrices taken in turn (their
+// rows packed in head-paired order); SwiGLU pairs row j of the gate and of
+// the up projection; the other epilogues take R consecutive tiles.
 template <int EPI, int R>
 __device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int *row0) {
   if constexpr (EPI == EPI_QKV) {
     const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
-    int m = 0, t = g;
-    if (t >= tq) {
-      t -= tq;
-      m = 1;
-      if (t >= tk) {
-        t -= tk;
-        m = 2;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      int m = 0, t = g * R + r;
+      if (t >= tq) {
+        t -= tq;
+        m = 1;
+        if (t >= tk) {
+          t -= tk;
+          m = 2;
+        }
       }
+      mat[r] = m;
+      row0[r] = 16 * t;  // past the v rows for a partial last group
     }
-    mat[0] = m;
-    row0[0] = 16 * t;
   } else if constexpr (EPI == EPI_SWIGLU) {
     mat[0] = 0;
     mat[1] = 1;
@@ -113,9 +116,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
         st_elem<DT>(o, j, g / (1.0f + expf(-g)) * u);
       }
     }
-  } else {  // EPI_QKV: packed rows rr..rr+3 of the tile are pairs (j, j + d_h/2), (j + 1, j + 1 + d_h/2)
-    const int m = mat[0], hd = a.head_dim, half = hd >> 1;
-    const int head = row0[0] / hd, j0 = (row0[0] - head * hd + rr) >> 1;
+  } else {  // EPI_QKV: packed rows rr..rr+3 of a tile are pairs (j, j + d_h/2), (j + 1, j + 1 + d_h/2)
+#pragma unroll
+   for (int r = 0; r < R; ++r) {
+    const int m = mat[r], hd = a.head_dim, half = hd >> 1;
+    if (row0[r] >= a.rows[m]) continue;
+    const int head = row0[r] / hd, j0 = (row0[r] - head * hd + rr) >> 1;
     int req, pos;
     if (a.prefill_req < 0) {
       req = col;
@@ -127,7 +133,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int i = j0 + e;  // frequency pair, < d_h / 2
-      float v1 = v[0][2 * e], v2 = v[0][2 * e + 1];
+      float v1 = v[r][2 * e], v2 = v[r][2 * e + 1];
       if (a.bias[m]) {
         v1 += ld_elem<DT>(a.bias[m], head * hd + i);
         v2 += ld_elem<DT>(a.bias[m], head * hd + i + half);
@@ -158,6 +164,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
       }
     }
   }
+   }
 }
 
 // fp64 sum over the 64 lanes of a wave; every lane gets it.
@@ -575,26 +582,48 @@ hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_
   return hipGetLastError();
 }
 
-// Launch shape per epilogue: q/k/v, SwiGLU (paired gate/up tiles) and the
-// LM head take 4 waves per work group, so that every work group of the grid
-// is resident at once; the residual projections, whose matrices have few row
-// tiles, take 8 waves per tile so that enough loads are in flight.
+// Launch shape per epilogue.  Work groups of 4 waves for q/k/v, SwiGLU
+// (paired gate/up tiles) and the LM head, so that the whole grid is resident
+// at once; the residual projections, whose matrices have few row tiles, take
+// 8 waves per tile so that enough loads are in flight.  One k-block per group,
+// two for the LM head at one staged column tile.
+// Columns staged in LDS (few): one row tile per work group (R = 1; SwiGLU 2).
+// Activations read from global memory: every row tile of a work group reuses
+// the activation chunks it loads, so q/k/v and the LM head take as many row
+// tiles per work group as keep the grid large (LM head 4; q/k/v 4 while that
+// leaves >= 192 work groups, else 2 while >= 128), the residual projections 1.
+template <int DT, int EPI, int R, int NW, int NT>
+hipError_t gemm_global(const GemmArgs &p, int tiles16, hipStream_t st) {
+  const int n_groups = EPI == EPI_SWIGLU ? tiles16 : (tiles16 + R - 1) / R;
+  return gemm_launch<DT, R, NT, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
+}
+
+template <int DT, int EPI, int NT>
+hipError_t gemm_global_r(const GemmArgs &p, int tiles16, hipStream_t st) {
+  constexpr int NW = EPI == EPI_RESID ? 8 : 4;
+  if constexpr (EPI == EPI_SWIGLU) return gemm_global<DT, EPI, 2, NW, NT>(p, tiles16, st);
+  else if constexpr (EPI == EPI_RESID) return gemm_global<DT, EPI, 1, NW, NT>(p, tiles16, st);
+  else if constexpr (EPI == EPI_STORE) return gemm_global<DT, EPI, 4, NW, NT>(p, tiles16, st);
+  else {
+    if (tiles16 % 4 == 0 && tiles16 / 4 >= 192) return gemm_global<DT, EPI, 4, NW, NT>(p, tiles16, st);
+    if (tiles16 % 2 == 0 && tiles16 / 2 >= 128) return gemm_global<DT, EPI, 2, NW, NT>(p, tiles16, st);
+    return gemm_global<DT, EPI, 1, NW, NT>(p, tiles16, st);
+  }
+}
+
 template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
-  constexpr int R = EPI == EPI_SWIGLU ? 2 : 1;
-  constexpr int NW = EPI == EPI_RESID ? 8 : 4;
-  // k-blocks per pipelined group at one column tile: two for the LM head;
-  // one elsewhere, where the registers of two would cut the resident work
-  // groups below the grid
-  constexpr int U1 = EPI == EPI_STORE ? 2 : 1;
-  // one work group per R row tiles
-  const int n_groups = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 16
-                                      : (a.rows[0] + 16 * (EPI == EPI_SWIGLU ? 1 : R) - 1) /
-                                            (16 * (EPI == EPI_SWIGLU ? 1 : R));
+  // row tiles of 16 (SwiGLU: of one of its two matrices)
+  const int tiles16 = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 16 : (a.rows[0] + 15) / 16;
   const int tiles = (a.ncols + 15) / 16;
   const int b = DT == HS_F32 ? 4 : 2;
   const size_t xs = (size_t)a.ncols * a.K * b;
-  if (tiles <= 1 && xs <= XS_MAX_BYTES) return gemm_launch<DT, R, 1, NW, U1, PRO, 1, EPI>(a, n_groups, xs, st);
+  if (tiles <= 1 && xs <= XS_MAX_BYTES) {
+    constexpr int R = EPI == EPI_SWIGLU ? 2 : 1;
+    constexpr int NW = EPI == EPI_RESID ? 8 : 4;
+    constexpr int U = EPI == EPI_STORE ? 2 : 1;
+    return gemm_launch<DT, R, 1, NW, U, PRO, 1, EPI>(a, tiles16, xs, st);
+  }
   GemmArgs p = a;
   if constexpr (PRO == PRO_NORM) {
     // more columns than the prologue stages: normalise them once, then read
@@ -604,9 +633,9 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
     if (e != hipSuccess) return e;
     p.x = a.h_work;
   }
-  if (tiles <= 1) return gemm_launch<DT, R, 1, NW, U1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
-  if (tiles <= 2) return gemm_launch<DT, R, 2, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
-  return gemm_launch<DT, R, 4, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
+  if (tiles <= 1) return gemm_global_r<DT, EPI, 1>(p, tiles16, st);
+  if (tiles <= 2) return gemm_global_r<DT, EPI, 2>(p, tiles16, st);
+  return gemm_global_r<DT, EPI, 4>(p, tiles16, st);
 }
 
 // the combine prologue: one column tile whose activations fit the LDS copy
