@@ -180,7 +180,7 @@ struct Step {
   // the split combine runs in the O projection's prologue when it fits there
   bool combine_fused() const {
     const hs_config &c = m->cfg;
-    return gemm_combine_fusable(c.dtype, ncols, c.n_heads * c.head_dim, n_split);
+    return gemm_combine_fusable(c.dtype, ncols, c.n_heads * c.head_dim, c.n_heads, n_split);
   }
 
   // launches nothing with a single split or a fused combine

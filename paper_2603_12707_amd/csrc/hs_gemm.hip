@@ -313,63 +313,81 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   float gv[PER][4];
   u32x4 xc[PER];
   // PRO_COMBINE: float4 item i of the staged activations is elements
-  // k = 4 (i mod K/4) .. +3 of column i / (K/4), i.e. of head k / head_dim
+  // k = 4 (i mod K/4) .. +3 of column i / (K/4), i.e. of head k / head_dim.
+  // The split weights e^(m_s - M) and the denominator of each (column, head)
+  // pair are computed once, by thread `pair`, into LDS.
   constexpr int PERC = 2, NSF = COMBINE_FUSE_SPLITS;
-  struct Part {
-    f32x4 o[NSF];
-    float m[NSF], l[NSF];
-  };
-  Part cp[PRO == PRO_COMBINE ? PERC : 1];
+  f32x4 co[PRO == PRO_COMBINE ? PERC : 1][NSF];
+  float cm[NSF], cl[NSF];
   const int ns = a.n_split, hd = a.head_dim;
+  const int npair = nst * a.n_heads;
   const rsrc_t por = make_rsrc(a.part_o + (int64_t)col0 * a.n_heads * ns * hd,
-                               PRO == PRO_COMBINE ? (uint32_t)nst * a.n_heads * ns * hd * 4u : 0u);
+                               PRO == PRO_COMBINE ? (uint32_t)npair * ns * hd * 4u : 0u);
   const rsrc_t pmr = make_rsrc(a.part_ml + (int64_t)col0 * a.n_heads * ns * 2,
-                               PRO == PRO_COMBINE ? (uint32_t)nst * a.n_heads * ns * 8u : 0u);
-  auto combine_load = [&](int item, Part &p) {
+                               PRO == PRO_COMBINE ? (uint32_t)npair * ns * 8u : 0u);
+  __shared__ float s_cw[PRO == PRO_COMBINE ? 64 * NW : 1][NSF + 1];  // weights, then the denominator
+  auto combine_load = [&](int item, f32x4 (&o)[NSF]) {
     const int c = item / (K / 4), k = (item - c * (K / 4)) * 4;
     const int h = k / hd, e = k - h * hd;
     const bool ok = item < nst * (K / 4);
     const int base = (c * a.n_heads + h) * ns;
 #pragma unroll
+    for (int sp = 0; sp < NSF; ++sp)
+      o[sp] = __builtin_bit_cast(f32x4, bld16(por, ok && sp < ns ? (uint32_t)((base + sp) * hd + e) * 4u : BUF_OOB));
+  };
+  auto combine_ml = [&]() {
+    const int pair = threadIdx.x;
+#pragma unroll
     for (int sp = 0; sp < NSF; ++sp) {
-      const bool in = ok && sp < ns;
-      p.o[sp] = __builtin_bit_cast(f32x4, bld16(por, in ? (uint32_t)((base + sp) * hd + e) * 4u : BUF_OOB));
-      const u32x2 ml = bld8(pmr, in ? (uint32_t)(base + sp) * 8u : BUF_OOB);
-      p.m[sp] = __uint_as_float(ml[0]);
-      p.l[sp] = __uint_as_float(ml[1]);
+      const u32x2 ml = bld8(pmr, pair < npair && sp < ns ? (uint32_t)(pair * ns + sp) * 8u : BUF_OOB);
+      cm[sp] = __uint_as_float(ml[0]);
+      cl[sp] = __uint_as_float(ml[1]);
     }
   };
-  // o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s in split order, rounded
-  // to the storage dtype (the arithmetic of the separate combine kernel)
-  auto combine_store = [&](int item, const Part &p) {
-    if (item >= nst * (K / 4)) return;
+  // M = max_s m_s, w_s = e^(m_s - M), den = sum_s w_s l_s in split order (the
+  // arithmetic of the separate combine kernel)
+  auto combine_weights = [&]() {
+    const int pair = threadIdx.x;
+    if (pair >= npair) return;
     float M = -INFINITY;
 #pragma unroll
     for (int sp = 0; sp < NSF; ++sp)
-      if (sp < ns) M = fmaxf(M, p.m[sp]);
-    float den = 0.f, num[4] = {0.f, 0.f, 0.f, 0.f};
+      if (sp < ns) M = fmaxf(M, cm[sp]);
+    float den = 0.f;
 #pragma unroll
     for (int sp = 0; sp < NSF; ++sp)
       if (sp < ns) {
-        const float w = expf(p.m[sp] - M);
-        den += w * p.l[sp];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) num[e] += w * p.o[sp][e];
+        const float w = expf(cm[sp] - M);
+        s_cw[pair][sp] = w;
+        den += w * cl[sp];
       }
-    float h[4];
+    s_cw[pair][NSF] = den;
+  };
+  // o = sum_s w_s o_s / den, rounded to the storage dtype
+  auto combine_store = [&](int item, const f32x4 (&o)[NSF]) {
+    if (item >= nst * (K / 4)) return;
+    const int c = item / (K / 4), h = (item - c * (K / 4)) * 4 / hd;
+    const float *w = s_cw[c * a.n_heads + h];
+    float num[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) h[e] = num[e] / den;
+    for (int sp = 0; sp < NSF; ++sp)
+      if (sp < ns)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) num[e] += w[sp] * o[sp][e];
+    float h4[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h4[e] = num[e] / w[NSF];
     const int64_t at = (int64_t)item * 4;  // staged rows are contiguous [nst][K]
     if constexpr (DT == HS_F32) {
-      *(f32x4 *)((float *)s_x + at) = f32x4{h[0], h[1], h[2], h[3]};
+      *(f32x4 *)((float *)s_x + at) = f32x4{h4[0], h4[1], h4[2], h4[3]};
     } else {
       uint32_t w0, w1;
       if constexpr (DT == HS_F16) {
-        w0 = f32_to_f16(h[0]) | (f32_to_f16(h[1]) << 16);
-        w1 = f32_to_f16(h[2]) | (f32_to_f16(h[3]) << 16);
+        w0 = f32_to_f16(h4[0]) | (f32_to_f16(h4[1]) << 16);
+        w1 = f32_to_f16(h4[2]) | (f32_to_f16(h4[3]) << 16);
       } else {
-        w0 = f32_to_bf16(h[0]) | (f32_to_bf16(h[1]) << 16);
-        w1 = f32_to_bf16(h[2]) | (f32_to_bf16(h[3]) << 16);
+        w0 = f32_to_bf16(h4[0]) | (f32_to_bf16(h4[1]) << 16);
+        w1 = f32_to_bf16(h4[2]) | (f32_to_bf16(h4[3]) << 16);
       }
       *(u32x2 *)((uint16_t *)s_x + at) = u32x2{w0, w1};
     }
@@ -382,9 +400,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       gain4<DT>(gr, k, k < K, gv[u]);
     }
   } else if constexpr (PRO == PRO_COMBINE) {
+    // split maxima and sums of one (column, head) pair per thread, and the
     // split partials of the first PERC float4 items of every thread
+    combine_ml();
 #pragma unroll
-    for (int i = 0; i < PERC; ++i) combine_load(i * 64 * NW + (int)threadIdx.x, cp[i]);
+    for (int i = 0; i < PERC; ++i) combine_load(i * 64 * NW + (int)threadIdx.x, co[i]);
   } else if constexpr (XS == 1) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
@@ -458,12 +478,14 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     }
     __syncthreads();
   } else if constexpr (PRO == PRO_COMBINE) {
+    combine_weights();
+    __syncthreads();
 #pragma unroll
-    for (int i = 0; i < PERC; ++i) combine_store(i * 64 * NW + (int)threadIdx.x, cp[i]);
+    for (int i = 0; i < PERC; ++i) combine_store(i * 64 * NW + (int)threadIdx.x, co[i]);
     for (int item = PERC * 64 * NW + (int)threadIdx.x; item < nst * (K / 4); item += 64 * NW) {
-      Part p;
-      combine_load(item, p);
-      combine_store(item, p);
+      f32x4 o[NSF];
+      combine_load(item, o);
+      combine_store(item, o);
     }
     __syncthreads();
   } else if constexpr (XS == 1) {
@@ -667,10 +689,10 @@ hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream
   return hipErrorInvalidValue;
 }
 
-bool gemm_combine_fusable(int dtype, int ncols, int K, int n_split) {
+bool gemm_combine_fusable(int dtype, int ncols, int K, int n_heads, int n_split) {
   const size_t b = dtype == HS_F32 ? 4 : 2;
   return n_split > 1 && n_split <= COMBINE_FUSE_SPLITS && ncols >= 1 && ncols <= 16 && K % 4 == 0 &&
-         (size_t)ncols * K * b <= XS_MAX_BYTES;
+         (size_t)ncols * K * b <= XS_MAX_BYTES && ncols * n_heads <= 64 * 8;
 }
 
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols) {

@@ -89,7 +89,7 @@ struct AttnArgs {
 
 hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st);
 // whether launch_gemm takes PRO_COMBINE for these shapes
-bool gemm_combine_fusable(int dtype, int ncols, int K, int n_split);
+bool gemm_combine_fusable(int dtype, int ncols, int K, int n_heads, int n_split);
 hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, int pair_hd,
                        hipStream_t st);
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
