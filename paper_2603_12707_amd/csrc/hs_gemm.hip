@@ -437,6 +437,18 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) xv[u][t][s] = load_x(t, (wave + (g * U + u) * NW) * 16 + s * 4 + lq);
   };
+  // residual epilogue: the 4 rows of x this thread adds into, read now (no
+  // other work group writes them) so the epilogue does not wait for them
+  constexpr bool XPRE = EPI == EPI_RESID && R == 1 && NT * 64 <= 64 * NW;
+  f32x4 xres = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (XPRE) {
+    const int it = (int)threadIdx.x, c = 16 * (it >> 6) + (it & 15), rr = 4 * ((it & 63) >> 4);
+    const rsrc_t xrr = make_rsrc(a.resid, (uint32_t)a.ncols * a.ld_resid * 4u);
+    xres = __builtin_bit_cast(
+        f32x4, bld16(xrr, it < NT * 64 && col0 + c < a.ncols ? (uint32_t)((col0 + c) * a.ld_resid + row0[0] + rr) * 4u
+                                                              : BUF_OOB));
+  }
+
   u32x4 w[D][U][R][4];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
@@ -588,7 +600,17 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       }
     }
     const int col = col0 + 16 * t + (ln & 15);
-    if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
+    if constexpr (XPRE) {
+      if (col < a.ncols) {
+        float *x = a.resid + (int64_t)col * a.ld_resid;
+        const int row = row0[0] + 4 * (ln >> 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (row + e < a.rows[0]) x[row + e] = xres[e] + v[0][e];
+      }
+    } else {
+      if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
+    }
   }
 }
 
