@@ -116,55 +116,123 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
         st_elem<DT>(o, j, g / (1.0f + expf(-g)) * u);
       }
     }
-  } else {  // EPI_QKV: packed rows rr..rr+3 of a tile are pairs (j, j + d_h/2), (j + 1, j + 1 + d_h/2)
+  }
+}
+
+// q/k/v epilogue inputs of one thread (one output column, packed rows
+// rr..rr+3 of each of its R tiles: RoPE pairs (j, j + d_h/2) and
+// (j + 1, j + 1 + d_h/2)), read ahead of the main loop: the KV position,
+// capacity and base of the column's request and the RoPE position of each
+// pair first; the cos/sin entries and the biases once those positions are in.
+// Every read goes through a buffer range, so none sits behind a branch.
+template <int R>
+struct QkvIn {
+  int pos, cap;
+  int64_t base;
+  int p[R][2];
+  float cs[R][2], sn[R][2], b1[R][2], b2[R][2];
+};
+
+template <int DT, int R>
+__device__ __forceinline__ void qkv_fetch_ids(const GemmArgs &a, const int *mat, const int *row0, int col, int rr,
+                                              bool ok, QkvIn<R> &in) {
+  const bool dec = a.prefill_req < 0;
+  const int nreq = dec ? a.ncols : a.prefill_req + 1, req = dec ? col : a.prefill_req;
+  const rsrc_t lr = make_rsrc(a.kv_len, dec ? (uint32_t)a.ncols * 4u : 0u);
+  const rsrc_t cr = make_rsrc(a.kv_cap, (uint32_t)nreq * 4u);
+  const rsrc_t br = make_rsrc(a.kv_base, (uint32_t)nreq * 8u);
+  const rsrc_t pr = make_rsrc(a.rope_pos, dec ? (uint32_t)a.ncols * 4u : (a.rope_m3 ? 3u * a.ncols * 4u : 0u));
+  const uint32_t pl = bld4(lr, ok && dec ? (uint32_t)col * 4u : BUF_OOB);
+  in.cap = (int)bld4(cr, ok ? (uint32_t)req * 4u : BUF_OOB);
+  const u32x2 bb = bld8(br, ok ? (uint32_t)req * 8u : BUF_OOB);
+  in.base = (int64_t)(((uint64_t)bb[1] << 32) | bb[0]);
+  in.pos = dec ? (int)pl : col;
+  const int hd = a.head_dim;
 #pragma unroll
-   for (int r = 0; r < R; ++r) {
-    const int m = mat[r], hd = a.head_dim, half = hd >> 1;
+  for (int r = 0; r < R; ++r) {
+    const int j0 = (row0[r] % hd + rr) >> 1;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int i = j0 + e, sec = i < a.sec0 ? 0 : (i < a.sec1 ? 1 : 2);
+      const bool rot = ok && mat[r] < 2 && (dec || a.rope_m3);
+      const uint32_t pv = bld4(pr, rot ? (uint32_t)(dec ? col : sec * a.ncols + col) * 4u : BUF_OOB);
+      in.p[r][e] = (dec || a.rope_m3) ? (int)pv : col;
+    }
+  }
+}
+
+template <int DT, int R>
+__device__ __forceinline__ void qkv_fetch_tab(const GemmArgs &a, const int *mat, const int *row0, int rr, bool ok,
+                                              QkvIn<R> &in) {
+  const int hd = a.head_dim, half = hd >> 1;
+  const rsrc_t tr = make_rsrc(a.rope_tab, (uint32_t)a.rope_max * half * 8u);
+  constexpr int SB = DT == HS_F32 ? 4 : 2;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int m = mat[r], head = row0[r] / hd, j0 = (row0[r] - head * hd + rr) >> 1;
+    const bool live = ok && row0[r] < a.rows[m];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int p = min(max(in.p[r][e], 0), a.rope_max - 1);
+      const u32x2 t = bld8(tr, live && m < 2 ? (uint32_t)(p * half + j0 + e) * 8u : BUF_OOB);
+      in.cs[r][e] = __uint_as_float(t[0]);
+      in.sn[r][e] = __uint_as_float(t[1]);
+    }
+    const rsrc_t bq = make_rsrc(a.bias[m], a.bias[m] ? (uint32_t)a.rows[m] * SB : 0u);
+    const uint32_t o1 = (uint32_t)(head * hd + j0) * SB, o2 = (uint32_t)(head * hd + half + j0) * SB;
+    if constexpr (DT == HS_F32) {
+      const u32x2 v1 = bld8(bq, live ? o1 : BUF_OOB), v2 = bld8(bq, live ? o2 : BUF_OOB);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        in.b1[r][e] = __uint_as_float(v1[e]);
+        in.b2[r][e] = __uint_as_float(v2[e]);
+      }
+    } else {
+      const uint32_t v1 = bld4(bq, live ? o1 : BUF_OOB), v2 = bld4(bq, live ? o2 : BUF_OOB);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint32_t h1 = (v1 >> (16 * e)) & 0xFFFFu, h2 = (v2 >> (16 * e)) & 0xFFFFu;
+        in.b1[r][e] = DT == HS_F16 ? f16_to_f32(h1) : bf16_to_f32(h1);
+        in.b2[r][e] = DT == HS_F16 ? f16_to_f32(h2) : bf16_to_f32(h2);
+      }
+    }
+  }
+}
+
+// bias, RoPE on q and k, then R(q) to the q workspace and k, v rows appended
+// to the cache at the request's position
+template <int DT, int R>
+__device__ __forceinline__ void qkv_store(const GemmArgs &a, const int *mat, const int *row0, const f32x4 *v, int col,
+                                          int rr, const QkvIn<R> &in) {
+  constexpr int B = DT == HS_F32 ? 4 : 2;
+  const int hd = a.head_dim, half = hd >> 1;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int m = mat[r];
     if (row0[r] >= a.rows[m]) continue;
     const int head = row0[r] / hd, j0 = (row0[r] - head * hd + rr) >> 1;
-    int req, pos;
-    if (a.prefill_req < 0) {
-      req = col;
-      pos = a.kv_len[col];
-    } else {
-      req = a.prefill_req;
-      pos = col;
-    }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int i = j0 + e;  // frequency pair, < d_h / 2
-      float v1 = v[r][2 * e], v2 = v[r][2 * e + 1];
-      if (a.bias[m]) {
-        v1 += ld_elem<DT>(a.bias[m], head * hd + i);
-        v2 += ld_elem<DT>(a.bias[m], head * hd + i + half);
-      }
+      const float v1 = v[r][2 * e] + in.b1[r][e], v2 = v[r][2 * e + 1] + in.b2[r][e];
       float o1 = v1, o2 = v2;
       if (m < 2) {
-        int p;
-        if (a.prefill_req < 0) p = a.rope_pos[col];
-        else if (!a.rope_m3) p = col;
-        else p = a.rope_pos[(i < a.sec0 ? 0 : (i < a.sec1 ? 1 : 2)) * a.ncols + col];
-        p = min(max(p, 0), a.rope_max - 1);
-        const float cs = a.rope_tab[((int64_t)p * half + i) * 2], sn = a.rope_tab[((int64_t)p * half + i) * 2 + 1];
-        o1 = v1 * cs - v2 * sn;
-        o2 = v2 * cs + v1 * sn;
+        o1 = v1 * in.cs[r][e] - v2 * in.sn[r][e];
+        o2 = v2 * in.cs[r][e] + v1 * in.sn[r][e];
       }
       if (m == 0) {
         void *q = (char *)a.out + ((int64_t)col * a.ld_out + head * hd) * B;
         st_elem<DT>(q, i, o1);
         st_elem<DT>(q, i + half, o2);
-      } else {
-        const int cap = a.kv_cap[req];
-        if (pos < cap) {
-          const int64_t off =
-              a.kv_base[req] + ((int64_t)((a.layer * 2 + (m == 2 ? 1 : 0)) * a.n_kv + head) * cap + pos) * hd;
-          st_elem<DT>(a.kv, off + i, o1);
-          st_elem<DT>(a.kv, off + i + half, o2);
-        }
+      } else if (in.pos < in.cap) {
+        const int64_t off =
+            in.base + ((int64_t)((a.layer * 2 + (m == 2 ? 1 : 0)) * a.n_kv + head) * in.cap + in.pos) * hd;
+        st_elem<DT>(a.kv, off + i, o1);
+        st_elem<DT>(a.kv, off + i + half, o2);
       }
     }
   }
-   }
+
 }
 
 // fp64 sum over the 64 lanes of a wave; every lane gets it.
@@ -449,6 +517,14 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
                                                               : BUF_OOB));
   }
 
+  // q/k/v epilogue: ids now, table entries and biases after the prologue
+  static_assert(EPI != EPI_QKV || NT * 64 <= 64 * NW, "one epilogue item per thread");
+  QkvIn<R> qin;
+  const int ep_col = col0 + 16 * ((int)threadIdx.x >> 6) + ((int)threadIdx.x & 15);
+  const int ep_rr = 4 * (((int)threadIdx.x & 63) >> 4);
+  const bool ep_ok = (int)threadIdx.x < NT * 64 && ep_col < a.ncols;
+  if constexpr (EPI == EPI_QKV) qkv_fetch_ids<DT, R>(a, mat, row0, ep_col, ep_rr, ep_ok, qin);
+
   u32x4 w[D][U][R][4];
 #pragma unroll
   for (int d = 0; d < D; ++d) {
@@ -511,6 +587,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     __syncthreads();
   }
 
+
+  if constexpr (EPI == EPI_QKV) qkv_fetch_tab<DT, R>(a, mat, row0, ep_rr, ep_ok, qin);
 
   // The MFMAs of one k-group accumulate in fp32 from zero; with ACC64 each
   // group's tile is then added into fp64 accumulators, so that fp32 rounding
@@ -608,6 +686,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         for (int e = 0; e < 4; ++e)
           if (row + e < a.rows[0]) x[row + e] = xres[e] + v[0][e];
       }
+    } else if constexpr (EPI == EPI_QKV) {
+      if (col < a.ncols) qkv_store<DT, R>(a, mat, row0, v, col, 4 * (ln >> 4), qin);
     } else {
       if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
     }
