@@ -343,12 +343,23 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lq = lane >> 4;
-  const int col0 = blockIdx.y * 16 * NT;
+  // Over several column groups the grid is one-dimensional and ordered so
+  // that the column groups of a row group take consecutive slots of one XCD
+  // (work groups are dealt to the 8 XCDs round robin): the later groups then
+  // read the row group's weights from that XCD's L2 instead of HBM.
+  int grp = blockIdx.x, cgi = 0;
+  if (a.n_colg > 1) {
+    const int slot = (int)blockIdx.x >> 3;
+    cgi = slot % a.n_colg;
+    grp = (slot / a.n_colg) * 8 + ((int)blockIdx.x & 7);
+    if (grp >= a.n_groups) return;
+  }
+  const int col0 = cgi * 16 * NT;
   const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4;
   const int nst = min(a.ncols - col0, 16 * NT);
 
   int mat[R], row0[R];
-  tile_map<EPI, R>(a, blockIdx.x, mat, row0);
+  tile_map<EPI, R>(a, grp, mat, row0);
   // one range per row tile: its packed k-blocks (4 KB each); empty past the matrix
   rsrc_t wr[R];
 #pragma unroll
@@ -701,8 +712,11 @@ constexpr int XS_MAX_BYTES = 32 * 1024;  // LDS for normalised activations
 
 template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
 hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_t st) {
-  const dim3 grid(n_groups, (a.ncols + 16 * NT - 1) / (16 * NT));
-  HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI>), grid, dim3(64 * NW), shmem, st, a);
+  GemmArgs g = a;
+  g.n_groups = n_groups;
+  g.n_colg = (a.ncols + 16 * NT - 1) / (16 * NT);
+  const int blocks = g.n_colg > 1 ? (n_groups + 7) / 8 * 8 * g.n_colg : n_groups;
+  HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI>), dim3(blocks), dim3(64 * NW), shmem, st, g);
   return hipGetLastError();
 }
 

@@ -50,6 +50,8 @@ struct GemmArgs {
   const float *rope_tab;
   int rope_max;
   int *status;
+  // set by the launcher: work groups per column group, and column groups
+  int n_groups, n_colg;
 };
 
 enum { PRO_PLAIN = 0, PRO_NORM = 1, PRO_COMBINE = 2 };
