@@ -705,6 +705,128 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   }
 }
 
+// Many columns (B > 32, and prefill): Y = X W^T as a tiled GEMM.  A work group
+// owns WR x RTW row tiles and WC x CTW column tiles; wave (wr, wc) computes
+// its RTW x CTW output tiles over the whole K, so there is no reduction
+// between waves and every weight operand feeds CTW MFMAs and every activation
+// operand RTW.  Operands go straight from global memory into MFMA registers,
+// one 32-element k step (a 1 KB weight sub-block per row tile, 16 bytes per
+// lane per column tile) at a time, through a ring of two steps.  SwiGLU work
+// groups hold gate tiles in their first RTW / 2 rows of each wave and the
+// matching up tiles in the rest.  Activations are plain rows of the storage
+// dtype (normalised once by k_rmsnorm when the projection has a norm).
+// Accumulation is fp32 over the whole K.
+template <int DT, int RTW, int CTW, int WR, int WC, int EPI>
+__global__ __launch_bounds__(64 * WR * WC) void k_gemm_tile(GemmArgs a) {
+  using S = typename Ty<DT>::S;
+  constexpr int CE = Ty<DT>::CE;
+  constexpr int SB = (int)sizeof(S);
+  constexpr int D = 2;
+  constexpr int RTG = WR * RTW, CTG = WC * CTW;  // tiles per work group
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = wave / WC, wc = wave % WC;
+  const int li = lane & 15, lq = lane >> 4;
+  const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4, nsb = nkb * 4;
+  // XCD-aware order: the column groups of a row group are consecutive slots of one XCD
+  int rg = blockIdx.x, cg = 0;
+  if (a.n_colg > 1) {
+    const int slot = (int)blockIdx.x >> 3;
+    cg = slot % a.n_colg;
+    rg = (slot / a.n_colg) * 8 + ((int)blockIdx.x & 7);
+    if (rg >= a.n_groups) return;
+  }
+  int mat[RTW], row0[RTW];
+#pragma unroll
+  for (int r = 0; r < RTW; ++r) {
+    if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int H = RTW / 2;
+      mat[r] = r < H ? 0 : 1;
+      row0[r] = 16 * ((rg * WR + wr) * H + (r % H));
+    } else if constexpr (EPI == EPI_QKV) {
+      const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
+      int m = 0, t = (rg * WR + wr) * RTW + r;
+      if (t >= tq) {
+        t -= tq;
+        m = 1;
+        if (t >= tk) {
+          t -= tk;
+          m = 2;
+        }
+      }
+      mat[r] = m;
+      row0[r] = 16 * t;
+    } else {
+      mat[r] = 0;
+      row0[r] = 16 * ((rg * WR + wr) * RTW + r);
+    }
+  }
+  rsrc_t wres[RTW];
+#pragma unroll
+  for (int r = 0; r < RTW; ++r)
+    wres[r] = make_rsrc((const S *)a.w[mat[r]] + (int64_t)(row0[r] >> 4) * nkb * 256 * CE,
+                        row0[r] < a.rows[mat[r]] ? (uint32_t)nkb * 4096u : 0u);
+  const rsrc_t xres = make_rsrc(a.x, (uint32_t)a.ncols * K * SB);
+  const int colw = (cg * WC + wc) * CTW * 16;  // first column of the wave
+  auto load = [&](u32x4 (&wv)[RTW], u32x4 (&xv)[CTW], int st) {
+    const bool in = st < nsb;
+    const uint32_t wo = (uint32_t)(st >> 2) * 4096u + (uint32_t)(st & 3) * 1024u + (uint32_t)lane * 16u;
+#pragma unroll
+    for (int r = 0; r < RTW; ++r) wv[r] = bld16_stream(wres[r], in ? wo : BUF_OOB);
+    const int kc = (st >> 2) * 16 + (st & 3) * 4 + lq;
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) {
+      const int col = colw + 16 * c + li;
+      xv[c] = bld16(xres, in && col < a.ncols && kc < kchunks ? (uint32_t)(col * K + kc * CE) * SB : BUF_OOB);
+    }
+  };
+  f32x4 acc[RTW][CTW];
+#pragma unroll
+  for (int r = 0; r < RTW; ++r)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) acc[r][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 wv[D][RTW], xv[D][CTW];
+#pragma unroll
+  for (int d = 0; d < D; ++d) load(wv[d], xv[d], d);
+  for (int s0 = 0; s0 < nsb; s0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+#pragma unroll
+      for (int r = 0; r < RTW; ++r)
+#pragma unroll
+        for (int c = 0; c < CTW; ++c) acc[r][c] = mma<DT>(wv[d][r], xv[d][c], acc[r][c]);
+      load(wv[d], xv[d], s0 + d + D);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  const int rr = 4 * lq;
+#pragma unroll
+  for (int c = 0; c < CTW; ++c) {
+    const int col = colw + 16 * c + li;
+    if (col >= a.ncols) continue;
+    if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int H = RTW / 2;
+#pragma unroll
+      for (int r = 0; r < H; ++r) {
+        const int m2[2] = {0, 1}, r2[2] = {row0[r], row0[r + H]};
+        const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
+        gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
+      }
+    } else if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+      for (int r = 0; r < RTW; ++r) {
+        QkvIn<1> in;
+        qkv_fetch_ids<DT, 1>(a, &mat[r], &row0[r], col, rr, true, in);
+        qkv_fetch_tab<DT, 1>(a, &mat[r], &row0[r], rr, true, in);
+        qkv_store<DT, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < RTW; ++r) gemm_epilogue<DT, EPI, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // launch shapes
 // ---------------------------------------------------------------------------
@@ -749,6 +871,26 @@ hipError_t gemm_global_r(const GemmArgs &p, int tiles16, hipStream_t st) {
   }
 }
 
+// Tiled GEMM launch: work-group tiles of WR*RTW row tiles by WC*CTW column
+// tiles (SwiGLU: RTW/2 gate and RTW/2 up tiles per wave).
+template <int DT, int RTW, int CTW, int WR, int WC, int EPI>
+hipError_t gemm_tile_launch(const GemmArgs &a, int tiles16, hipStream_t st) {
+  GemmArgs g = a;
+  const int rows_per_group = EPI == EPI_SWIGLU ? WR * RTW / 2 : WR * RTW;
+  g.n_groups = (tiles16 + rows_per_group - 1) / rows_per_group;
+  g.n_colg = (a.ncols + 16 * WC * CTW - 1) / (16 * WC * CTW);
+  const int blocks = g.n_colg > 1 ? (g.n_groups + 7) / 8 * 8 * g.n_colg : g.n_groups;
+  HS_LAUNCH((k_gemm_tile<DT, RTW, CTW, WR, WC, EPI>), dim3(blocks), dim3(64 * WR * WC), 0, st, g);
+  return hipGetLastError();
+}
+
+template <int DT, int EPI>
+hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
+  if constexpr (EPI == EPI_SWIGLU) return gemm_tile_launch<DT, 4, 4, 2, 2, EPI>(p, tiles16, st);
+  else if constexpr (EPI == EPI_RESID) return gemm_tile_launch<DT, 2, 2, 1, 4, EPI>(p, tiles16, st);
+  else return gemm_tile_launch<DT, 2, 4, 2, 2, EPI>(p, tiles16, st);
+}
+
 template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   // row tiles of 16 (SwiGLU: of one of its two matrices)
@@ -773,7 +915,7 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   }
   if (tiles <= 1) return gemm_global_r<DT, EPI, 1>(p, tiles16, st);
   if (tiles <= 2) return gemm_global_r<DT, EPI, 2>(p, tiles16, st);
-  return gemm_global_r<DT, EPI, 4>(p, tiles16, st);
+  return gemm_tiled<DT, EPI>(p, tiles16, st);
 }
 
 // the combine prologue: one column tile whose activations fit the LDS copy
