@@ -173,6 +173,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=DEFAULT_WARMUP)
     ap.add_argument("--workload", default="llava7b_b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the decode step replayed from a HIP graph (stream capture)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -189,7 +191,8 @@ def main() -> int:
     cfg = configs.get(args.workload)
     B = cfg["batch"]
     torch.cuda.set_device(0)
-    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps))
+    graph_steps = 2 * (max(1, args.steps // 4) + 1) if args.graph else 0
+    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps)
 
     tin = first.clone()
     tout = torch.empty_like(tin)
@@ -212,6 +215,26 @@ def main() -> int:
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     lens_after = kv.lengths()
+
+    graph_ms = None
+    if args.graph:
+        # two steps per graph (the token buffers ping-pong), replayed back to back
+        ga, gb = tin.clone(), torch.empty_like(tin)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            kv.decode(ga, gb if has_head else None)
+            kv.decode(gb if has_head else ga, ga if has_head else None)
+        kv.sync()
+        reps_g = max(1, args.steps // 4)
+        graph.replay()  # warm
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps_g):
+            graph.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) / (2 * reps_g) * 1e3
+        kv.sync()
+        lens_after = [n - 2 * (reps_g + 1) for n in kv.lengths()]
 
     # dominant kernel (gate/up projection): replayed back to back over every
     # layer's weights, HIP events around the batch on the stream the library
@@ -285,6 +308,9 @@ def main() -> int:
         "roofline": roofline,
         "kernel_us": kernels,
     }
+    if graph_ms is not None:
+        out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
+                        "note": "the same step replayed from a HIP graph (stream capture)"}
     if not args.no_cpu_baseline:
         del w
         out["cpu_baseline"] = cpu_baseline(cfg, lens_start[0])

@@ -187,7 +187,14 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
  * hidden_out (device fp32 [batch, d], the residual stream after the last
  * layer) are optional outputs.  Errors: HS_E_STATE if a request is not
  * prefilled, HS_E_CAPACITY if len_b == capacity_b for some b.  Token ids
- * outside [0, vocab) are replaced by 0 and flagged (hs_model_status). */
+ * outside [0, vocab) are replaced by 0 and flagged (hs_model_status).
+ * The call only enqueues kernels (and, with hidden_out, one device copy) on
+ * the stream, with a launch configuration fixed by the handle, so it can be
+ * recorded into a HIP graph (stream capture) and the graph replayed, one step
+ * per replay, for as long as every request has capacity left: the checks
+ * above run on host mirrors when the call is made, not at replay (the paper
+ * captures its decode iteration with CUDA Graphs, §5.4).  After replays,
+ * hs_kv_sync brings the host mirrors up to date. */
 int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
                    float *hidden_out, hs_stream_t stream);
 
@@ -224,6 +231,11 @@ int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_st
 
 /* Host copy of every request's current length (int32 [batch]). */
 int hs_kv_lengths(const hs_kv *kv, int32_t *host_len);
+
+/* Waits for the device and copies the lengths and RoPE positions into the
+ * handle's host mirrors (needed after replaying a captured decode step, whose
+ * advances happen on the device only). */
+int hs_kv_sync(hs_kv *kv);
 
 /* Copies n rows of head_dim elements (model dtype) into / out of the cache at
  * (req, layer, kv_sel 0 = K / 1 = V, head, positions pos0..pos0+n-1);

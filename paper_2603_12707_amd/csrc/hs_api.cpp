@@ -612,6 +612,14 @@ int hs_kv_lengths(const hs_kv *kv, int32_t *host_len) {
   return HS_OK;
 }
 
+int hs_kv_sync(hs_kv *kv) {
+  if (!kv) return fail(HS_E_INVALID, "hs_kv_sync: NULL handle");
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpy(kv->len.data(), kv->d_len, kv->batch * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(hipMemcpy(kv->rope.data(), kv->d_rope, kv->batch * 4, hipMemcpyDeviceToHost));
+  return HS_OK;
+}
+
 static int kv_slab(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0,
                    int32_t n, const void *p, int64_t *off_bytes, size_t *bytes) {
   if (!kv || !p) return fail(HS_E_INVALID, "kv copy: NULL argument");

@@ -20,7 +20,7 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads")
+           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -81,6 +81,7 @@ def lib() -> ctypes.CDLL:
         "hs_decode_step": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
+        "hs_kv_sync": [P],
         "hs_kv_write": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_read": [P, I32, I32, I32, I32, I32, I32, P, I32],
         "hs_kv_set_length": [P, I32, I32, I32],
@@ -268,6 +269,10 @@ class KVCache:
     def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None) -> None:
         _call("hs_decode_step", self.model.handle, self.handle, _ptr(tokens_in), _ptr(tokens_out), _ptr(logits),
               _ptr(hidden_out), _stream())
+
+    def sync(self) -> None:
+        """Host mirrors of the lengths from the device (after graph replays)."""
+        _call("hs_kv_sync", self.handle)
 
     def lengths(self) -> list:
         out = (ctypes.c_int32 * self.batch)()

@@ -170,3 +170,60 @@ def test_prefill_then_decode_matches_longer_prefill(rope_kind):
     b.prefill(0, emb.cuda(), ids.cuda(), None if pos is None else pos.cuda(), last_logits=lb)
     torch.cuda.synchronize()
     assert rel_err(la[0].cpu().numpy(), lb.cpu().numpy()) <= 2e-3
+
+
+def test_decode_step_replays_from_a_hip_graph():
+    """hs_decode_step recorded by stream capture (two steps, ping-ponging the
+    token buffers) and replayed gives, replay after replay, the tokens and
+    logits of eager calls on an identical cache; eager work and
+    synchronisation run between the replays."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
+    n_v, s_text = [30, 9, 50], [5, 40, 2]
+    caps = [n + s + 12 for n, s in zip(n_v, s_text)]
+    pair = Pair(cfg, max_batch=3, max_ctx=max(caps))
+    handles = []
+    for _ in range(2):
+        kv = hs.KVCache(pair.gpu, n_v, caps)
+        first = torch.empty(3, dtype=torch.int32, device="cuda")
+        for r in range(3):
+            emb, ids, _ = pair.request_inputs(r, n_v[r], s_text[r])
+            kv.prefill(r, emb.cuda(), ids.cuda(), first_token=first[r:r + 1])
+        handles.append((kv, first))
+    torch.cuda.synchronize()
+    V = cfg["vocab"]
+    # eager reference: 8 steps
+    kv_e, t_e = handles[0]
+    a, b = t_e.clone(), torch.empty_like(t_e)
+    ref_tok, ref_log = [], []
+    lg = torch.empty(3, V, device="cuda")
+    for _ in range(8):
+        kv_e.decode(a, b, lg)
+        ref_tok.append(b.cpu().clone())
+        ref_log.append(lg.cpu().clone())
+        a, b = b, a
+    # captured: two steps per graph, replayed four times
+    kv_g, t_g = handles[1]
+    ga, gb = t_g.clone(), torch.empty_like(t_g)
+    lg1, lg2 = torch.empty(3, V, device="cuda"), torch.empty(3, V, device="cuda")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        kv_g.decode(ga, gb, lg1)
+        kv_g.decode(gb, ga, lg2)
+    kv_g.sync()  # capture ran no kernel: the device lengths are those after prefill
+    assert kv_g.lengths() == [n + s for n, s in zip(n_v, s_text)]
+    for k in range(4):
+        graph.replay()
+        torch.cuda.synchronize()
+        scratch = torch.randn(1 << 16, device="cuda").sum()  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.isfinite(scratch)
+        assert torch.equal(gb.cpu(), ref_tok[2 * k]), k
+        assert torch.equal(ga.cpu(), ref_tok[2 * k + 1]), k
+        assert torch.equal(lg1.cpu(), ref_log[2 * k]), k
+        assert torch.equal(lg2.cpu(), ref_log[2 * k + 1]), k
+    kv_g.sync()
+    assert kv_g.lengths() == kv_e.lengths() == [n + s + 8 for n, s in zip(n_v, s_text)]
+    for kv, _ in handles:
+        kv.close()
+    pair.gpu.close()
