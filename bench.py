@@ -132,7 +132,9 @@ def setup(cfg: dict, n_steps_total: int):
             pos = synth.mrope_positions(n_v[r], s_text[r]).cuda() if cfg["rope_kind"] == 1 else None
             kv.prefill(r, emb if n_v[r] else None, ids if s_text[r] else None, pos, first_token=first[r:r + 1])
     torch.cuda.synchronize()
-    log(f"context ready for {B} request(s) in {time.time() - t:.1f} s (lengths {min(lens)}..{max(lens)})")
+    ready_s = time.time() - t
+    log(f"context ready for {B} request(s) in {ready_s * 1e3:.1f} ms (lengths {min(lens)}..{max(lens)})")
+    setup.prefill_ms = None if "kv_len" in cfg else ready_s * 1e3 / B
     return w, model, kv, first, lens
 
 
@@ -308,6 +310,8 @@ def main() -> int:
         "roofline": roofline,
         "kernel_us": kernels,
     }
+    if getattr(setup, "prefill_ms", None) is not None:
+        out["prefill_ms_per_request"] = round(setup.prefill_ms, 2)
     if graph_ms is not None:
         out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
                         "note": "the same step replayed from a HIP graph (stream capture)"}

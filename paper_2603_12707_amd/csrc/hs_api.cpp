@@ -174,6 +174,8 @@ struct Step {
 
   hipError_t attn(int l) const {
     const hs_config &c = m->cfg;
+    if (prefill_req >= 0 && attn_prefill_on_mma(c.dtype))
+      return launch_attention_prefill(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
     return launch_attention(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
   }
 
@@ -526,7 +528,8 @@ int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, 
   if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "hs_prefill_embeddings: request %d is not empty", req);
   if (s_ctx > kv->cap[req])
     return fail(HS_E_CAPACITY, "hs_prefill_embeddings: context %d exceeds capacity %d", s_ctx, kv->cap[req]);
-  // prefill: every row is its own query, so one split per (row, KV head)
+  // prefill: every row is its own query over the rows before it; no splits
+  // (S = s_ctx, the row count, which the causal kernel reads)
   const int S = s_ctx, ns = 1;
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));

@@ -352,6 +352,122 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   }
 }
 
+// Prefill attention on the matrix cores (causal: row r of the request attends
+// to rows 0..r).  The 16 MFMA columns hold QPT = 16 / G consecutive query rows
+// x the G query heads of KV head j; a wave takes one such query tile and walks
+// the key tiles of 16 positions up to its last query row, masking the keys
+// past each row.  Operand layouts and the p = hi + lo split are those of
+// k_attn_mma; each wave finishes its own queries (no splits, no merge), so
+// the K/V rows a tile loads serve QPT x G (query, head) pairs at once instead
+// of one.
+template <int DT, int HD, int G, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
+  static_assert(DT != HS_F32 && G <= 16 && (HD == 64 || HD == 128), "16-bit storage, at most 16 heads per group");
+  constexpr int SB = 2;
+  constexpr int CPR = HD / 8;
+  constexpr int KK = HD / 32;
+  constexpr int UB = ATTN_MMA_BATCH;
+  constexpr int QPT = 16 / G;  // query rows per tile
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int li = lane & 15, lg = lane >> 4;
+  const int j = blockIdx.y;
+  const int nrows = a.S;  // rows of the prefill
+  const int q0 = ((int)blockIdx.x * NW + wave) * QPT;
+  if (q0 >= nrows) return;  // whole wave; no barrier below
+  const int req = a.prefill_req, cap = a.kv_cap[req];
+  const int sq = q0 + li / G, sh = li % G;  // the lane column's query row and head
+  const bool slot = li < QPT * G && sq < nrows;
+  const int qlast = min(q0 + QPT - 1, nrows - 1);
+  const int n_kt = qlast / 16 + 1;  // key tiles
+  const uint16_t *kbase = (const uint16_t *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2) * a.n_kv + j) * cap * HD;
+  const uint16_t *vbase =
+      (const uint16_t *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap * HD;
+  const uint32_t nbytes = (uint32_t)(qlast + 1) * HD * SB;
+  const rsrc_t kr = make_rsrc(kbase, nbytes), vr = make_rsrc(vbase, nbytes);
+
+  u32x4 qb[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk)
+    qb[kk] = slot ? ld16((const uint16_t *)a.q + (int64_t)sq * a.ld_q + (j * G + sh) * HD + (kk * 4 + lg) * 8)
+                  : u32x4{0u, 0u, 0u, 0u};
+
+  float m = -INFINITY, l = 0.f;
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kt0 = 0; kt0 < n_kt; kt0 += UB) {
+    u32x4 kc[UB][KK], vc[UB][4];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int p0 = (kt0 + u) * 16;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kc[u][kk] = bld16(kr, (uint32_t)((p0 + li) * HD + (kk * 4 + lg) * 8) * SB);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        vc[u][i] = bld16(vr, li < CPR ? (uint32_t)((p0 + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int p0 = (kt0 + u) * 16;
+      f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) sc = mma<DT>(kc[u][kk], qb[kk], sc);
+      float sv[4];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sv[i] = slot && p0 + 4 * lg + i <= sq ? sc[i] * a.scale : -INFINITY;
+        tmax = fmaxf(tmax, sv[i]);
+      }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      const float mn = fmaxf(m, tmax);
+      const float corr = m == -INFINITY ? 0.f : __expf(m - mn);
+      float pr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[i] = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mn);
+      u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u};
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr[i]) : f32_to_bf16(pr[i]);
+        const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
+        const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr[i] - hf) : f32_to_bf16(pr[i] - hf);
+        ps += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));
+        ph[i >> 1] |= hb << (16 * (i & 1));
+        pl[i >> 1] |= lb << (16 * (i & 1));
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      l = l * corr + ps;
+      m = mn;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        o[dt] *= corr;
+        const int w = dt >> 1, sh2 = 16 * (dt & 1);
+        u32x2 av;
+        av[0] = ((vc[u][0][w] >> sh2) & 0xFFFFu) | (((vc[u][1][w] >> sh2) & 0xFFFFu) << 16);
+        av[1] = ((vc[u][2][w] >> sh2) & 0xFFFFu) | (((vc[u][3][w] >> sh2) & 0xFFFFu) << 16);
+        o[dt] = mma16<DT>(av, ph, o[dt]);
+        o[dt] = mma16<DT>(av, pl, o[dt]);
+      }
+    }
+  }
+  if (!slot) return;
+  // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
+  const int64_t orow = ((int64_t)sq * a.n_heads + j * G + sh) * HD;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d = (4 * lg + i) * 8 + dt;
+      if (d < HD) st_elem<DT>(a.out, orow + d, o[dt][i] / l);
+    }
+}
+
 // o = sum_s e^(m_s - M) o_s / sum_s e^(m_s - M) l_s over the n_split splits
 // of one (query, head), in split order (empty splits have weight zero);
 // rounded to the storage dtype.  NSF > 0: at most NSF splits, whose partials
@@ -446,7 +562,35 @@ hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+template <int DT, int HD>
+hipError_t prefill_hd(int group, int nrows, const AttnArgs &a, hipStream_t st) {
+  constexpr int NW = 4;
+  const int qpt = 16 / group;
+  const dim3 grid(((nrows + qpt - 1) / qpt + NW - 1) / NW, a.n_kv), block(64 * NW);
+  switch (group) {
+    case 1: HS_LAUNCH((k_attn_prefill<DT, HD, 1, NW>), grid, block, 0, st, a); break;
+    case 2: HS_LAUNCH((k_attn_prefill<DT, HD, 2, NW>), grid, block, 0, st, a); break;
+    case 4: HS_LAUNCH((k_attn_prefill<DT, HD, 4, NW>), grid, block, 0, st, a); break;
+    case 7: HS_LAUNCH((k_attn_prefill<DT, HD, 7, NW>), grid, block, 0, st, a); break;
+    case 8: HS_LAUNCH((k_attn_prefill<DT, HD, 8, NW>), grid, block, 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool attn_prefill_on_mma(int dtype) { return dtype != HS_F32; }
+
+hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
+                                    hipStream_t st) {
+  if (nrows <= 0) return hipSuccess;
+  if (dtype == HS_F16) return head_dim == 64 ? prefill_hd<HS_F16, 64>(group, nrows, a, st)
+                                             : prefill_hd<HS_F16, 128>(group, nrows, a, st);
+  if (dtype == HS_BF16) return head_dim == 64 ? prefill_hd<HS_BF16, 64>(group, nrows, a, st)
+                                              : prefill_hd<HS_BF16, 128>(group, nrows, a, st);
+  return hipErrorInvalidValue;
+}
 
 bool attn_supported(int dtype, int head_dim, int group) {
   (void)dtype;

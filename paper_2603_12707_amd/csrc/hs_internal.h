@@ -97,6 +97,10 @@ hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, v
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
 hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);
 hipError_t launch_combine(int dtype, int head_dim, int nq, const AttnArgs &a, hipStream_t st);
+// causal prefill attention over the nrows rows of request a.prefill_req (a.S == nrows), 16-bit storage
+bool attn_prefill_on_mma(int dtype);
+hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
+                                    hipStream_t st);
 hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x,
                         int *status, hipStream_t st);
 hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *embed, int vocab, int d,
