@@ -92,7 +92,8 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
 
 void free_model(hs_model *m) {
   if (!m) return;
-  void *ptrs[] = {m->x, m->q, m->attn, m->act, m->hnorm, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
+  void *ptrs[] = {m->x,      m->q,      m->attn,     m->act,      m->hnorm,  m->splitk,
+                  m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
@@ -202,6 +203,8 @@ struct Step {
     o.x = x;
     o.resid = m->x;
     o.ld_resid = c.d_model;
+    o.splitk_ws = m->splitk;
+    o.splitk_cap = m->splitk_floats;
     return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st);
   }
 
@@ -394,6 +397,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
     if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
   }
   m->part_entries = entries;
+  m->splitk_floats = (int64_t)SPLITK_MAX * max_batch * c.d_model;
 
   struct Alloc {
     void **p;
@@ -404,6 +408,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {&m->attn, (size_t)rows * nh * hd * b},
       {&m->act, (size_t)rows * c.ffn_dim * b},
       {&m->hnorm, (size_t)rows * c.d_model * b},
+      {(void **)&m->splitk, (size_t)m->splitk_floats * 4},
       {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
       {(void **)&m->part_o, (size_t)std::max<int64_t>(entries, 1) * hd * 4},
       {(void **)&m->part_ml, (size_t)std::max<int64_t>(entries, 1) * 2 * 4},

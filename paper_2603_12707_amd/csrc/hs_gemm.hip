@@ -8,6 +8,8 @@
 // every wave-wide load instruction reads 1 KB of contiguous HBM.
 #include "hs_device.h"
 
+#include <algorithm>
+
 namespace hs {
 namespace {
 
@@ -722,7 +724,6 @@ __global__ __launch_bounds__(64 * WR * WC) void k_gemm_tile(GemmArgs a) {
   constexpr int CE = Ty<DT>::CE;
   constexpr int SB = (int)sizeof(S);
   constexpr int D = 2;
-  constexpr int RTG = WR * RTW, CTG = WC * CTW;  // tiles per work group
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wr = wave / WC, wc = wave % WC;
@@ -827,6 +828,208 @@ __global__ __launch_bounds__(64 * WR * WC) void k_gemm_tile(GemmArgs a) {
   }
 }
 
+// Many columns (prefill rows, large batches) with both operands shared
+// through LDS: a work group of 8 waves (4 x 2) owns RTG row tiles (SwiGLU:
+// RTG/2 gate and the RTG/2 matching up tiles) by CTG column tiles, each wave
+// RTG/4 x CTG/2 of them.  K advances in stages of two 32-element sub-blocks:
+// the stage's weight sub-blocks (1 KB each, contiguous in the packed layout)
+// and activation sub-blocks are staged in LDS in MFMA operand order, and each
+// wave reads the operands of its output tiles from there (16 B per lane,
+// conflict free).  Global loads run two stages ahead through registers, LDS
+// is double buffered.  fp32 accumulation.
+constexpr int LG_NW = 8;
+template <int DT, int EPI, int RTG, int CTG>
+__global__ __launch_bounds__(64 * LG_NW) void k_gemm_lds(GemmArgs a) {
+  using S = typename Ty<DT>::S;
+  constexpr int CE = Ty<DT>::CE;
+  constexpr int SB = (int)sizeof(S);
+  constexpr int RTW = RTG / 4, CTW = CTG / 2;        // tiles per wave
+  constexpr int WSUB = RTG * 2, XSUB = CTG * 2;      // 1 KB sub-blocks per stage
+  constexpr int WPT = WSUB / LG_NW, XPT = XSUB / LG_NW;  // of them moved per thread
+  static_assert(WSUB % LG_NW == 0 && XSUB % LG_NW == 0, "stage split over the waves");
+  static_assert(EPI != EPI_SWIGLU || RTW % 2 == 0, "gate/up pairs per wave");
+  __shared__ __align__(16) u32x4 s_w[2][WSUB * 64];
+  __shared__ __align__(16) u32x4 s_x[2][XSUB * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = wave >> 1, wc = wave & 1;
+  const int li = lane & 15, lq = lane >> 4;
+  const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4, nsb = nkb * 4;
+  // XCD-aware order: the (column group, K split) units of a row group are
+  // consecutive slots of one XCD
+  const int nks = a.k_split > 1 ? a.k_split : 1, nu = a.n_colg * nks;
+  int rg = blockIdx.x, cg = 0, ks = 0;
+  if (nu > 1) {
+    const int slot = (int)blockIdx.x >> 3, u = slot % nu;
+    cg = u % a.n_colg;
+    ks = u / a.n_colg;
+    rg = (slot / nu) * 8 + ((int)blockIdx.x & 7);
+    if (rg >= a.n_groups) return;
+  }
+  // this work group's K range, in 32-element sub-blocks [g_begin, g_end)
+  const int kb_split = (nkb + nks - 1) / nks;
+  const int g_begin = ks * kb_split * 4, g_end = min(nsb, (ks + 1) * kb_split * 4);
+  const int nstage = g_end > g_begin ? (g_end - g_begin + 1) / 2 : 0;
+  // row tile t of the work group (wave t / RTW) -> matrix and first row
+  auto tile_of = [&](int t, int &m, int &r0) {
+    if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int H = RTW / 2;
+      const int w = t / RTW, k = t % RTW;
+      m = k < H ? 0 : 1;
+      r0 = 16 * (rg * (RTG / 2) + w * H + k % H);
+    } else if constexpr (EPI == EPI_QKV) {
+      const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
+      int mm = 0, u = rg * RTG + t;
+      if (u >= tq) {
+        u -= tq;
+        mm = 1;
+        if (u >= tk) {
+          u -= tk;
+          mm = 2;
+        }
+      }
+      m = mm;
+      r0 = 16 * u;  // past the v rows for a partial last group
+    } else {
+      m = 0;
+      r0 = 16 * (rg * RTG + t);
+    }
+  };
+  const int colg0 = cg * CTG * 16;
+  const rsrc_t xres = make_rsrc(a.x, (uint32_t)a.ncols * K * SB);
+  // stage loads: thread (wave, lane) moves lane `lane` of sub-blocks
+  // wave + 8 u; sub-block b of a stage is row tile (column tile) b / 2, k
+  // sub-block b % 2 of the stage, so every buffer resource is wave-uniform
+  rsrc_t wres[WPT];
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int t = (wave + LG_NW * u) >> 1;
+    int m, r0;
+    tile_of(t, m, r0);
+    wres[u] = make_rsrc((const S *)a.w[m] + (int64_t)(r0 >> 4) * nkb * 256 * CE,
+                        r0 < a.rows[m] ? (uint32_t)nkb * 4096u : 0u);
+  }
+  auto gload = [&](u32x4 (&wv)[WPT], u32x4 (&xv)[XPT], int st) {
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int g = g_begin + st * 2 + ((wave + LG_NW * u) & 1);
+      wv[u] = bld16_stream(wres[u], g < g_end ? (uint32_t)(g >> 2) * 4096u + (uint32_t)(g & 3) * 1024u +
+                                                    (uint32_t)lane * 16u
+                                              : BUF_OOB);
+    }
+#pragma unroll
+    for (int u = 0; u < XPT; ++u) {
+      const int sbk = wave + LG_NW * u, ct = sbk >> 1, g = g_begin + st * 2 + (sbk & 1);
+      const int col = colg0 + ct * 16 + li, kc = g * 4 + lq;
+      xv[u] = bld16(xres, g < g_end && col < a.ncols && kc < kchunks ? (uint32_t)(col * K + kc * CE) * SB : BUF_OOB);
+    }
+  };
+  auto lstore = [&](const u32x4 (&wv)[WPT], const u32x4 (&xv)[XPT], int buf) {
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) s_w[buf][(wave + LG_NW * u) * 64 + lane] = wv[u];
+#pragma unroll
+    for (int u = 0; u < XPT; ++u) s_x[buf][(wave + LG_NW * u) * 64 + lane] = xv[u];
+  };
+
+  f32x4 acc[RTW][CTW];
+#pragma unroll
+  for (int r = 0; r < RTW; ++r)
+#pragma unroll
+    for (int c = 0; c < CTW; ++c) acc[r][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 ra_w[WPT], ra_x[XPT], rb_w[WPT], rb_x[XPT];
+  gload(ra_w, ra_x, 0);
+  lstore(ra_w, ra_x, 0);
+  gload(ra_w, ra_x, 1);
+  gload(rb_w, rb_x, 2);
+  __syncthreads();
+  for (int st0 = 0; st0 < nstage; st0 += 2) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int st = st0 + h, buf = h;  // stage st sits in LDS buffer st % 2
+      if (st < nstage) {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          u32x4 av[RTW], bv[CTW];
+#pragma unroll
+          for (int r = 0; r < RTW; ++r) av[r] = s_w[buf][((wr * RTW + r) * 2 + sub) * 64 + lane];
+#pragma unroll
+          for (int c = 0; c < CTW; ++c) bv[c] = s_x[buf][((wc * CTW + c) * 2 + sub) * 64 + lane];
+#pragma unroll
+          for (int r = 0; r < RTW; ++r)
+#pragma unroll
+            for (int c = 0; c < CTW; ++c) acc[r][c] = mma<DT>(av[r], bv[c], acc[r][c]);
+        }
+      }
+      // stage st + 1 (in registers since two stages ago) into the other
+      // buffer, then request stage st + 3 into the registers it leaves
+      if (h == 0) {
+        lstore(ra_w, ra_x, 1);
+        gload(ra_w, ra_x, st + 3);
+      } else {
+        lstore(rb_w, rb_x, 0);
+        gload(rb_w, rb_x, st + 3);
+      }
+      __syncthreads();
+    }
+  }
+
+  const int rr = 4 * lq;
+  int mat[RTW], row0[RTW];
+#pragma unroll
+  for (int r = 0; r < RTW; ++r) tile_of(wr * RTW + r, mat[r], row0[r]);
+#pragma unroll
+  for (int c = 0; c < CTW; ++c) {
+    const int col = colg0 + (wc * CTW + c) * 16 + li;
+    if (col >= a.ncols) continue;
+    if constexpr (EPI == EPI_SWIGLU) {
+      constexpr int H = RTW / 2;
+#pragma unroll
+      for (int r = 0; r < H; ++r) {
+        const int m2[2] = {0, 1}, r2[2] = {row0[r], row0[r + H]};
+        const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
+        gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
+      }
+    } else if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+      for (int r = 0; r < RTW; ++r) {
+        QkvIn<1> in;
+        qkv_fetch_ids<DT, 1>(a, &mat[r], &row0[r], col, rr, true, in);
+        qkv_fetch_tab<DT, 1>(a, &mat[r], &row0[r], rr, true, in);
+        qkv_store<DT, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
+      }
+    } else if (EPI == EPI_RESID && nks > 1) {
+      // K split: this split's fp32 partial, summed into the residual later
+      float *o = a.splitk_ws + ((int64_t)ks * a.ncols + col) * a.rows[0];
+#pragma unroll
+      for (int r = 0; r < RTW; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = row0[r] + rr + e;
+          if (row < a.rows[0]) o[row] = acc[r][c][e];
+        }
+    } else {
+#pragma unroll
+      for (int r = 0; r < RTW; ++r) gemm_epilogue<DT, EPI, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr);
+    }
+  }
+}
+
+// x[col][row] += the K-split partials of (col, row), in split order; four
+// rows per thread (rows % 4 == 0)
+__global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int k_split, int ncols, int rows, float *x,
+                                                   int ld_x) {
+  const int n4 = rows / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)ncols * n4) return;
+  const int col = (int)(i / n4), row = (int)(i % n4) * 4;
+  const int64_t slice = (int64_t)ncols * rows;
+  f32x4 s = *(const f32x4 *)(part + (int64_t)col * rows + row);
+  for (int k = 1; k < k_split; ++k) s += *(const f32x4 *)(part + k * slice + (int64_t)col * rows + row);
+  f32x4 *xp = (f32x4 *)(x + (int64_t)col * ld_x + row);
+  *xp += s;
+}
+
 // ---------------------------------------------------------------------------
 // launch shapes
 // ---------------------------------------------------------------------------
@@ -884,8 +1087,52 @@ hipError_t gemm_tile_launch(const GemmArgs &a, int tiles16, hipStream_t st) {
   return hipGetLastError();
 }
 
+// work groups of the LDS kernel with RTG x CTG tiles (and k_split K splits)
+template <int EPI, int RTG, int CTG>
+int lds_groups(const GemmArgs &a, int tiles16, int k_split, int &n_groups, int &n_colg) {
+  const int rows_per_group = EPI == EPI_SWIGLU ? RTG / 2 : RTG;
+  n_groups = (tiles16 + rows_per_group - 1) / rows_per_group;
+  n_colg = (a.ncols + 16 * CTG - 1) / (16 * CTG);
+  const int nu = n_colg * k_split;
+  return nu > 1 ? (n_groups + 7) / 8 * 8 * nu : n_groups;
+}
+
+template <int DT, int EPI, int RTG, int CTG>
+hipError_t gemm_lds_launch(const GemmArgs &a, int tiles16, int k_split, hipStream_t st) {
+  GemmArgs g = a;
+  g.k_split = k_split;
+  const int blocks = lds_groups<EPI, RTG, CTG>(a, tiles16, k_split, g.n_groups, g.n_colg);
+  HS_LAUNCH((k_gemm_lds<DT, EPI, RTG, CTG>), dim3(blocks), dim3(64 * LG_NW), 0, st, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || k_split <= 1) return e;
+  const int64_t n = (int64_t)a.ncols * (a.rows[0] / 4);
+  HS_LAUNCH(k_splitk_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.splitk_ws, k_split, a.ncols,
+            a.rows[0], a.resid, a.ld_resid);
+  return hipGetLastError();
+}
+
+// Many columns.  A residual GEMM with fewer than SPLITK_BELOW work groups
+// splits K (up to SPLITK_MAX ways, at least 4 k-blocks each) when the
+// partials fit the workspace.  Otherwise the LDS-staged kernel from
+// LDS_MIN_GROUPS work groups up, and below that the register-tiled kernel,
+// whose smaller work groups spread narrow matrices over more CUs (measured
+// crossover: between 64 and 80 work groups of the LDS kernel).
+constexpr int LDS_MIN_GROUPS = 72, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
 template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
+  int ng, nc;
+  const int blocks = lds_groups<EPI, 8, 8>(p, tiles16, 1, ng, nc);
+  if constexpr (EPI == EPI_RESID) {
+    const int nkb = (p.K / Ty<DT>::CE + 15) / 16;
+    int ks = blocks < SPLITK_BELOW ? std::min(std::min(SPLITK_MAX, (SPLITK_TARGET + blocks - 1) / blocks), nkb / 4) : 1;
+    if (ks > 1) {
+      const int per = (nkb + ks - 1) / ks;
+      ks = (nkb + per - 1) / per;  // no empty split
+    }
+    if (ks > 1 && p.splitk_ws && p.rows[0] % 4 == 0 && (int64_t)ks * p.ncols * p.rows[0] <= p.splitk_cap)
+      return gemm_lds_launch<DT, EPI, 8, 8>(p, tiles16, ks, st);
+  }
+  if (blocks >= LDS_MIN_GROUPS) return gemm_lds_launch<DT, EPI, 8, 8>(p, tiles16, 1, st);
   if constexpr (EPI == EPI_SWIGLU) return gemm_tile_launch<DT, 4, 4, 2, 2, EPI>(p, tiles16, st);
   else if constexpr (EPI == EPI_RESID) return gemm_tile_launch<DT, 2, 2, 1, 4, EPI>(p, tiles16, st);
   else return gemm_tile_launch<DT, 2, 4, 2, 2, EPI>(p, tiles16, st);

@@ -36,6 +36,11 @@ struct GemmArgs {
   int ld_out;
   float *resid; // residual stream fp32 [ncols][ld_resid], updated in place
   int ld_resid;
+  // residual epilogue split over K: fp32 partials [k_split][ncols][rows[0]]
+  // (workspace of splitk_cap floats), summed into resid in split order
+  float *splitk_ws;
+  int64_t splitk_cap;
+  int k_split;  // set by the launcher
   // q/k/v epilogue: RoPE and KV append
   int head_dim, n_heads, n_kv;
   void *kv;
@@ -55,6 +60,8 @@ struct GemmArgs {
 };
 
 enum { PRO_PLAIN = 0, PRO_NORM = 1, PRO_COMBINE = 2 };
+// most K splits of a residual GEMM over many columns
+constexpr int SPLITK_MAX = 4;
 // the attention combine runs in the projection's prologue for at most this
 // many splits (and activations that fit the prologue's LDS copy)
 constexpr int COMBINE_FUSE_SPLITS = 8;
@@ -127,6 +134,8 @@ struct hs_model {
   void *attn = nullptr;     // [max_rows][n_h * d_h] attention output
   void *act = nullptr;      // [max_rows][F] SwiGLU output
   void *hnorm = nullptr;    // [max_rows][d] normalised rows for GEMMs over many columns
+  float *splitk = nullptr;  // [SPLITK_MAX][max_batch][d] residual GEMM partials
+  int64_t splitk_floats = 0;
   float *logits = nullptr;  // [max_batch][V] (used when the caller passes no logits buffer)
   float *part_o = nullptr;
   float *part_ml = nullptr;

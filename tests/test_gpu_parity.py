@@ -114,6 +114,18 @@ def test_column_tiles(B):
     assert near <= 2
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_many_columns_split_k(dtype):
+    """40 requests (three column tiles) and a long, ragged down projection
+    (K = 2040): the residual GEMM splits K four ways into fp32 partials and
+    sums them into the residual stream."""
+    cfg = small_cfg(n_layers=1, ffn_dim=2040, dtype=dtype)
+    n_v = [(11 * b) % 29 for b in range(40)]
+    s_text = [1 + (3 * b) % 7 for b in range(40)]
+    near = _run_pair(cfg, n_v, s_text, 2)
+    assert near <= 2
+
+
 @pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
 def test_long_context_many_splits(n_v, dtype):
     """Contexts long enough for many attention splits in decode: at most 8
