@@ -59,9 +59,30 @@ def step_bytes(cfg: dict, lens: list) -> int:
     return L * per_layer + wb["head"] + B * d * b + sum(kv_row * (n + 1) for n in lens) + B * kv_row
 
 
-def kernel_source_hash() -> str:
+def attn_bytes(cfg: dict, lens: list) -> int:
+    """Algorithmic bytes of one attention launch (one layer): K and V rows
+    0..len_b of every request, its q rows read and its output rows written."""
+    b = 2 if cfg["dtype"] != "f32" else 4
+    nkv, nh, hd = cfg["n_kv_heads"], cfg["n_heads"], cfg["head_dim"]
+    return sum(2 * nkv * hd * (n + 1) * b for n in lens) + len(lens) * 2 * nh * hd * b
+
+
+# what each replayable kind launches, for the roofline line
+KIND_NAMES = {
+    "qkv": "q/k/v projection (RMSNorm + GEMM + RoPE + KV append)",
+    "attn": "split-K attention over the KV cache",
+    "oproj": "O projection + residual",
+    "gateup": "gate/up projection (RMSNorm + GEMM + SwiGLU)",
+    "down": "down projection + residual",
+    "head": "final RMSNorm + LM head",
+}
+
+
+def kernel_source_hash(kind: str = "gateup") -> str:
+    """Hash of the sources that build the kernels of one replayable kind."""
     h = hashlib.sha256()
-    for rel in ("paper_2603_12707_amd/csrc/hs_gemm.hip", "paper_2603_12707_amd/csrc/hs_device.h",
+    main = "hs_attn.hip" if kind in ("attn", "combine") else "hs_gemm.hip"
+    for rel in ("paper_2603_12707_amd/csrc/" + main, "paper_2603_12707_amd/csrc/hs_device.h",
                 "paper_2603_12707_amd/csrc/hs_internal.h"):
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
@@ -77,7 +98,7 @@ def stored_traffic(workload: str, kernel: str):
     text = open(path).read()
     src = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
     val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not src or not val or src.group(1) != kernel_source_hash():
+    if not src or not val or src.group(1) != kernel_source_hash(kernel):
         return None
     return float(val.group(1))
 
@@ -238,20 +259,10 @@ def main() -> int:
         kv.sync()
         lens_after = [n - 2 * (reps_g + 1) for n in kv.lengths()]
 
-    # dominant kernel (gate/up projection): replayed back to back over every
-    # layer's weights, HIP events around the batch on the stream the library
-    # launches on (torch's current stream)
-    dominant = "gateup"
-    reps = 4 * cfg["n_layers"]
+    # per-kernel breakdown, the same way for every replayable kind: each
+    # layer's launch replayed once, HIP events around the batch on the stream
+    # the library launches on (torch's current stream)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    kv.replay(dominant, cfg["n_layers"])  # warm
-    ev0.record()
-    kv.replay(dominant, reps)
-    ev1.record()
-    torch.cuda.synchronize()
-    dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
-
-    # per-kernel breakdown, the same way for every replayable kind
     breakdown = {}
     for kind in ("qkv", "attn", "combine", "oproj", "gateup", "down", "head"):
         try:
@@ -263,6 +274,19 @@ def main() -> int:
         ev1.record()
         torch.cuda.synchronize()
         breakdown[kind] = ev0.elapsed_time(ev1) / cfg["n_layers"] * 1e3  # us per launch
+
+    # dominant kernel: the kind with the most time per step, replayed back
+    # to back over every layer's weights (4 passes)
+    per_step = {k: v * (1 if k == "head" else cfg["n_layers"]) for k, v in breakdown.items() if k in KIND_NAMES}
+    dominant = max(per_step, key=per_step.get)
+    lens_replay = kv.lengths()
+    reps = 4 * cfg["n_layers"]
+    kv.replay(dominant, cfg["n_layers"])  # warm
+    ev0.record()
+    kv.replay(dominant, reps)
+    ev1.record()
+    torch.cuda.synchronize()
+    dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
 
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
@@ -278,12 +302,12 @@ def main() -> int:
     gbs = total_bytes / elapsed / 1e9
     assert lens_after == [n + args.steps for n in lens_start], (lens_after[:4], lens_start[:4])
 
-    dom_bytes = weight_bytes(cfg)[dominant]
+    dom_bytes = attn_bytes(cfg, lens_replay) if dominant == "attn" else weight_bytes(cfg)[dominant]
     achieved = dom_bytes / dom_avg_s / 1e9
     traffic = stored_traffic(args.workload, dominant)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "k_gemm (RMSNorm + gate/up projection + SwiGLU)",
+                "kernel": KIND_NAMES[dominant], "kind": dominant,
                 "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps}
     kernels = {k: round(v, 2) for k, v in breakdown.items()}
 
