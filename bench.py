@@ -104,6 +104,7 @@ def stored_traffic(workload: str, kernel: str):
 
 
 DEFAULT_WARMUP, DEFAULT_STEPS = 8, 120
+PREFILL_ROWS = 16384  # packed prefill rows per pass at batch > 1
 
 
 def steps_after_context(warmup: int, steps: int) -> int:
@@ -147,11 +148,21 @@ def setup(cfg: dict, n_steps_total: int):
             kv.set_length(r, lens[r], lens[r])
         first.copy_(synth.decode_tokens(cfg, 0, B, device="cuda"))
     else:
-        for r in range(B):
-            emb = synth.vision_rows(cfg, r, n_v[r], device="cuda")
-            ids = synth.text_ids(cfg, r, s_text[r], device="cuda")
-            pos = synth.mrope_positions(n_v[r], s_text[r]).cuda() if cfg["rope_kind"] == 1 else None
-            kv.prefill(r, emb if n_v[r] else None, ids if s_text[r] else None, pos, first_token=first[r:r + 1])
+        # inputs first, packed request by request; then the timed prefill
+        embs = [synth.vision_rows(cfg, r, n_v[r], device="cuda") for r in range(B) if n_v[r]]
+        idss = [synth.text_ids(cfg, r, s_text[r], device="cuda") for r in range(B) if s_text[r]]
+        emb = torch.cat(embs) if embs else None
+        ids = torch.cat(idss) if idss else None
+        pos = (torch.cat([synth.mrope_positions(n_v[r], s_text[r]) for r in range(B)], dim=1).contiguous().cuda()
+               if cfg["rope_kind"] == 1 else None)
+        if B > 1:  # room for several requests per packed pass
+            model.reserve_rows(min(sum(lens), PREFILL_ROWS))
+        torch.cuda.synchronize()
+        t = time.time()
+        if B == 1:
+            kv.prefill(0, emb, ids, pos, first_token=first)
+        else:
+            kv.prefill_batch(list(range(B)), emb, ids, s_text, pos, first_tokens=first)
     torch.cuda.synchronize()
     ready_s = time.time() - t
     log(f"context ready for {B} request(s) in {ready_s * 1e3:.1f} ms (lengths {min(lens)}..{max(lens)})")

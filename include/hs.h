@@ -23,8 +23,9 @@
  *     (workspaces and per-request metadata) and frees it in the matching
  *     *_free call.
  *   - Calls taking a stream are asynchronous on that stream (NULL = the
- *     default stream).  hs_decode_step and hs_prefill_embeddings allocate no
- *     device memory and perform no device-to-host copy.
+ *     default stream).  hs_decode_step, hs_prefill_embeddings and
+ *     hs_prefill_batch allocate no device memory and perform no
+ *     device-to-host copy.
  *   - Argument, state and capacity checks run on host-side mirrors before any
  *     launch; a failing call launches nothing and changes no state.
  *
@@ -177,6 +178,40 @@ int hs_kv_free(hs_kv *kv);
 int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, const int32_t *text_ids,
                           int32_t s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_token,
                           hs_stream_t stream);
+
+/* Language prefill of n requests at once (§5.4: prefill of the requests whose
+ * embeddings have arrived; §5.2 "Aligned Batch Handoff" hands them over in
+ * batches).  Their rows are packed request by request, each request's rows
+ * as in hs_prefill_embeddings (vision rows, then text rows):
+ *   reqs      host int32 [n], distinct requests of the handle, all empty;
+ *   emb       device, model dtype: the vision rows of reqs[0], then of
+ *             reqs[1], ... ([sum_i n_v(reqs[i])][d], n_v as given to
+ *             hs_kv_alloc; 16-byte aligned; NULL if that sum is 0);
+ *   text_ids  device int32: the text ids of reqs[0], then of reqs[1], ...
+ *             ([sum_i s_text[i]]; NULL if that sum is 0);
+ *   s_text    host int32 [n];
+ *   pos_thw   HS_ROPE_M3: device int32 [3][R], R = sum_i (n_v + s_text[i]),
+ *             section-major (all rows' t ids, then h, then w), rows packed as
+ *             above; HS_ROPE_1D: NULL (row r of a request is position r);
+ *   first_tokens  device int32 [n]: the first generated token of reqs[i];
+ *   last_logits   device fp32 [n][vocab] or NULL.
+ * The requests are taken in order, in passes of at most 32 requests whose rows
+ * fit the model's row workspaces (max(max_batch, max_ctx) rows, or what
+ * hs_model_reserve_rows set); with last_logits NULL a pass also holds at most
+ * max_batch requests.  Each pass runs every layer once over all its rows:
+ * the projections as GEMMs over the packed rows, attention causal within
+ * each request.  Every check (requests, lengths, capacities, pointers) runs
+ * before the first launch. */
+int hs_prefill_batch(hs_model *m, hs_kv *kv, int32_t n, const int32_t *reqs, const void *emb,
+                     const int32_t *text_ids, const int32_t *s_text, const int32_t *pos_thw, float *last_logits,
+                     int32_t *first_tokens, hs_stream_t stream);
+
+/* Grows the model's row workspaces (residual stream, q, attention and SwiGLU
+ * outputs, normalised rows) to hold `rows` packed prefill rows, so that
+ * hs_prefill_batch packs more requests per pass; never shrinks them.  It
+ * allocates, and waits for the device to go idle before freeing the old
+ * buffers: call it outside any stream capture and not from a serving loop. */
+int hs_model_reserve_rows(hs_model *m, int64_t rows);
 
 /* One greedy decode step for every request of the handle: request b embeds
  * tokens_in[b] (device int32 [batch]), writes its K/V rows at position len_b,

@@ -92,21 +92,23 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
 
 void free_model(hs_model *m) {
   if (!m) return;
-  void *ptrs[] = {m->x,      m->q,      m->attn,     m->act,      m->hnorm,  m->splitk,
-                  m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
+  void *ptrs[] = {m->x,     m->q,      m->attn,   m->act,     m->hnorm,    m->splitk,
+                  m->xlast, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
 }
 
 // The launches of one pass over ncols activation rows held in m->x: decode
-// (one row per request, prefill_req < 0) or prefill (one row per position of
-// request prefill_req).  Each member launches one kernel.
+// (one row per request, prefill = 0) or prefill (the packed rows of the
+// requests in pk).  Each member launches one kernel.
 struct Step {
   hs_model *m;
   hs_kv *kv;
-  int ncols, prefill_req;
+  int ncols, prefill;
+  PackedRows pk;
   const int *rope_pos;
+  int rope_ld;
   int S, n_split;
   hipStream_t st;
 
@@ -140,8 +142,11 @@ struct Step {
     g.kv_cap = kv->d_cap;
     g.kv_len = kv->d_len;
     g.layer = l;
-    g.prefill_req = prefill_req;
+    g.prefill = prefill;
+    g.pk = pk;
+    g.kv_nreq = kv->batch;
     g.rope_pos = rope_pos;
+    g.rope_ld = rope_ld;
     g.rope_m3 = c.rope_kind == HS_ROPE_M3;
     g.sec0 = c.mrope_section[0];
     g.sec1 = c.mrope_section[0] + c.mrope_section[1];
@@ -163,7 +168,8 @@ struct Step {
     a.layer = l;
     a.n_heads = c.n_heads;
     a.n_kv = c.n_kv_heads;
-    a.prefill_req = prefill_req;
+    a.prefill = prefill;
+    a.pk = pk;
     a.S = S;
     a.n_split = n_split;
     a.part_o = m->part_o;
@@ -175,7 +181,7 @@ struct Step {
 
   hipError_t attn(int l) const {
     const hs_config &c = m->cfg;
-    if (prefill_req >= 0 && attn_prefill_on_mma(c.dtype))
+    if (prefill && attn_prefill_on_mma(c.dtype))
       return launch_attention_prefill(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
     return launch_attention(c.dtype, c.head_dim, c.n_heads / c.n_kv_heads, ncols, attn_args(l), st);
   }
@@ -289,7 +295,91 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out) {
   split_policy(B, c.n_kv_heads, c.n_heads / c.n_kv_heads, c.head_dim, c.dtype, kv->max_cap, &S, &ns);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
-  *out = Step{m, kv, B, -1, kv->d_rope, S, ns, st};
+  *out = Step{m, kv, B, 0, PackedRows{}, kv->d_rope, B, S, ns, st};
+  return HS_OK;
+}
+
+// Prefill of n requests (§5.4: the language prefill from the transferred
+// embedding rows).  Their rows are packed request by request; the requests are
+// taken in order, in passes of at most PACK_MAX requests whose rows fit the row
+// workspaces, and each pass runs every layer once over all its rows.
+int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const void *emb, const int32_t *text_ids,
+                     const int32_t *s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_tokens,
+                     hs_stream_t stream, const char *fn) {
+  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "%s: model/handle mismatch", fn);
+  if (!m->w.lm_head) return fail(HS_E_STATE, "%s: model has no LM head", fn);
+  if (!first_tokens) return fail(HS_E_INVALID, "%s: first_token is NULL", fn);
+  if (n <= 0 || n > kv->batch || !reqs || !s_text) return fail(HS_E_INVALID, "%s: bad request list", fn);
+  const hs_config &c = m->cfg;
+  int64_t total = 0, total_v = 0, total_t = 0;
+  std::vector<char> seen(kv->batch, 0);
+  for (int i = 0; i < n; ++i) {
+    const int req = reqs[i];
+    if (req < 0 || req >= kv->batch) return fail(HS_E_INVALID, "%s: request %d out of range", fn, req);
+    if (seen[req]) return fail(HS_E_INVALID, "%s: request %d listed twice", fn, req);
+    seen[req] = 1;
+    if (s_text[i] < 0) return fail(HS_E_INVALID, "%s: negative s_text", fn);
+    const int s_ctx = kv->n_v[req] + s_text[i];
+    if (s_ctx <= 0) return fail(HS_E_INVALID, "%s: empty context", fn);
+    if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "%s: request %d is not empty", fn, req);
+    if (s_ctx > kv->cap[req])
+      return fail(HS_E_CAPACITY, "%s: context %d exceeds capacity %d", fn, s_ctx, kv->cap[req]);
+    total += s_ctx;
+    total_v += kv->n_v[req];
+    total_t += s_text[i];
+  }
+  if ((total_v > 0 && !emb) || (total_t > 0 && !text_ids))
+    return fail(HS_E_INVALID, "%s: missing embedding rows or text ids", fn);
+  if (((uintptr_t)emb) % 16) return fail(HS_E_INVALID, "%s: emb must be 16-byte aligned", fn);
+  if (c.rope_kind == HS_ROPE_M3 && !pos_thw) return fail(HS_E_INVALID, "%s: M-RoPE needs pos_thw", fn);
+  if (c.rope_kind == HS_ROPE_1D && pos_thw) return fail(HS_E_INVALID, "%s: 1-D RoPE takes no pos_thw", fn);
+  if (total > INT32_MAX) return fail(HS_E_INVALID, "%s: too many rows", fn);
+  hipStream_t st = (hipStream_t)stream;
+  const int b = dtype_bytes(c.dtype);
+  // without a caller logits buffer, a pass's logits go to the [max_batch][V] workspace
+  const int max_np = last_logits ? PACK_MAX : std::min(PACK_MAX, m->max_batch);
+  int64_t voff = 0, toff = 0, roff = 0;
+  for (int i0 = 0; i0 < n;) {
+    PackedRows pk{};
+    int rows = 0;
+    while (i0 + pk.n < n && pk.n < max_np) {
+      const int k = i0 + pk.n, s_ctx = kv->n_v[reqs[k]] + s_text[k];
+      if (pk.n > 0 && rows + s_ctx > m->rows) break;  // one request always fits (s_ctx <= max_ctx <= rows)
+      pk.req[pk.n] = reqs[k];
+      pk.cu[pk.n] = rows;
+      rows += s_ctx;
+      ++pk.n;
+    }
+    pk.cu[pk.n] = rows;
+    for (int k = 0; k < pk.n; ++k) {
+      const int nv = kv->n_v[pk.req[k]], nt = s_text[i0 + k];
+      HIP_TRY(launch_prefill_rows(c.dtype, (const char *)emb + voff * c.d_model * b, nv, m->w.embed, c.vocab,
+                                  c.d_model, text_ids ? text_ids + toff : nullptr, nt, m->x + (int64_t)pk.cu[k] * c.d_model,
+                                  m->status, st));
+      voff += nv;
+      toff += nt;
+    }
+    // every row is its own query over the rows before it in its request; no
+    // splits (S covers the longest request)
+    Step pre{m, kv, rows, 1, pk, pos_thw ? pos_thw + roff : nullptr, (int)total, rows, 1, st};
+    const int rc = pre.layers();
+    if (rc) return rc;
+    HIP_TRY(launch_gather_last(m->x, c.d_model, pk, m->xlast, st));
+    float *lg = last_logits ? last_logits + (int64_t)i0 * c.vocab : m->logits;
+    Step last = pre;
+    last.ncols = pk.n;
+    HIP_TRY(last.head(m->xlast, lg));
+    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, pk.n, first_tokens + i0, nullptr, nullptr, 0, st));
+    for (int k = 0; k < pk.n; ++k)
+      HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, pk.req[k], pk.cu[k + 1] - pk.cu[k],
+                                    pos_thw ? pos_thw + roff + pk.cu[k] : nullptr, (int)total, st));
+    for (int k = 0; k < pk.n; ++k) {
+      kv->len[pk.req[k]] = pk.cu[k + 1] - pk.cu[k];
+      kv->ready[pk.req[k]] = 1;
+    }
+    roff += rows;
+    i0 += pk.n;
+  }
   return HS_OK;
 }
 
@@ -381,6 +471,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   const hs_config &c = *cfg;
   const int b = dtype_bytes(c.dtype), hd = c.head_dim, nh = c.n_heads;
   const int64_t rows = std::max(max_batch, max_ctx);
+  m->rows = rows;
 
   // attention partial capacity: the largest (queries x heads x splits) any
   // decode batch <= max_batch with capacities <= max_ctx, or any prefill of
@@ -409,6 +500,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {&m->act, (size_t)rows * c.ffn_dim * b},
       {&m->hnorm, (size_t)rows * c.d_model * b},
       {(void **)&m->splitk, (size_t)m->splitk_floats * 4},
+      {(void **)&m->xlast, (size_t)PACK_MAX * c.d_model * 4},
       {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
       {(void **)&m->part_o, (size_t)std::max<int64_t>(entries, 1) * hd * 4},
       {(void **)&m->part_ml, (size_t)std::max<int64_t>(entries, 1) * 2 * 4},
@@ -517,38 +609,43 @@ int hs_kv_free(hs_kv *kv) {
 int hs_prefill_embeddings(hs_model *m, hs_kv *kv, int32_t req, const void *emb, const int32_t *text_ids,
                           int32_t s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_token,
                           hs_stream_t stream) {
-  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_prefill_embeddings: model/handle mismatch");
-  if (req < 0 || req >= kv->batch) return fail(HS_E_INVALID, "hs_prefill_embeddings: request %d out of range", req);
-  if (!m->w.lm_head) return fail(HS_E_STATE, "hs_prefill_embeddings: model has no LM head");
-  if (!first_token) return fail(HS_E_INVALID, "hs_prefill_embeddings: first_token is NULL");
-  if (s_text < 0) return fail(HS_E_INVALID, "hs_prefill_embeddings: negative s_text");
+  return prefill_requests(m, kv, 1, &req, emb, text_ids, &s_text, pos_thw, last_logits, first_token, stream,
+                          "hs_prefill_embeddings");
+}
+
+int hs_prefill_batch(hs_model *m, hs_kv *kv, int32_t n, const int32_t *reqs, const void *emb,
+                     const int32_t *text_ids, const int32_t *s_text, const int32_t *pos_thw, float *last_logits,
+                     int32_t *first_tokens, hs_stream_t stream) {
+  return prefill_requests(m, kv, n, reqs, emb, text_ids, s_text, pos_thw, last_logits, first_tokens, stream,
+                          "hs_prefill_batch");
+}
+
+int hs_model_reserve_rows(hs_model *m, int64_t rows) {
+  if (!m) return fail(HS_E_INVALID, "hs_model_reserve_rows: model is NULL");
+  if (rows <= 0 || rows > (1 << 24)) return fail(HS_E_INVALID, "hs_model_reserve_rows: rows %lld out of range", (long long)rows);
+  if (rows <= m->rows) return HS_OK;
   const hs_config &c = m->cfg;
-  const int n_v = kv->n_v[req], s_ctx = n_v + s_text;
-  if (s_ctx <= 0) return fail(HS_E_INVALID, "hs_prefill_embeddings: empty context");
-  if ((n_v > 0 && !emb) || (s_text > 0 && !text_ids))
-    return fail(HS_E_INVALID, "hs_prefill_embeddings: missing embedding rows or text ids");
-  if (((uintptr_t)emb) % 16) return fail(HS_E_INVALID, "hs_prefill_embeddings: emb must be 16-byte aligned");
-  if (c.rope_kind == HS_ROPE_M3 && !pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: M-RoPE needs pos_thw");
-  if (c.rope_kind == HS_ROPE_1D && pos_thw) return fail(HS_E_INVALID, "hs_prefill_embeddings: 1-D RoPE takes no pos_thw");
-  if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "hs_prefill_embeddings: request %d is not empty", req);
-  if (s_ctx > kv->cap[req])
-    return fail(HS_E_CAPACITY, "hs_prefill_embeddings: context %d exceeds capacity %d", s_ctx, kv->cap[req]);
-  // prefill: every row is its own query over the rows before it; no splits
-  // (S = s_ctx, the row count, which the causal kernel reads)
-  const int S = s_ctx, ns = 1;
-  hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(launch_prefill_rows(c.dtype, emb, n_v, m->w.embed, c.vocab, c.d_model, text_ids, s_text, m->x, m->status, st));
-  Step pre{m, kv, s_ctx, req, pos_thw, S, ns, st};
-  int rc = pre.layers();
-  if (rc) return rc;
-  float *lg = last_logits ? last_logits : m->logits;
-  Step last = pre;
-  last.ncols = 1;
-  HIP_TRY(last.head(m->x + (int64_t)(s_ctx - 1) * c.d_model, lg));
-  HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, 1, first_token, nullptr, nullptr, 0, st));
-  HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, req, s_ctx, pos_thw, st));
-  kv->len[req] = s_ctx;
-  kv->ready[req] = 1;
+  const int b = dtype_bytes(c.dtype), nhd = c.n_heads * c.head_dim;
+  void *fresh[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  const size_t bytes[5] = {(size_t)rows * c.d_model * 4, (size_t)rows * nhd * b, (size_t)rows * nhd * b,
+                           (size_t)rows * c.ffn_dim * b, (size_t)rows * c.d_model * b};
+  for (int i = 0; i < 5; ++i)
+    if (hipMalloc(&fresh[i], bytes[i]) != hipSuccess) {
+      for (void *p : fresh)
+        if (p) (void)hipFree(p);
+      return fail(HS_E_DEVICE, "hs_model_reserve_rows: hipMalloc of %zu bytes failed", bytes[i]);
+    }
+  // the old buffers may still be in use by queued work
+  if (hipDeviceSynchronize() != hipSuccess) {
+    for (void *p : fresh) (void)hipFree(p);
+    return fail(HS_E_DEVICE, "hs_model_reserve_rows: device synchronisation failed");
+  }
+  void **slots[5] = {(void **)&m->x, &m->q, &m->attn, &m->act, &m->hnorm};
+  for (int i = 0; i < 5; ++i) {
+    (void)hipFree(*slots[i]);
+    *slots[i] = fresh[i];
+  }
+  m->rows = rows;
   return HS_OK;
 }
 

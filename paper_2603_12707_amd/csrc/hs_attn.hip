@@ -44,12 +44,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   constexpr int UB = attn_batch(G);       // iterations per batch of loads
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
   int req, L;
-  if (a.prefill_req < 0) {
+  if (!a.prefill) {
     req = qi;
     L = a.kv_len[qi] + 1;
   } else {
-    req = a.prefill_req;
-    L = qi + 1;
+    const int i = packed_request(a.pk, qi);
+    req = a.pk.req[i];
+    L = qi - a.pk.cu[i] + 1;
   }
   const int cap = a.kv_cap[req];
   L = min(L, cap);
@@ -205,12 +206,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   constexpr int STEP = NW * 16;       // positions per work-group iteration
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
   int req, L;
-  if (a.prefill_req < 0) {
+  if (!a.prefill) {
     req = qi;
     L = a.kv_len[qi] + 1;
   } else {
-    req = a.prefill_req;
-    L = qi + 1;
+    const int i = packed_request(a.pk, qi);
+    req = a.pk.req[i];
+    L = qi - a.pk.cu[i] + 1;
   }
   const int cap = a.kv_cap[req];
   L = min(L, cap);
@@ -372,11 +374,15 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lg = lane >> 4;
   const int j = blockIdx.y;
-  const int nrows = a.S;  // rows of the prefill
-  const int q0 = ((int)blockIdx.x * NW + wave) * QPT;
-  if (q0 >= nrows) return;  // whole wave; no barrier below
-  const int req = a.prefill_req, cap = a.kv_cap[req];
-  const int sq = q0 + li / G, sh = li % G;  // the lane column's query row and head
+  // the wave's query tile: tile t - tcu[i] of packed request i
+  const int t = (int)blockIdx.x * NW + wave;
+  if (t >= a.pk.tcu[a.pk.n]) return;  // whole wave; no barrier below
+  int pi = 0;
+  for (int k = 1; k < a.pk.n; ++k) pi += t >= a.pk.tcu[k];
+  const int roff = a.pk.cu[pi], nrows = a.pk.cu[pi + 1] - roff;
+  const int q0 = (t - a.pk.tcu[pi]) * QPT;
+  const int req = a.pk.req[pi], cap = a.kv_cap[req];
+  const int sq = q0 + li / G, sh = li % G;  // the lane column's query position and head
   const bool slot = li < QPT * G && sq < nrows;
   const int qlast = min(q0 + QPT - 1, nrows - 1);
   const int n_kt = qlast / 16 + 1;  // key tiles
@@ -389,7 +395,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   u32x4 qb[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk)
-    qb[kk] = slot ? ld16((const uint16_t *)a.q + (int64_t)sq * a.ld_q + (j * G + sh) * HD + (kk * 4 + lg) * 8)
+    qb[kk] = slot ? ld16((const uint16_t *)a.q + (int64_t)(roff + sq) * a.ld_q + (j * G + sh) * HD + (kk * 4 + lg) * 8)
                   : u32x4{0u, 0u, 0u, 0u};
 
   float m = -INFINITY, l = 0.f;
@@ -458,7 +464,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   }
   if (!slot) return;
   // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
-  const int64_t orow = ((int64_t)sq * a.n_heads + j * G + sh) * HD;
+  const int64_t orow = ((int64_t)(roff + sq) * a.n_heads + j * G + sh) * HD;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
@@ -563,10 +569,13 @@ hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
 }
 
 template <int DT, int HD>
-hipError_t prefill_hd(int group, int nrows, const AttnArgs &a, hipStream_t st) {
+hipError_t prefill_hd(int group, const AttnArgs &args, hipStream_t st) {
   constexpr int NW = 4;
   const int qpt = 16 / group;
-  const dim3 grid(((nrows + qpt - 1) / qpt + NW - 1) / NW, a.n_kv), block(64 * NW);
+  AttnArgs a = args;
+  a.pk.tcu[0] = 0;
+  for (int i = 0; i < a.pk.n; ++i) a.pk.tcu[i + 1] = a.pk.tcu[i] + (a.pk.cu[i + 1] - a.pk.cu[i] + qpt - 1) / qpt;
+  const dim3 grid((a.pk.tcu[a.pk.n] + NW - 1) / NW, a.n_kv), block(64 * NW);
   switch (group) {
     case 1: HS_LAUNCH((k_attn_prefill<DT, HD, 1, NW>), grid, block, 0, st, a); break;
     case 2: HS_LAUNCH((k_attn_prefill<DT, HD, 2, NW>), grid, block, 0, st, a); break;
@@ -584,11 +593,11 @@ bool attn_prefill_on_mma(int dtype) { return dtype != HS_F32; }
 
 hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
                                     hipStream_t st) {
-  if (nrows <= 0) return hipSuccess;
-  if (dtype == HS_F16) return head_dim == 64 ? prefill_hd<HS_F16, 64>(group, nrows, a, st)
-                                             : prefill_hd<HS_F16, 128>(group, nrows, a, st);
-  if (dtype == HS_BF16) return head_dim == 64 ? prefill_hd<HS_BF16, 64>(group, nrows, a, st)
-                                              : prefill_hd<HS_BF16, 128>(group, nrows, a, st);
+  if (nrows <= 0 || a.pk.n <= 0) return hipSuccess;
+  if (dtype == HS_F16) return head_dim == 64 ? prefill_hd<HS_F16, 64>(group, a, st)
+                                             : prefill_hd<HS_F16, 128>(group, a, st);
+  if (dtype == HS_BF16) return head_dim == 64 ? prefill_hd<HS_BF16, 64>(group, a, st)
+                                              : prefill_hd<HS_BF16, 128>(group, a, st);
   return hipErrorInvalidValue;
 }
 

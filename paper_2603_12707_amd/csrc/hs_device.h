@@ -176,6 +176,13 @@ __device__ __forceinline__ u32x2 bld8(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
+// request (index into pk) of packed prefill row `row`
+__device__ __forceinline__ int packed_request(const PackedRows &pk, int row) {
+  int i = 0;
+  for (int k = 1; k < pk.n; ++k) i += row >= pk.cu[k];
+  return i;
+}
+
 // ---------------------------------------------------------------------------
 // cross-lane reductions (DPP within 16-lane rows, then across rows)
 // ---------------------------------------------------------------------------

@@ -138,17 +138,23 @@ struct QkvIn {
 template <int DT, int R>
 __device__ __forceinline__ void qkv_fetch_ids(const GemmArgs &a, const int *mat, const int *row0, int col, int rr,
                                               bool ok, QkvIn<R> &in) {
-  const bool dec = a.prefill_req < 0;
-  const int nreq = dec ? a.ncols : a.prefill_req + 1, req = dec ? col : a.prefill_req;
+  const bool dec = !a.prefill;
+  // prefill: the packed row's request and its position in that request
+  int req = col, ppos = 0;
+  if (!dec) {
+    const int i = packed_request(a.pk, col);
+    req = a.pk.req[i];
+    ppos = col - a.pk.cu[i];
+  }
   const rsrc_t lr = make_rsrc(a.kv_len, dec ? (uint32_t)a.ncols * 4u : 0u);
-  const rsrc_t cr = make_rsrc(a.kv_cap, (uint32_t)nreq * 4u);
-  const rsrc_t br = make_rsrc(a.kv_base, (uint32_t)nreq * 8u);
-  const rsrc_t pr = make_rsrc(a.rope_pos, dec ? (uint32_t)a.ncols * 4u : (a.rope_m3 ? 3u * a.ncols * 4u : 0u));
+  const rsrc_t cr = make_rsrc(a.kv_cap, (uint32_t)a.kv_nreq * 4u);
+  const rsrc_t br = make_rsrc(a.kv_base, (uint32_t)a.kv_nreq * 8u);
+  const rsrc_t pr = make_rsrc(a.rope_pos, dec ? (uint32_t)a.ncols * 4u : (a.rope_m3 ? 3u * a.rope_ld * 4u : 0u));
   const uint32_t pl = bld4(lr, ok && dec ? (uint32_t)col * 4u : BUF_OOB);
   in.cap = (int)bld4(cr, ok ? (uint32_t)req * 4u : BUF_OOB);
   const u32x2 bb = bld8(br, ok ? (uint32_t)req * 8u : BUF_OOB);
   in.base = (int64_t)(((uint64_t)bb[1] << 32) | bb[0]);
-  in.pos = dec ? (int)pl : col;
+  in.pos = dec ? (int)pl : ppos;
   const int hd = a.head_dim;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -157,8 +163,8 @@ __device__ __forceinline__ void qkv_fetch_ids(const GemmArgs &a, const int *mat,
     for (int e = 0; e < 2; ++e) {
       const int i = j0 + e, sec = i < a.sec0 ? 0 : (i < a.sec1 ? 1 : 2);
       const bool rot = ok && mat[r] < 2 && (dec || a.rope_m3);
-      const uint32_t pv = bld4(pr, rot ? (uint32_t)(dec ? col : sec * a.ncols + col) * 4u : BUF_OOB);
-      in.p[r][e] = (dec || a.rope_m3) ? (int)pv : col;
+      const uint32_t pv = bld4(pr, rot ? (uint32_t)(dec ? col : sec * a.rope_ld + col) * 4u : BUF_OOB);
+      in.p[r][e] = (dec || a.rope_m3) ? (int)pv : in.pos;
     }
   }
 }

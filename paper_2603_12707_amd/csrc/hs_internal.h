@@ -15,6 +15,19 @@ namespace hs {
 // Arguments of the weight-streaming GEMM  Y[c][n] = sum_k X[c][k] * W[n][k].
 // Columns c are activation rows (decode requests or prefill rows); rows n are
 // output features.  Row tiles of 16 are enumerated over up to three matrices.
+// The rows of one prefill pass: up to PACK_MAX requests, their rows packed
+// request by request.  Request i of the pass is KV request req[i] and owns the
+// rows cu[i] .. cu[i + 1] - 1, its positions 0 .. cu[i + 1] - cu[i] - 1.
+// tcu is set by the prefill attention launcher: request i's query tiles are
+// tcu[i] .. tcu[i + 1] - 1.
+constexpr int PACK_MAX = 32;
+struct PackedRows {
+  int n;
+  int cu[PACK_MAX + 1];
+  int req[PACK_MAX];
+  int tcu[PACK_MAX + 1];
+};
+
 struct GemmArgs {
   const void *w[3];
   const void *bias[3];
@@ -48,8 +61,11 @@ struct GemmArgs {
   const int *kv_cap;
   const int *kv_len;
   int layer;
-  int prefill_req;     // < 0: decode (column = request, position = len); else prefill row = position
-  const int *rope_pos; // decode: [ncols]; prefill M-RoPE: [3][ncols]; prefill 1-D: NULL
+  int prefill;         // 0: decode (column = request, position = len); 1: prefill rows described by pk
+  PackedRows pk;
+  int kv_nreq;         // entries of kv_base / kv_cap
+  const int *rope_pos; // decode: [ncols]; prefill M-RoPE: [3][rope_ld] (section-major); prefill 1-D: NULL
+  int rope_ld;
   int rope_m3;
   int sec0, sec1;      // M-RoPE section boundaries (pairs)
   const float *rope_tab;
@@ -87,7 +103,8 @@ struct AttnArgs {
   const int *kv_len;
   int layer;
   int n_heads, n_kv;
-  int prefill_req; // < 0: decode (query = request, length = len + 1); else prefill row r, length r + 1
+  int prefill;     // 0: decode (query = request, length = len + 1); 1: prefill rows described by pk
+  PackedRows pk;   // prefill: query row r of request i has length r - cu[i] + 1
   int S;           // positions per split
   int n_split;     // splits per (query, kv head)
   float *part_o;   // [nq][n_heads][n_split][head_dim]
@@ -104,7 +121,7 @@ hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, v
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
 hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);
 hipError_t launch_combine(int dtype, int head_dim, int nq, const AttnArgs &a, hipStream_t st);
-// causal prefill attention over the nrows rows of request a.prefill_req (a.S == nrows), 16-bit storage
+// causal prefill attention over the packed rows of a.pk (nrows in all), 16-bit storage
 bool attn_prefill_on_mma(int dtype);
 hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
                                     hipStream_t st);
@@ -115,7 +132,11 @@ hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *
 hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
                          int advance, hipStream_t st);
 hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st);
-hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, hipStream_t st);
+// len[req] = s_ctx and the next RoPE position; pos_thw: [3][ld] section-major, this request's s_ctx columns
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, int ld,
+                                 hipStream_t st);
+// out[i] = x[pk.cu[i + 1] - 1] for the pk.n requests (rows of d floats)
+hipError_t launch_gather_last(const float *x, int d, const PackedRows &pk, float *out, hipStream_t st);
 
 bool attn_supported(int dtype, int head_dim, int group);
 
@@ -127,6 +148,7 @@ struct hs_model {
   std::vector<hs_layer_weights> layers;
   int device = 0;
   int max_batch = 0, max_ctx = 0;
+  int64_t rows = 0;         // capacity of the row workspaces below (max_rows)
   int64_t part_entries = 0; // capacity of the attention partial buffers in (query, head, split) entries
   // workspaces (device)
   float *x = nullptr;       // [max_rows][d] residual stream
@@ -136,6 +158,7 @@ struct hs_model {
   void *hnorm = nullptr;    // [max_rows][d] normalised rows for GEMMs over many columns
   float *splitk = nullptr;  // [SPLITK_MAX][max_batch][d] residual GEMM partials
   int64_t splitk_floats = 0;
+  float *xlast = nullptr;   // [PACK_MAX][d] last rows of the requests of a prefill pass
   float *logits = nullptr;  // [max_batch][V] (used when the caller passes no logits buffer)
   float *part_o = nullptr;
   float *part_ml = nullptr;

@@ -132,11 +132,12 @@ __global__ void k_advance(int *len, int *rope, int n) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int req, int s_ctx, const int *pos_thw) {
+__global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int req, int s_ctx, const int *pos_thw,
+                                                        int ld) {
   int mx = s_ctx - 1;
   if (pos_thw) {
     mx = 0x80000000;
-    for (int i = threadIdx.x; i < 3 * s_ctx; i += 256) mx = max(mx, pos_thw[i]);
+    for (int i = threadIdx.x; i < 3 * s_ctx; i += 256) mx = max(mx, pos_thw[(i / s_ctx) * ld + i % s_ctx]);
     for (int off = 32; off >= 1; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
     __shared__ int s_mx[4];
     if ((threadIdx.x & 63) == 0) s_mx[threadIdx.x >> 6] = mx;
@@ -147,6 +148,12 @@ __global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int
     len[req] = s_ctx;
     rope[req] = mx + 1;
   }
+}
+
+__global__ __launch_bounds__(256) void k_gather_last(const float *x, int d, PackedRows pk, float *out) {
+  const float *src = x + (int64_t)(pk.cu[blockIdx.x + 1] - 1) * d;
+  float *dst = out + (int64_t)blockIdx.x * d;
+  for (int i = threadIdx.x; i < d; i += 256) dst[i] = src[i];
 }
 
 }  // namespace
@@ -189,8 +196,15 @@ hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, hipStream_t st) {
-  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw);
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, int ld,
+                                 hipStream_t st) {
+  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw, ld);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_last(const float *x, int d, const PackedRows &pk, float *out, hipStream_t st) {
+  if (pk.n <= 0) return hipSuccess;
+  HS_LAUNCH(k_gather_last, dim3(pk.n), dim3(256), 0, st, x, d, pk, out);
   return hipGetLastError();
 }
 

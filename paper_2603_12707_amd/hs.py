@@ -20,7 +20,8 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 # every symbol include/hs.h declares
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
-           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync")
+           "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync",
+           "hs_prefill_batch", "hs_model_reserve_rows")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -78,6 +79,8 @@ def lib() -> ctypes.CDLL:
         "hs_kv_alloc": [P, I32, P, P, P, U64, ctypes.POINTER(P)],
         "hs_kv_free": [P],
         "hs_prefill_embeddings": [P, P, I32, P, P, I32, P, P, P, P],
+        "hs_prefill_batch": [P, P, I32, P, P, P, P, P, P, P, P],
+        "hs_model_reserve_rows": [P, I64],
         "hs_decode_step": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
@@ -219,6 +222,10 @@ class Model:
         self.handle = h
         self.max_batch, self.max_ctx = max_batch, max_ctx
 
+    def reserve_rows(self, rows: int) -> None:
+        """Room for `rows` packed prefill rows per pass (grows only)."""
+        _call("hs_model_reserve_rows", self.handle, rows)
+
     def status(self) -> int:
         f = ctypes.c_int32()
         _call("hs_model_status", self.handle, ctypes.byref(f))
@@ -265,6 +272,20 @@ class KVCache:
               0 if text_ids is None else text_ids.numel(), _ptr(pos_thw), _ptr(last_logits), _ptr(first_token),
               _stream())
         return first_token
+
+    def prefill_batch(self, reqs, emb, text_ids, s_text, pos_thw=None, last_logits=None, first_tokens=None):
+        """Prefill of several requests with their rows packed request by
+        request: emb holds their vision rows back to back, text_ids their
+        text ids, pos_thw (M-RoPE) [3][rows]; returns first_tokens [n]."""
+        import torch
+        n = len(reqs)
+        if first_tokens is None:
+            first_tokens = torch.empty(n, dtype=torch.int32, device="cuda")
+        r = (ctypes.c_int32 * n)(*reqs)
+        t = (ctypes.c_int32 * n)(*s_text)
+        _call("hs_prefill_batch", self.model.handle, self.handle, n, r, _ptr(emb), _ptr(text_ids), t, _ptr(pos_thw),
+              _ptr(last_logits), _ptr(first_tokens), _stream())
+        return first_tokens
 
     def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None) -> None:
         _call("hs_decode_step", self.model.handle, self.handle, _ptr(tokens_in), _ptr(tokens_out), _ptr(logits),

@@ -178,6 +178,38 @@ def test_error_paths():
     assert e.value.code == hs.HS_E_INVALID
 
 
+def test_prefill_batch_error_paths_launch_nothing():
+    """Every request of a batch prefill is checked before the first launch:
+    a failing call leaves all requests empty."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(dtype="bf16", n_layers=1)
+    model = _model(cfg, max_batch=3, max_ctx=32)
+    kv = hs.KVCache(model, [2, 0, 1], [8, 8, 4])
+    emb = torch.cat([synth.vision_rows(cfg, 0, 2), synth.vision_rows(cfg, 2, 1)]).cuda()
+    ids = synth.text_ids(cfg, 0, 9).cuda()
+    cases = [
+        ([0, 0], [3, 3], hs.HS_E_INVALID),        # request listed twice
+        ([0, 3], [3, 3], hs.HS_E_INVALID),        # request out of range
+        ([0, 2], [3, 4], hs.HS_E_CAPACITY),       # request 2: 1 + 4 rows > capacity 4
+        ([1], [0], hs.HS_E_INVALID),              # empty context
+        ([0, 1, 2, 0], [1, 1, 1, 1], hs.HS_E_INVALID),  # more requests than the handle holds
+    ]
+    for reqs, s_text, code in cases:
+        with pytest.raises(hs.HsError) as e:
+            kv.prefill_batch(reqs, emb, ids, s_text)
+        assert e.value.code == code, (reqs, e.value)
+        assert kv.lengths() == [0, 0, 0]
+    with pytest.raises(hs.HsError) as e:
+        model.reserve_rows(0)
+    assert e.value.code == hs.HS_E_INVALID
+    kv.prefill_batch([2, 0], emb[[2, 0, 1]].contiguous(), ids[:5], [2, 3])
+    assert kv.lengths() == [5, 0, 3]
+    with pytest.raises(hs.HsError) as e:
+        kv.prefill_batch([1, 0], None, ids[:4], [1, 3])  # request 0 already prefilled
+    assert e.value.code == hs.HS_E_STATE
+    assert kv.lengths() == [5, 0, 3]
+
+
 def test_out_of_range_token_is_flagged_and_read_as_zero():
     import paper_2603_12707_amd as hs
     cfg = small_cfg(dtype="f16", n_layers=1)

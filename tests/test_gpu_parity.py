@@ -13,10 +13,23 @@ from workload import configs, synth
 pytestmark = pytest.mark.gpu
 
 
-def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False):
+def _packed_inputs(inputs, order):
+    """The inputs of the requests in `order`, packed request by request as
+    hs_prefill_batch takes them (device tensors or None)."""
+    embs = [inputs[b][0] for b in order if inputs[b][0].shape[0]]
+    ids = [inputs[b][1] for b in order if inputs[b][1].shape[0]]
+    pos = [inputs[b][2] for b in order] if inputs[order[0]][2] is not None else None
+    return (torch.cat(embs).cuda() if embs else None, torch.cat(ids).cuda() if ids else None,
+            torch.cat(pos, dim=1).contiguous().cuda() if pos else None)
+
+
+def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False, packed=None):
     """Prefills every request on both sides, then runs n_dec decode steps for
     the whole batch (teacher-forced on the oracle's tokens unless
-    free_running).  Returns the number of near ties."""
+    free_running).  With packed = {"order": [...], "rows": R}, the GPU side
+    prefills all requests in one hs_prefill_batch call, in that order, with
+    the row workspaces grown to R rows (0: as created).  Returns the number
+    of near ties."""
     import paper_2603_12707_amd as hs
     B = len(n_v_list)
     caps = [n + s + n_dec + extra_cap for n, s in zip(n_v_list, s_text_list)]
@@ -25,22 +38,41 @@ def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False
     seqs, cur_ref, cur_gpu = [], [], []
     near = 0
     V = cfg["vocab"]
+    inputs = [pair.request_inputs(b, n_v_list[b], s_text_list[b]) for b in range(B)]
+    refs = []
     for b in range(B):
-        emb, ids, pos = pair.request_inputs(b, n_v_list[b], s_text_list[b])
+        emb, ids, pos = inputs[b]
         s = pair.ora.new_seq(caps[b])
-        ref_logits, ref_tok = s.prefill(emb if n_v_list[b] else None, ids, pos)
+        refs.append(s.prefill(emb if n_v_list[b] else None, ids, pos))
         seqs.append(s)
-        lg = torch.empty(V, dtype=torch.float32, device="cuda")
-        tok = kv.prefill(b, emb.cuda() if n_v_list[b] else None, ids.cuda() if s_text_list[b] else None,
-                         None if pos is None else pos.cuda(), last_logits=lg)
+    g_first = [None] * B
+    if packed is None:
+        for b in range(B):
+            emb, ids, pos = inputs[b]
+            lg = torch.empty(V, dtype=torch.float32, device="cuda")
+            tok = kv.prefill(b, emb.cuda() if n_v_list[b] else None, ids.cuda() if s_text_list[b] else None,
+                             None if pos is None else pos.cuda(), last_logits=lg)
+            torch.cuda.synchronize()
+            g_first[b] = (int(tok.item()), lg.cpu().numpy())
+    else:
+        order = packed["order"]
+        if packed.get("rows"):
+            pair.gpu.reserve_rows(packed["rows"])
+        emb, ids, pos = _packed_inputs(inputs, order)
+        lg = torch.empty(len(order), V, dtype=torch.float32, device="cuda")
+        toks = kv.prefill_batch(order, emb, ids, [s_text_list[b] for b in order], pos, last_logits=lg)
         torch.cuda.synchronize()
-        g = lg.cpu().numpy()
+        for k, b in enumerate(order):
+            g_first[b] = (int(toks[k].item()), lg[k].cpu().numpy())
+    for b in range(B):
+        ref_logits, ref_tok = refs[b]
+        tok, g = g_first[b]
         assert rel_err(g, ref_logits) <= LOGIT_TOL, (b, rel_err(g, ref_logits))
-        ok, tie = token_ok(int(tok.item()), g, ref_logits)
-        assert ok, (b, int(tok.item()), ref_tok)
+        ok, tie = token_ok(tok, g, ref_logits)
+        assert ok, (b, tok, ref_tok)
         near += tie
         cur_ref.append(ref_tok)
-        cur_gpu.append(int(tok.item()))
+        cur_gpu.append(tok)
     assert kv.lengths() == [n + s for n, s in zip(n_v_list, s_text_list)]
     tin = torch.empty(B, dtype=torch.int32, device="cuda")
     tout = torch.empty(B, dtype=torch.int32, device="cuda")
@@ -111,6 +143,42 @@ def test_column_tiles(B):
     n_v = [(7 * b) % 23 for b in range(B)]
     s_text = [1 + (5 * b) % 11 for b in range(B)]
     near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 2
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f32"])
+def test_packed_prefill_mha(dtype):
+    """Six requests of mixed shapes (no vision rows, no text, one row)
+    prefilled by one hs_prefill_batch call in a shuffled order; the row
+    workspaces hold 86 rows (the largest capacity), so the 225 rows go in
+    three packed passes."""
+    cfg = small_cfg(n_layers=2, dtype=dtype)
+    n_v = [0, 37, 70, 1, 16, 45]
+    s_text = [9, 0, 13, 0, 30, 4]
+    near = _run_pair(cfg, n_v, s_text, 3, packed={"order": [4, 1, 5, 0, 3, 2], "rows": 0})
+    assert near <= 1
+
+
+def test_packed_prefill_gqa7_mrope_bias():
+    """Packed prefill with 7 query heads per KV head (2 query rows per matrix
+    tile), M-RoPE ids taken section-major over all packed rows, q/k/v bias;
+    one pass holds every request."""
+    cfg = small_cfg(n_heads=14, n_kv_heads=2, head_dim=64, dtype="bf16", rope_kind=1, mrope_section=(8, 12, 12),
+                    qkv_bias=1, rope_theta=1e6, rms_eps=1e-6)
+    n_v = [70, 16, 121, 9]
+    s_text = [12, 12, 3, 31]
+    near = _run_pair(cfg, n_v, s_text, 3, packed={"order": [2, 0, 3, 1], "rows": 512})
+    assert near <= 1
+
+
+def test_packed_prefill_more_requests_than_a_pass():
+    """37 short requests: a pass takes at most 32 of them."""
+    cfg = small_cfg(n_layers=1, dtype="bf16")
+    B = 37
+    n_v = [(5 * b) % 11 for b in range(B)]
+    s_text = [1 + (3 * b) % 6 for b in range(B)]
+    order = list(range(B))[::-1]
+    near = _run_pair(cfg, n_v, s_text, 2, packed={"order": order, "rows": 4096})
     assert near <= 2
 
 
