@@ -164,6 +164,41 @@ int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *c
                 uint64_t buf_bytes, hs_kv **out);
 int hs_kv_free(hs_kv *kv);
 
+/* A block-granular KV cache for serving (§5.4 "Lazy KV Cache Allocation":
+ * KV memory is taken only when a request enters prefill, and grows with it).
+ * dev_buf (caller-owned, 16-byte aligned) is cut into blocks of block_tokens
+ * positions; a block holds those positions for every (layer, K|V, KV head):
+ * kv_bytes(block_tokens) = 2 * n_layers * n_kv * head_dim * block_tokens * b
+ * bytes, and the buffer holds floor(buf_bytes / that) blocks.  Element
+ * (layer l, K|V = s, kv head j, position p, channel e) of the request in
+ * slot r sits at
+ *   start(r, p / block_tokens) + (((l * 2 + s) * n_kv + j) * block_tokens
+ *                                 + p % block_tokens) * head_dim + e,
+ * start(r, k) being the element offset of the k-th block the slot holds.
+ * The handle has `slots` slots (1..4096), all empty; block_tokens is a power
+ * of two in 64..4096 (attention splits never cross a block); 16-bit storage
+ * only.  Blocks are handed out on the device, from a free list, as a slot's
+ * length reaches them: at prefill for the context, and inside
+ * hs_decode_step when a request enters a new block, so decode stays
+ * graph-replayable.  hs_prefill_embeddings / hs_prefill_batch take slot
+ * numbers as request numbers.  hs_decode_step runs over the slots holding a
+ * prefilled request, in slot order; tokens_in / tokens_out are indexed by
+ * slot ([slots]; other entries untouched) and logits / hidden_out rows
+ * follow that order.  Host-side checks refuse a prefill or step the free
+ * blocks cannot cover (HS_E_CAPACITY) before launching anything. */
+int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *dev_buf, uint64_t buf_bytes,
+                      hs_kv **out);
+/* Puts a request (n_v vision rows, at most `capacity` positions,
+ * capacity <= max_ctx) in an empty slot of a pooled cache; takes no block. */
+int hs_kv_admit(hs_kv *kv, int32_t slot, int32_t n_v, int32_t capacity, hs_stream_t stream);
+/* Ends the slot's request: its blocks return to the free list and the slot
+ * is empty again.  Stream-ordered: work queued before it on `stream` still
+ * sees the blocks. */
+int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream);
+/* Free and total blocks of a pooled cache (host mirror; exact after
+ * hs_kv_sync when graph replays have taken blocks). */
+int hs_kv_pool_blocks(const hs_kv *kv, int32_t *free_blocks, int32_t *n_blocks);
+
 /* Language prefill of request `req` from its projected visual embedding:
  * rows 0..n_v-1 are emb [n_v, d] (device, model dtype), rows n_v..n_v+s_text-1
  * are the embeddings of text_ids [s_text] (device int32, 0 <= id < vocab).

@@ -90,10 +90,44 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
   return 2ll * c.n_layers * c.n_kv_heads * (int64_t)c.head_dim * cap;
 }
 
+KvRef kv_ref(const hs_kv *kv) {
+  return KvRef{kv->buf,   kv->d_base, kv->d_toff, kv->d_bt,  kv->d_cap,
+               kv->d_len, kv->d_act,  kv->batch,  kv->ntab, kv->pool ? 1 : 0};
+}
+
+KvPool kv_pool(const hs_kv *kv) {
+  return KvPool{kv->d_base, kv->d_toff,  kv->d_cap, kv->d_len,   kv->d_rope,       kv->d_ready,
+                kv->d_nblk, kv->d_stack, kv->d_top, kv->m->status, kv->d_act, kv->block_tokens,
+                kv->block_elems};
+}
+
+int blocks_for(const hs_kv *kv, int len) { return (len + kv->block_tokens - 1) / kv->block_tokens; }
+
+// The split policy, with splits that never cross a block of a pooled cache:
+// a power of two between 64 (a multiple of every attention kernel's step)
+// and the block size.
+void kv_split_policy(const hs_config &c, bool pool, int block_tokens, int nq, int max_len, int *S, int *ns) {
+  split_policy(nq, c.n_kv_heads, c.n_heads / c.n_kv_heads, c.head_dim, c.dtype, max_len, S, ns);
+  if (!pool) return;
+  int s = 64;
+  while (s < *S && s < block_tokens) s *= 2;
+  *S = s;
+  *ns = (max_len + s - 1) / s;
+}
+
+// the ready requests, in order, as the decode columns (pooled caches)
+hipError_t rebuild_active(hs_kv *kv, hipStream_t st) {
+  kv->act_host.clear();
+  for (int r = 0; r < kv->batch; ++r)
+    if (kv->ready[r]) kv->act_host.push_back(r);
+  kv->n_active = (int)kv->act_host.size();
+  return launch_build_act(kv->d_ready, kv->batch, kv->d_act, st);
+}
+
 void free_model(hs_model *m) {
   if (!m) return;
-  void *ptrs[] = {m->x,     m->q,      m->attn,   m->act,     m->hnorm,    m->splitk,
-                  m->xlast, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
+  void *ptrs[] = {m->x,      m->q,      m->attn,    m->act,      m->hnorm,  m->splitk, m->xlast,
+                  m->pk_dev, m->logits, m->part_o, m->part_ml, m->rope_tab, m->status};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete m;
@@ -137,14 +171,10 @@ struct Step {
     g.head_dim = c.head_dim;
     g.n_heads = c.n_heads;
     g.n_kv = c.n_kv_heads;
-    g.kv = kv->buf;
-    g.kv_base = kv->d_base;
-    g.kv_cap = kv->d_cap;
-    g.kv_len = kv->d_len;
+    g.kv = kv_ref(kv);
     g.layer = l;
     g.prefill = prefill;
-    g.pk = pk;
-    g.kv_nreq = kv->batch;
+    g.pk = m->pk_dev;
     g.rope_pos = rope_pos;
     g.rope_ld = rope_ld;
     g.rope_m3 = c.rope_kind == HS_ROPE_M3;
@@ -153,7 +183,7 @@ struct Step {
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
-    return launch_gemm(c.dtype, PRO_NORM, EPI_QKV, g, st);
+    return launch_gemm(c.dtype, PRO_NORM, kv->pool ? EPI_QKV_PAGED : EPI_QKV, g, st);
   }
 
   AttnArgs attn_args(int l) const {
@@ -161,15 +191,13 @@ struct Step {
     AttnArgs a{};
     a.q = m->q;
     a.ld_q = c.n_heads * c.head_dim;
-    a.kv = kv->buf;
-    a.kv_base = kv->d_base;
-    a.kv_cap = kv->d_cap;
-    a.kv_len = kv->d_len;
+    a.kv = kv_ref(kv);
     a.layer = l;
     a.n_heads = c.n_heads;
     a.n_kv = c.n_kv_heads;
     a.prefill = prefill;
-    a.pk = pk;
+    a.pk = m->pk_dev;
+    a.prefill_tiles = pk.tcu[pk.n];
     a.S = S;
     a.n_split = n_split;
     a.part_o = m->part_o;
@@ -283,16 +311,24 @@ struct Step {
 };
 
 // The decode pass of a handle (checks that every request can take a step).
-int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out) {
+// A decode step runs over the handle's active requests: every request of a
+// contiguous cache (all must be prefilled), the ready requests of a pool.
+int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out, int *blocks_needed = nullptr) {
   const hs_config &c = m->cfg;
-  const int B = kv->batch;
+  const int B = kv->n_active;
+  if (B <= 0) return fail(HS_E_STATE, "decode: no prefilled request");
   if (B > m->max_batch) return fail(HS_E_INVALID, "decode: batch %d exceeds max_batch %d", B, m->max_batch);
-  for (int b = 0; b < B; ++b) {
+  int need = 0;
+  for (int b : kv->act_host) {
     if (!kv->ready[b]) return fail(HS_E_STATE, "decode: request %d is not prefilled", b);
     if (kv->len[b] >= kv->cap[b]) return fail(HS_E_CAPACITY, "decode: request %d is full (%d positions)", b, kv->cap[b]);
+    if (kv->pool) need += blocks_for(kv, kv->len[b] + 1) - kv->nblk[b];
   }
+  if (kv->pool && need > kv->free_blocks)
+    return fail(HS_E_CAPACITY, "decode: the pool has %d free blocks, the step needs %d", kv->free_blocks, need);
+  if (blocks_needed) *blocks_needed = need;
   int S, ns;
-  split_policy(B, c.n_kv_heads, c.n_heads / c.n_kv_heads, c.head_dim, c.dtype, kv->max_cap, &S, &ns);
+  kv_split_policy(c, kv->pool, kv->block_tokens, B, kv->max_cap, &S, &ns);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
   *out = Step{m, kv, B, 0, PackedRows{}, kv->d_rope, B, S, ns, st};
@@ -311,7 +347,7 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
   if (!first_tokens) return fail(HS_E_INVALID, "%s: first_token is NULL", fn);
   if (n <= 0 || n > kv->batch || !reqs || !s_text) return fail(HS_E_INVALID, "%s: bad request list", fn);
   const hs_config &c = m->cfg;
-  int64_t total = 0, total_v = 0, total_t = 0;
+  int64_t total = 0, total_v = 0, total_t = 0, blocks = 0;
   std::vector<char> seen(kv->batch, 0);
   for (int i = 0; i < n; ++i) {
     const int req = reqs[i];
@@ -319,6 +355,7 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     if (seen[req]) return fail(HS_E_INVALID, "%s: request %d listed twice", fn, req);
     seen[req] = 1;
     if (s_text[i] < 0) return fail(HS_E_INVALID, "%s: negative s_text", fn);
+    if (kv->pool && kv->cap[req] == 0) return fail(HS_E_STATE, "%s: slot %d holds no admitted request", fn, req);
     const int s_ctx = kv->n_v[req] + s_text[i];
     if (s_ctx <= 0) return fail(HS_E_INVALID, "%s: empty context", fn);
     if (kv->ready[req] || kv->len[req] != 0) return fail(HS_E_STATE, "%s: request %d is not empty", fn, req);
@@ -327,7 +364,11 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     total += s_ctx;
     total_v += kv->n_v[req];
     total_t += s_text[i];
+    if (kv->pool) blocks += blocks_for(kv, s_ctx) - kv->nblk[req];
   }
+  if (kv->pool && blocks > kv->free_blocks)
+    return fail(HS_E_CAPACITY, "%s: the pool has %d free blocks, the contexts need %lld", fn, kv->free_blocks,
+                (long long)blocks);
   if ((total_v > 0 && !emb) || (total_t > 0 && !text_ids))
     return fail(HS_E_INVALID, "%s: missing embedding rows or text ids", fn);
   if (((uintptr_t)emb) % 16) return fail(HS_E_INVALID, "%s: emb must be 16-byte aligned", fn);
@@ -351,6 +392,18 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
       ++pk.n;
     }
     pk.cu[pk.n] = rows;
+    const int qpt = attn_prefill_rows_per_tile(c.n_heads / c.n_kv_heads);
+    for (int k = 0; k < pk.n; ++k) pk.tcu[k + 1] = pk.tcu[k] + (pk.cu[k + 1] - pk.cu[k] + qpt - 1) / qpt;
+    HIP_TRY(launch_set_packed(m->pk_dev, pk, st));
+    if (kv->pool) {  // blocks for the pass's contexts
+      KvReserve r{};
+      r.n = pk.n;
+      for (int k = 0; k < pk.n; ++k) {
+        r.req[k] = pk.req[k];
+        r.target[k] = pk.cu[k + 1] - pk.cu[k];
+      }
+      HIP_TRY(launch_kv_reserve(kv_pool(kv), r, 0, st));
+    }
     for (int k = 0; k < pk.n; ++k) {
       const int nv = kv->n_v[pk.req[k]], nt = s_text[i0 + k];
       HIP_TRY(launch_prefill_rows(c.dtype, (const char *)emb + voff * c.d_model * b, nv, m->w.embed, c.vocab,
@@ -369,17 +422,23 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     Step last = pre;
     last.ncols = pk.n;
     HIP_TRY(last.head(m->xlast, lg));
-    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, pk.n, first_tokens + i0, nullptr, nullptr, 0, st));
+    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, pk.n, first_tokens + i0, nullptr, nullptr, nullptr, 0, st));
     for (int k = 0; k < pk.n; ++k)
-      HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, pk.req[k], pk.cu[k + 1] - pk.cu[k],
+      HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, kv->d_ready, pk.req[k], pk.cu[k + 1] - pk.cu[k],
                                     pos_thw ? pos_thw + roff + pk.cu[k] : nullptr, (int)total, st));
     for (int k = 0; k < pk.n; ++k) {
-      kv->len[pk.req[k]] = pk.cu[k + 1] - pk.cu[k];
-      kv->ready[pk.req[k]] = 1;
+      const int req = pk.req[k], s_ctx = pk.cu[k + 1] - pk.cu[k];
+      kv->len[req] = s_ctx;
+      kv->ready[req] = 1;
+      if (kv->pool) {
+        kv->free_blocks -= blocks_for(kv, s_ctx) - kv->nblk[req];
+        kv->nblk[req] = blocks_for(kv, s_ctx);
+      }
     }
     roff += rows;
     i0 += pk.n;
   }
+  if (kv->pool) HIP_TRY(rebuild_active(kv, st));
   return HS_OK;
 }
 
@@ -501,6 +560,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {&m->hnorm, (size_t)rows * c.d_model * b},
       {(void **)&m->splitk, (size_t)m->splitk_floats * 4},
       {(void **)&m->xlast, (size_t)PACK_MAX * c.d_model * 4},
+      {(void **)&m->pk_dev, sizeof(PackedRows)},
       {(void **)&m->logits, w->lm_head ? (size_t)max_batch * c.vocab * 4 : 0},
       {(void **)&m->part_o, (size_t)std::max<int64_t>(entries, 1) * hd * 4},
       {(void **)&m->part_ml, (size_t)std::max<int64_t>(entries, 1) * 2 * 4},
@@ -584,11 +644,24 @@ int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *c
     off += kv_request_elems(c, capacity[i]);
     kv->max_cap = std::max(kv->max_cap, capacity[i]);
   }
+  // one block per request: the block table is the base offsets, the block
+  // size the capacity; every request is a decode column
+  std::vector<int> ident(batch);
+  for (int i = 0; i < batch; ++i) ident[i] = i;
+  kv->ntab = batch;
+  kv->n_active = batch;
+  kv->act_host = ident;
   bool ok = hipMalloc(&kv->d_base, batch * 8) == hipSuccess && hipMalloc(&kv->d_cap, batch * 4) == hipSuccess &&
-            hipMalloc(&kv->d_len, batch * 4) == hipSuccess && hipMalloc(&kv->d_rope, batch * 4) == hipSuccess;
+            hipMalloc(&kv->d_len, batch * 4) == hipSuccess && hipMalloc(&kv->d_rope, batch * 4) == hipSuccess &&
+            hipMalloc(&kv->d_toff, batch * 4) == hipSuccess && hipMalloc(&kv->d_act, batch * 4) == hipSuccess &&
+            hipMalloc(&kv->d_ready, batch * 4) == hipSuccess;
   ok = ok && hipMemcpy(kv->d_base, kv->base.data(), batch * 8, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(kv->d_cap, kv->cap.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
-       hipMemset(kv->d_len, 0, batch * 4) == hipSuccess && hipMemset(kv->d_rope, 0, batch * 4) == hipSuccess;
+       hipMemcpy(kv->d_toff, ident.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_act, ident.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemset(kv->d_len, 0, batch * 4) == hipSuccess && hipMemset(kv->d_rope, 0, batch * 4) == hipSuccess &&
+       hipMemset(kv->d_ready, 0, batch * 4) == hipSuccess;
+  kv->d_bt = kv->d_cap;
   if (!ok) {
     hs_kv_free(kv);
     return fail(HS_E_DEVICE, "hs_kv_alloc: metadata allocation failed");
@@ -599,10 +672,133 @@ int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *c
 
 int hs_kv_free(hs_kv *kv) {
   if (!kv) return fail(HS_E_INVALID, "hs_kv_free: NULL");
-  void *ptrs[] = {kv->d_base, kv->d_cap, kv->d_len, kv->d_rope};
+  void *ptrs[] = {kv->d_base, kv->d_cap,  kv->d_len,   kv->d_rope, kv->d_toff, kv->d_act,
+                  kv->d_ready, kv->d_stack, kv->d_top, kv->d_nblk, kv->d_bt == kv->d_cap ? nullptr : kv->d_bt};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
   delete kv;
+  return HS_OK;
+}
+
+int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *dev_buf, uint64_t buf_bytes,
+                      hs_kv **out) {
+  if (!out) return fail(HS_E_INVALID, "hs_kv_pool_create: out is NULL");
+  *out = nullptr;
+  if (!m || !dev_buf) return fail(HS_E_INVALID, "hs_kv_pool_create: NULL argument");
+  const hs_config &c = m->cfg;
+  if (c.dtype == HS_F32) return fail(HS_E_INVALID, "hs_kv_pool_create: pooled caches take 16-bit storage");
+  if (slots <= 0 || slots > 4096) return fail(HS_E_INVALID, "hs_kv_pool_create: slots must be in 1..4096");
+  if (block_tokens < 64 || block_tokens > 4096 || (block_tokens & (block_tokens - 1)))
+    return fail(HS_E_INVALID, "hs_kv_pool_create: block_tokens must be a power of two in 64..4096");
+  if (((uintptr_t)dev_buf) % 16) return fail(HS_E_INVALID, "hs_kv_pool_create: buffer must be 16-byte aligned");
+  const int64_t block_elems = kv_request_elems(c, block_tokens);
+  const uint64_t block_bytes = (uint64_t)block_elems * dtype_bytes(c.dtype);
+  const uint64_t n_blocks = buf_bytes / block_bytes;
+  if (n_blocks < 1 || n_blocks > (1u << 30))
+    return fail(HS_E_BUFFER, "hs_kv_pool_create: buffer holds %llu blocks of %llu bytes",
+                (unsigned long long)n_blocks, (unsigned long long)block_bytes);
+  // attention partials for the block-aligned splits
+  int64_t entries = m->part_entries;
+  for (int nq = 1; nq <= std::min(slots, m->max_batch); ++nq) {
+    int S, ns;
+    kv_split_policy(c, true, block_tokens, nq, m->max_ctx, &S, &ns);
+    if (ns > 1) entries = std::max(entries, (int64_t)nq * c.n_heads * ns);
+  }
+  if (entries > m->part_entries) {
+    float *po = nullptr, *pm = nullptr;
+    if (hipMalloc(&po, (size_t)entries * c.head_dim * 4) != hipSuccess ||
+        hipMalloc(&pm, (size_t)entries * 2 * 4) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+      if (po) (void)hipFree(po);
+      if (pm) (void)hipFree(pm);
+      return fail(HS_E_DEVICE, "hs_kv_pool_create: attention workspace allocation failed");
+    }
+    (void)hipFree(m->part_o);
+    (void)hipFree(m->part_ml);
+    m->part_o = po;
+    m->part_ml = pm;
+    m->part_entries = entries;
+  }
+  hs_kv *kv = new (std::nothrow) hs_kv();
+  if (!kv) return fail(HS_E_DEVICE, "hs_kv_pool_create: out of host memory");
+  kv->m = m;
+  kv->batch = slots;
+  kv->buf = dev_buf;
+  kv->buf_bytes = buf_bytes;
+  kv->pool = true;
+  kv->block_tokens = block_tokens;
+  kv->block_elems = block_elems;
+  kv->n_blocks = (int)n_blocks;
+  kv->free_blocks = (int)n_blocks;
+  kv->max_blocks = (m->max_ctx + block_tokens - 1) / block_tokens;
+  kv->ntab = slots * kv->max_blocks;
+  kv->n_v.assign(slots, 0);
+  kv->cap.assign(slots, 0);
+  kv->len.assign(slots, 0);
+  kv->rope.assign(slots, 0);
+  kv->ready.assign(slots, 0);
+  kv->nblk.assign(slots, 0);
+  kv->n_active = 0;
+  std::vector<int64_t> tab(kv->ntab, -1);
+  std::vector<int> toff(slots), bt(slots, block_tokens), stack(n_blocks);
+  for (int i = 0; i < slots; ++i) toff[i] = i * kv->max_blocks;
+  for (uint64_t i = 0; i < n_blocks; ++i) stack[i] = (int)i;
+  const int top = (int)n_blocks;
+  const size_t sb = (size_t)slots * 4;
+  bool ok = hipMalloc(&kv->d_base, (size_t)kv->ntab * 8) == hipSuccess && hipMalloc(&kv->d_cap, sb) == hipSuccess &&
+            hipMalloc(&kv->d_len, sb) == hipSuccess && hipMalloc(&kv->d_rope, sb) == hipSuccess &&
+            hipMalloc(&kv->d_toff, sb) == hipSuccess && hipMalloc(&kv->d_bt, sb) == hipSuccess &&
+            hipMalloc(&kv->d_act, sb) == hipSuccess && hipMalloc(&kv->d_ready, sb) == hipSuccess &&
+            hipMalloc(&kv->d_nblk, sb) == hipSuccess && hipMalloc(&kv->d_stack, n_blocks * 4) == hipSuccess &&
+            hipMalloc(&kv->d_top, 4) == hipSuccess;
+  ok = ok && hipMemcpy(kv->d_base, tab.data(), (size_t)kv->ntab * 8, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_toff, toff.data(), sb, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_bt, bt.data(), sb, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_stack, stack.data(), n_blocks * 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_top, &top, 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemset(kv->d_cap, 0, sb) == hipSuccess && hipMemset(kv->d_len, 0, sb) == hipSuccess &&
+       hipMemset(kv->d_rope, 0, sb) == hipSuccess && hipMemset(kv->d_act, 0, sb) == hipSuccess &&
+       hipMemset(kv->d_ready, 0, sb) == hipSuccess && hipMemset(kv->d_nblk, 0, sb) == hipSuccess;
+  if (!ok) {
+    hs_kv_free(kv);
+    return fail(HS_E_DEVICE, "hs_kv_pool_create: metadata allocation failed");
+  }
+  *out = kv;
+  return HS_OK;
+}
+
+int hs_kv_admit(hs_kv *kv, int32_t slot, int32_t n_v, int32_t capacity, hs_stream_t stream) {
+  if (!kv || !kv->pool) return fail(HS_E_INVALID, "hs_kv_admit: not a pooled cache");
+  if (slot < 0 || slot >= kv->batch) return fail(HS_E_INVALID, "hs_kv_admit: slot %d out of range", slot);
+  if (kv->cap[slot] != 0) return fail(HS_E_STATE, "hs_kv_admit: slot %d is in use", slot);
+  if (n_v < 0 || capacity <= 0 || n_v > capacity || capacity > kv->m->max_ctx)
+    return fail(HS_E_INVALID, "hs_kv_admit: n_v %d, capacity %d (max_ctx %d)", n_v, capacity, kv->m->max_ctx);
+  HIP_TRY(launch_set_int(kv->d_cap + slot, capacity, (hipStream_t)stream));
+  kv->n_v[slot] = n_v;
+  kv->cap[slot] = capacity;
+  kv->max_cap = std::max(kv->max_cap, capacity);
+  return HS_OK;
+}
+
+int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream) {
+  if (!kv || !kv->pool) return fail(HS_E_INVALID, "hs_kv_release: not a pooled cache");
+  if (slot < 0 || slot >= kv->batch) return fail(HS_E_INVALID, "hs_kv_release: slot %d out of range", slot);
+  if (kv->cap[slot] == 0) return fail(HS_E_STATE, "hs_kv_release: slot %d is empty", slot);
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(launch_kv_release(kv_pool(kv), slot, st));
+  HIP_TRY(launch_set_int(kv->d_cap + slot, 0, st));
+  const bool was_ready = kv->ready[slot];
+  kv->free_blocks += kv->nblk[slot];
+  kv->nblk[slot] = 0;
+  kv->n_v[slot] = kv->cap[slot] = kv->len[slot] = kv->rope[slot] = 0;
+  kv->ready[slot] = 0;
+  if (was_ready) HIP_TRY(rebuild_active(kv, st));
+  return HS_OK;
+}
+
+int hs_kv_pool_blocks(const hs_kv *kv, int32_t *free_blocks, int32_t *n_blocks) {
+  if (!kv || !kv->pool) return fail(HS_E_INVALID, "hs_kv_pool_blocks: not a pooled cache");
+  if (free_blocks) *free_blocks = kv->free_blocks;
+  if (n_blocks) *n_blocks = kv->n_blocks;
   return HS_OK;
 }
 
@@ -654,7 +850,6 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
   if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_decode_step: model/handle mismatch");
   if (!tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_in is NULL");
   const hs_config &c = m->cfg;
-  const int B = kv->batch;
   if (m->w.lm_head) {
     if (!tokens_out) return fail(HS_E_INVALID, "hs_decode_step: tokens_out is NULL");
     if (tokens_out == tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_out aliases tokens_in");
@@ -663,9 +858,14 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
   }
   hipStream_t st = (hipStream_t)stream;
   Step step;
-  int rc = decode_step_args(m, kv, st, &step);
+  int need = 0;
+  int rc = decode_step_args(m, kv, st, &step, &need);
   if (rc) return rc;
-  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, B, m->x, m->status, st));
+  const int B = kv->n_active;
+  // a pooled request entering a new block takes it now, on the device
+  if (kv->pool) HIP_TRY(launch_kv_reserve(kv_pool(kv), KvReserve{}, B, st));
+  const int *act = kv->pool ? kv->d_act : nullptr;  // a contiguous cache decodes request c in column c
+  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, act, B, m->x, m->status, st));
   rc = step.layers();
   if (rc) return rc;
   if (hidden_out)
@@ -673,11 +873,18 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
   if (m->w.lm_head) {
     float *lg = logits ? logits : m->logits;
     HIP_TRY(step.head(m->x, lg));
-    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, kv->d_len, kv->d_rope, 1, st));
+    HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, act, kv->d_len, kv->d_rope, 1, st));
   } else {
-    HIP_TRY(launch_advance(kv->d_len, kv->d_rope, B, st));
+    HIP_TRY(launch_advance(kv->d_len, kv->d_rope, act, B, st));
   }
-  for (int b = 0; b < B; ++b) kv->len[b] += 1;
+  for (int b : kv->act_host) {
+    if (kv->pool) {
+      const int k = blocks_for(kv, kv->len[b] + 1) - kv->nblk[b];
+      kv->nblk[b] += k;
+      kv->free_blocks -= k;
+    }
+    kv->len[b] += 1;
+  }
   return HS_OK;
 }
 
@@ -722,11 +929,18 @@ int hs_kv_sync(hs_kv *kv) {
   HIP_TRY(hipDeviceSynchronize());
   HIP_TRY(hipMemcpy(kv->len.data(), kv->d_len, kv->batch * 4, hipMemcpyDeviceToHost));
   HIP_TRY(hipMemcpy(kv->rope.data(), kv->d_rope, kv->batch * 4, hipMemcpyDeviceToHost));
+  if (kv->pool) {
+    HIP_TRY(hipMemcpy(kv->nblk.data(), kv->d_nblk, kv->batch * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&kv->free_blocks, kv->d_top, 4, hipMemcpyDeviceToHost));
+  }
   return HS_OK;
 }
 
-static int kv_slab(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0,
-                   int32_t n, const void *p, int64_t *off_bytes, size_t *bytes) {
+// The byte ranges of the cache buffer that hold rows pos0 .. pos0 + n - 1 of
+// (req, layer, K|V, head), one per block they touch (host-side layout; a pooled
+// cache's block starts are read from the device).
+static int kv_slabs(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0,
+                    int32_t n, const void *p, std::vector<std::pair<int64_t, size_t>> *out) {
   if (!kv || !p) return fail(HS_E_INVALID, "kv copy: NULL argument");
   const hs_config &c = kv->m->cfg;
   if (req < 0 || req >= kv->batch || layer < 0 || layer >= c.n_layers || kv_sel < 0 || kv_sel > 1 || head < 0 ||
@@ -734,36 +948,56 @@ static int kv_slab(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, 
     return fail(HS_E_INVALID, "kv copy: (req %d, layer %d, kv %d, head %d, pos %d + %d) outside the cache", req, layer,
                 kv_sel, head, pos0, n);
   const int b = dtype_bytes(c.dtype);
-  const int64_t elem =
-      kv->base[req] + ((int64_t)((layer * 2 + kv_sel) * c.n_kv_heads + head) * kv->cap[req] + pos0) * c.head_dim;
-  *off_bytes = elem * b;
-  *bytes = (size_t)n * c.head_dim * b;
+  const int bt = kv->pool ? kv->block_tokens : kv->cap[req];
+  std::vector<int64_t> starts;
+  if (kv->pool) {
+    starts.resize(kv->max_blocks);
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(hipMemcpy(starts.data(), kv->d_base + (int64_t)req * kv->max_blocks, kv->max_blocks * 8,
+                      hipMemcpyDeviceToHost));
+  } else {
+    starts.assign(1, kv->base[req]);
+  }
+  out->clear();
+  for (int p0 = pos0; p0 < pos0 + n;) {
+    const int blk = p0 / bt, in_blk = std::min(pos0 + n, (blk + 1) * bt) - p0;
+    if (starts[blk] < 0) return fail(HS_E_INVALID, "kv copy: position %d of request %d has no block", p0, req);
+    const int64_t elem =
+        starts[blk] + ((int64_t)((layer * 2 + kv_sel) * c.n_kv_heads + head) * bt + p0 - blk * bt) * c.head_dim;
+    out->push_back({elem * b, (size_t)in_blk * c.head_dim * b});
+    p0 += in_blk;
+  }
   return HS_OK;
 }
 
 int hs_kv_write(hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
                 const void *src, int32_t src_is_device) {
-  int64_t off;
-  size_t bytes;
-  int rc = kv_slab(kv, req, layer, kv_sel, head, pos0, n, src, &off, &bytes);
+  std::vector<std::pair<int64_t, size_t>> slabs;
+  int rc = kv_slabs(kv, req, layer, kv_sel, head, pos0, n, src, &slabs);
   if (rc) return rc;
-  if (!bytes) return HS_OK;
   HIP_TRY(hipDeviceSynchronize());
-  HIP_TRY(hipMemcpy((char *)kv->buf + off, src, bytes, src_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice));
+  size_t done = 0;
+  for (auto &sl : slabs) {
+    HIP_TRY(hipMemcpy((char *)kv->buf + sl.first, (const char *)src + done, sl.second,
+                      src_is_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice));
+    done += sl.second;
+  }
   HIP_TRY(hipDeviceSynchronize());
   return HS_OK;
 }
 
 int hs_kv_read(const hs_kv *kv, int32_t req, int32_t layer, int32_t kv_sel, int32_t head, int32_t pos0, int32_t n,
                void *dst, int32_t dst_is_device) {
-  int64_t off;
-  size_t bytes;
-  int rc = kv_slab(kv, req, layer, kv_sel, head, pos0, n, dst, &off, &bytes);
+  std::vector<std::pair<int64_t, size_t>> slabs;
+  int rc = kv_slabs(kv, req, layer, kv_sel, head, pos0, n, dst, &slabs);
   if (rc) return rc;
-  if (!bytes) return HS_OK;
   HIP_TRY(hipDeviceSynchronize());
-  HIP_TRY(hipMemcpy(dst, (const char *)kv->buf + off, bytes,
-                    dst_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost));
+  size_t done = 0;
+  for (auto &sl : slabs) {
+    HIP_TRY(hipMemcpy((char *)dst + done, (const char *)kv->buf + sl.first, sl.second,
+                      dst_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost));
+    done += sl.second;
+  }
   return HS_OK;
 }
 
@@ -771,12 +1005,32 @@ int hs_kv_set_length(hs_kv *kv, int32_t req, int32_t len, int32_t rope_pos) {
   if (!kv) return fail(HS_E_INVALID, "hs_kv_set_length: NULL");
   if (req < 0 || req >= kv->batch || len < 0 || len > kv->cap[req] || rope_pos < 0)
     return fail(HS_E_INVALID, "hs_kv_set_length: bad request/length");
+  if (kv->pool) {  // blocks to cover the new length
+    const int need = blocks_for(kv, len) - kv->nblk[req];
+    if (need > kv->free_blocks)
+      return fail(HS_E_CAPACITY, "hs_kv_set_length: the pool has %d free blocks, %d needed", kv->free_blocks, need);
+    if (need > 0) {
+      KvReserve r{};
+      r.n = 1;
+      r.req[0] = req;
+      r.target[0] = len;
+      HIP_TRY(launch_kv_reserve(kv_pool(kv), r, 0, nullptr));
+      kv->nblk[req] += need;
+      kv->free_blocks -= need;
+    }
+  }
+  const int ready = len > 0;
   HIP_TRY(hipDeviceSynchronize());
   HIP_TRY(hipMemcpy(kv->d_len + req, &len, 4, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(kv->d_rope + req, &rope_pos, 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(kv->d_ready + req, &ready, 4, hipMemcpyHostToDevice));
   kv->len[req] = len;
   kv->rope[req] = rope_pos;
-  kv->ready[req] = len > 0;
+  kv->ready[req] = ready;
+  if (kv->pool) {
+    HIP_TRY(rebuild_active(kv, nullptr));
+    HIP_TRY(hipDeviceSynchronize());
+  }
   return HS_OK;
 }
 

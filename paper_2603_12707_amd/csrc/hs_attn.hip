@@ -33,7 +33,7 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
 // writing the neutral (o = 0, m = -inf, l = 0).
 // K/V are read through buffer ranges that end at the split's last position,
 // so that no load sits behind a branch.
-template <int DT, int HD, int G, int NW>
+template <int DT, int HD, int G, int NW, bool PAGED>
 __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   using S = typename Ty<DT>::S;
   constexpr int CE = Ty<DT>::CE;
@@ -45,14 +45,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
   int req, L;
   if (!a.prefill) {
-    req = qi;
-    L = a.kv_len[qi] + 1;
+    req = PAGED ? a.kv.act[qi] : qi;
+    L = a.kv.len[req] + 1;
   } else {
     const int i = packed_request(a.pk, qi);
-    req = a.pk.req[i];
-    L = qi - a.pk.cu[i] + 1;
+    req = a.pk->req[i];
+    L = qi - a.pk->cu[i] + 1;
   }
-  const int cap = a.kv_cap[req];
+  const int cap = a.kv.cap[req];
   L = min(L, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;  // first (query, head) row of this group
@@ -72,9 +72,19 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tg = lane / LPT, c = lane % LPT;
-  const S *kbase = (const S *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
-  const S *vbase = (const S *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap + t0) * HD;
-  const rsrc_t kr = make_rsrc(kbase, (uint32_t)n * HD * SB), vr = make_rsrc(vbase, (uint32_t)n * HD * SB);
+  // the split lies in one block of the request
+  int64_t ko, vo;
+  if constexpr (PAGED) {
+    ko = kv_rows(a.kv, req, a.layer, 0, a.n_kv, j, t0, HD);
+    vo = kv_rows(a.kv, req, a.layer, 1, a.n_kv, j, t0, HD);
+  } else {
+    const int64_t b = a.kv.tab[req];
+    ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+    vo = ko + (int64_t)a.n_kv * cap * HD;
+  }
+  const uint32_t nbytes = ko < 0 ? 0u : (uint32_t)n * HD * SB;
+  const rsrc_t kr = make_rsrc((const S *)a.kv.buf + max(ko, (int64_t)0), nbytes);
+  const rsrc_t vr = make_rsrc((const S *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
   float qf[G][CE];
 #pragma unroll
@@ -196,7 +206,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
 // chunk c = lane % 16 of the 4 positions it covers, and output row c of d-tile
 // dt is element d = 8 c + dt, which a lane gathers from its four chunks.
 // The waves merge through LDS as in k_attn.
-template <int DT, int HD, int G, int NW>
+template <int DT, int HD, int G, int NW, bool PAGED>
 __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   static_assert(DT != HS_F32 && G <= 16 && (HD == 64 || HD == 128), "16-bit storage, at most 16 heads per group");
   constexpr int SB = 2;
@@ -207,14 +217,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
   int req, L;
   if (!a.prefill) {
-    req = qi;
-    L = a.kv_len[qi] + 1;
+    req = PAGED ? a.kv.act[qi] : qi;
+    L = a.kv.len[req] + 1;
   } else {
     const int i = packed_request(a.pk, qi);
-    req = a.pk.req[i];
-    L = qi - a.pk.cu[i] + 1;
+    req = a.pk->req[i];
+    L = qi - a.pk->cu[i] + 1;
   }
-  const int cap = a.kv_cap[req];
+  const int cap = a.kv.cap[req];
   L = min(L, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;
@@ -234,11 +244,19 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lg = lane >> 4;
-  const uint16_t *kbase =
-      (const uint16_t *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
-  const uint16_t *vbase =
-      (const uint16_t *)a.kv + a.kv_base[req] + ((int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap + t0) * HD;
-  const rsrc_t kr = make_rsrc(kbase, (uint32_t)n * HD * SB), vr = make_rsrc(vbase, (uint32_t)n * HD * SB);
+  // the split lies in one block of the request
+  int64_t ko, vo;
+  if constexpr (PAGED) {
+    ko = kv_rows(a.kv, req, a.layer, 0, a.n_kv, j, t0, HD);
+    vo = kv_rows(a.kv, req, a.layer, 1, a.n_kv, j, t0, HD);
+  } else {
+    const int64_t b = a.kv.tab[req];
+    ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+    vo = ko + (int64_t)a.n_kv * cap * HD;
+  }
+  const uint32_t nbytes = ko < 0 ? 0u : (uint32_t)n * HD * SB;
+  const rsrc_t kr = make_rsrc((const uint16_t *)a.kv.buf + max(ko, (int64_t)0), nbytes);
+  const rsrc_t vr = make_rsrc((const uint16_t *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
   // Q^T operand: head lane % 16 of the group (zero past G), k = 32 kk + 8 q ..
   u32x4 qb[KK];
@@ -376,21 +394,21 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   const int j = blockIdx.y;
   // the wave's query tile: tile t - tcu[i] of packed request i
   const int t = (int)blockIdx.x * NW + wave;
-  if (t >= a.pk.tcu[a.pk.n]) return;  // whole wave; no barrier below
+  if (t >= a.prefill_tiles) return;  // whole wave; no barrier below
+  const PackedRows *pk = a.pk;
   int pi = 0;
-  for (int k = 1; k < a.pk.n; ++k) pi += t >= a.pk.tcu[k];
-  const int roff = a.pk.cu[pi], nrows = a.pk.cu[pi + 1] - roff;
-  const int q0 = (t - a.pk.tcu[pi]) * QPT;
-  const int req = a.pk.req[pi], cap = a.kv_cap[req];
+  for (int k = 1; k < pk->n; ++k) pi += t >= pk->tcu[k];
+  const int roff = pk->cu[pi], nrows = pk->cu[pi + 1] - roff;
+  const int q0 = (t - pk->tcu[pi]) * QPT;
+  const int req = pk->req[pi];
   const int sq = q0 + li / G, sh = li % G;  // the lane column's query position and head
   const bool slot = li < QPT * G && sq < nrows;
   const int qlast = min(q0 + QPT - 1, nrows - 1);
   const int n_kt = qlast / 16 + 1;  // key tiles
-  const uint16_t *kbase = (const uint16_t *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2) * a.n_kv + j) * cap * HD;
-  const uint16_t *vbase =
-      (const uint16_t *)a.kv + a.kv_base[req] + (int64_t)((a.layer * 2 + 1) * a.n_kv + j) * cap * HD;
-  const uint32_t nbytes = (uint32_t)(qlast + 1) * HD * SB;
-  const rsrc_t kr = make_rsrc(kbase, nbytes), vr = make_rsrc(vbase, nbytes);
+  // key tiles are read block by block (a block holds a whole number of tiles)
+  const int bt = a.kv.bt[req], toff = a.kv.toff[req];
+  const int64_t kin = (int64_t)((a.layer * 2) * a.n_kv + j) * bt * HD, vin = kin + (int64_t)a.n_kv * bt * HD;
+  const uint16_t *buf = (const uint16_t *)a.kv.buf;
 
   u32x4 qb[KK];
 #pragma unroll
@@ -407,13 +425,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
     u32x4 kc[UB][KK], vc[UB][4];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int p0 = (kt0 + u) * 16;
+      const int p0 = (kt0 + u) * 16, blk = p0 / bt, pb = p0 - blk * bt;
+      const int64_t b0 = p0 <= qlast ? a.kv.tab[toff + blk] : -1;
+      // rows of the block up to the tile's last query position; past them, zeros
+      const uint32_t nbytes = b0 < 0 ? 0u : (uint32_t)min(bt, qlast + 1 - blk * bt) * HD * SB;
+      const rsrc_t kr = make_rsrc(buf + max(b0, (int64_t)0) + kin, nbytes);
+      const rsrc_t vr = make_rsrc(buf + max(b0, (int64_t)0) + vin, nbytes);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        kc[u][kk] = bld16(kr, (uint32_t)((p0 + li) * HD + (kk * 4 + lg) * 8) * SB);
+        kc[u][kk] = bld16(kr, (uint32_t)((pb + li) * HD + (kk * 4 + lg) * 8) * SB);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        vc[u][i] = bld16(vr, li < CPR ? (uint32_t)((p0 + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
+        vc[u][i] = bld16(vr, li < CPR ? (uint32_t)((pb + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -522,23 +545,23 @@ __global__ __launch_bounds__(HD) void k_combine(AttnArgs a) {
   st_elem<DT>(a.out, ((int64_t)qi * a.n_heads + h) * HD + e, num / den);
 }
 
-template <int DT, int HD>
+template <int DT, int HD, bool PAGED>
 hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
   const dim3 grid(a.n_split, a.n_kv, nq), block(64 * ATTN_WAVES);
   switch (group) {
-    case 1: HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES>), grid, block, 0, st, a); break;
-    case 2: HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES>), grid, block, 0, st, a); break;
+    case 1: HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES, PAGED>), grid, block, 0, st, a); break;
+    case 2: HS_LAUNCH((k_attn<DT, HD, 2, ATTN_WAVES, PAGED>), grid, block, 0, st, a); break;
     case 4:
-      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a);
-      else HS_LAUNCH((k_attn_mma<DT, HD, 4, ATTN_WAVES>), grid, block, 0, st, a);
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 4, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 4, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
       break;
     case 7:
-      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a);
-      else HS_LAUNCH((k_attn_mma<DT, HD, 7, ATTN_WAVES>), grid, block, 0, st, a);
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 7, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 7, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
       break;
     case 8:
-      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a);
-      else HS_LAUNCH((k_attn_mma<DT, HD, 8, ATTN_WAVES>), grid, block, 0, st, a);
+      if constexpr (DT == HS_F32) HS_LAUNCH((k_attn<DT, HD, 8, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
+      else HS_LAUNCH((k_attn_mma<DT, HD, 8, ATTN_WAVES, PAGED>), grid, block, 0, st, a);
       break;
     default: return hipErrorInvalidValue;
   }
@@ -547,8 +570,16 @@ hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
 
 template <int DT>
 hipError_t attn_dt(int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st) {
-  if (head_dim == 64) return attn_hd<DT, 64>(group, nq, a, st);
-  if (head_dim == 128) return attn_hd<DT, 128>(group, nq, a, st);
+  // pooled caches hold 16-bit storage only
+  if constexpr (DT != HS_F32) {
+    if (a.kv.paged) {
+      if (head_dim == 64) return attn_hd<DT, 64, true>(group, nq, a, st);
+      if (head_dim == 128) return attn_hd<DT, 128, true>(group, nq, a, st);
+      return hipErrorInvalidValue;
+    }
+  }
+  if (head_dim == 64) return attn_hd<DT, 64, false>(group, nq, a, st);
+  if (head_dim == 128) return attn_hd<DT, 128, false>(group, nq, a, st);
   return hipErrorInvalidValue;
 }
 
@@ -569,13 +600,9 @@ hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
 }
 
 template <int DT, int HD>
-hipError_t prefill_hd(int group, const AttnArgs &args, hipStream_t st) {
+hipError_t prefill_hd(int group, const AttnArgs &a, hipStream_t st) {
   constexpr int NW = 4;
-  const int qpt = 16 / group;
-  AttnArgs a = args;
-  a.pk.tcu[0] = 0;
-  for (int i = 0; i < a.pk.n; ++i) a.pk.tcu[i + 1] = a.pk.tcu[i] + (a.pk.cu[i + 1] - a.pk.cu[i] + qpt - 1) / qpt;
-  const dim3 grid((a.pk.tcu[a.pk.n] + NW - 1) / NW, a.n_kv), block(64 * NW);
+  const dim3 grid((a.prefill_tiles + NW - 1) / NW, a.n_kv), block(64 * NW);
   switch (group) {
     case 1: HS_LAUNCH((k_attn_prefill<DT, HD, 1, NW>), grid, block, 0, st, a); break;
     case 2: HS_LAUNCH((k_attn_prefill<DT, HD, 2, NW>), grid, block, 0, st, a); break;
@@ -591,9 +618,11 @@ hipError_t prefill_hd(int group, const AttnArgs &args, hipStream_t st) {
 
 bool attn_prefill_on_mma(int dtype) { return dtype != HS_F32; }
 
+int attn_prefill_rows_per_tile(int group) { return 16 / group; }
+
 hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
                                     hipStream_t st) {
-  if (nrows <= 0 || a.pk.n <= 0) return hipSuccess;
+  if (nrows <= 0 || a.prefill_tiles <= 0) return hipSuccess;
   if (dtype == HS_F16) return head_dim == 64 ? prefill_hd<HS_F16, 64>(group, a, st)
                                              : prefill_hd<HS_F16, 128>(group, a, st);
   if (dtype == HS_BF16) return head_dim == 64 ? prefill_hd<HS_BF16, 64>(group, a, st)

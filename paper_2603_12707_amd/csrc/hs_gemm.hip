@@ -57,7 +57,7 @@ __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_
 // the up projection; the other epilogues take R consecutive tiles.
 template <int EPI, int R>
 __device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int *row0) {
-  if constexpr (EPI == EPI_QKV) {
+  if constexpr (epi_qkv(EPI)) {
     const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -129,32 +129,51 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
 // Every read goes through a buffer range, so none sits behind a branch.
 template <int R>
 struct QkvIn {
-  int pos, cap;
-  int64_t base;
+  int pos, cap, bt;
+  int64_t base;  // start of the block holding pos (negative: none)
   int p[R][2];
   float cs[R][2], sn[R][2], b1[R][2], b2[R][2];
 };
 
-template <int DT, int R>
+template <int DT, int R, bool PAGED>
 __device__ __forceinline__ void qkv_fetch_ids(const GemmArgs &a, const int *mat, const int *row0, int col, int rr,
                                               bool ok, QkvIn<R> &in) {
   const bool dec = !a.prefill;
-  // prefill: the packed row's request and its position in that request
-  int req = col, ppos = 0;
+  const KvRef &kv = a.kv;
+  // decode: column col is request act[col]; prefill: the packed row's request
+  // and its position in that request
+  int req = 0, ppos = 0;
   if (!dec) {
     const int i = packed_request(a.pk, col);
-    req = a.pk.req[i];
-    ppos = col - a.pk.cu[i];
+    req = a.pk->req[i];
+    ppos = col - a.pk->cu[i];
   }
-  const rsrc_t lr = make_rsrc(a.kv_len, dec ? (uint32_t)a.ncols * 4u : 0u);
-  const rsrc_t cr = make_rsrc(a.kv_cap, (uint32_t)a.kv_nreq * 4u);
-  const rsrc_t br = make_rsrc(a.kv_base, (uint32_t)a.kv_nreq * 8u);
-  const rsrc_t pr = make_rsrc(a.rope_pos, dec ? (uint32_t)a.ncols * 4u : (a.rope_m3 ? 3u * a.rope_ld * 4u : 0u));
-  const uint32_t pl = bld4(lr, ok && dec ? (uint32_t)col * 4u : BUF_OOB);
-  in.cap = (int)bld4(cr, ok ? (uint32_t)req * 4u : BUF_OOB);
-  const u32x2 bb = bld8(br, ok ? (uint32_t)req * 8u : BUF_OOB);
-  in.base = (int64_t)(((uint64_t)bb[1] << 32) | bb[0]);
-  in.pos = dec ? (int)pl : ppos;
+  const uint32_t nb = (uint32_t)kv.nreq * 4u;
+  if constexpr (PAGED) {
+    const rsrc_t ar = make_rsrc(kv.act, dec ? (uint32_t)a.ncols * 4u : 0u);
+    if (dec) req = (int)bld4(ar, ok ? (uint32_t)col * 4u : BUF_OOB);
+  } else if (dec) {
+    req = col;
+  }
+  const rsrc_t lr = make_rsrc(kv.len, dec ? nb : 0u), cr = make_rsrc(kv.cap, nb);
+  const rsrc_t br = make_rsrc(kv.tab, (uint32_t)kv.ntab * 8u);
+  const rsrc_t pr = make_rsrc(a.rope_pos, dec ? nb : (a.rope_m3 ? 3u * a.rope_ld * 4u : 0u));
+  const uint32_t ro = ok ? (uint32_t)req * 4u : BUF_OOB;
+  const uint32_t pl = bld4(lr, dec ? ro : BUF_OOB);
+  in.cap = (int)bld4(cr, ro);
+  if constexpr (PAGED) {  // the block holding the position
+    const rsrc_t or_ = make_rsrc(kv.toff, nb), tr = make_rsrc(kv.bt, nb);
+    const int toff = (int)bld4(or_, ro);
+    in.bt = max(1, (int)bld4(tr, ro));
+    in.pos = dec ? (int)pl : ppos;
+    const u32x2 bb = bld8(br, ok && in.pos < in.cap ? (uint32_t)(toff + in.pos / in.bt) * 8u : BUF_OOB);
+    in.base = ok && in.pos < in.cap ? (int64_t)(((uint64_t)bb[1] << 32) | bb[0]) : -1;
+  } else {  // one block per request: its start, read beside the length
+    const u32x2 bb = bld8(br, ok ? (uint32_t)req * 8u : BUF_OOB);
+    in.bt = in.cap;
+    in.pos = dec ? (int)pl : ppos;
+    in.base = ok && in.pos < in.cap ? (int64_t)(((uint64_t)bb[1] << 32) | bb[0]) : -1;
+  }
   const int hd = a.head_dim;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -163,7 +182,7 @@ __device__ __forceinline__ void qkv_fetch_ids(const GemmArgs &a, const int *mat,
     for (int e = 0; e < 2; ++e) {
       const int i = j0 + e, sec = i < a.sec0 ? 0 : (i < a.sec1 ? 1 : 2);
       const bool rot = ok && mat[r] < 2 && (dec || a.rope_m3);
-      const uint32_t pv = bld4(pr, rot ? (uint32_t)(dec ? col : sec * a.rope_ld + col) * 4u : BUF_OOB);
+      const uint32_t pv = bld4(pr, rot ? (uint32_t)(dec ? req : sec * a.rope_ld + col) * 4u : BUF_OOB);
       in.p[r][e] = (dec || a.rope_m3) ? (int)pv : in.pos;
     }
   }
@@ -209,7 +228,7 @@ __device__ __forceinline__ void qkv_fetch_tab(const GemmArgs &a, const int *mat,
 
 // bias, RoPE on q and k, then R(q) to the q workspace and k, v rows appended
 // to the cache at the request's position
-template <int DT, int R>
+template <int DT, int R, bool PAGED>
 __device__ __forceinline__ void qkv_store(const GemmArgs &a, const int *mat, const int *row0, const f32x4 *v, int col,
                                           int rr, const QkvIn<R> &in) {
   constexpr int B = DT == HS_F32 ? 4 : 2;
@@ -232,11 +251,11 @@ __device__ __forceinline__ void qkv_store(const GemmArgs &a, const int *mat, con
         void *q = (char *)a.out + ((int64_t)col * a.ld_out + head * hd) * B;
         st_elem<DT>(q, i, o1);
         st_elem<DT>(q, i + half, o2);
-      } else if (in.pos < in.cap) {
-        const int64_t off =
-            in.base + ((int64_t)((a.layer * 2 + (m == 2 ? 1 : 0)) * a.n_kv + head) * in.cap + in.pos) * hd;
-        st_elem<DT>(a.kv, off + i, o1);
-        st_elem<DT>(a.kv, off + i + half, o2);
+      } else if (in.base >= 0) {
+        const int pin = PAGED ? in.pos % in.bt : in.pos;  // position within its block
+        const int64_t off = in.base + ((int64_t)((a.layer * 2 + (m == 2 ? 1 : 0)) * a.n_kv + head) * in.bt + pin) * hd;
+        st_elem<DT>(a.kv.buf, off + i, o1);
+        st_elem<DT>(a.kv.buf, off + i + half, o2);
       }
     }
   }
@@ -537,12 +556,12 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   }
 
   // q/k/v epilogue: ids now, table entries and biases after the prologue
-  static_assert(EPI != EPI_QKV || NT * 64 <= 64 * NW, "one epilogue item per thread");
+  static_assert(!epi_qkv(EPI) || NT * 64 <= 64 * NW, "one epilogue item per thread");
   QkvIn<R> qin;
   const int ep_col = col0 + 16 * ((int)threadIdx.x >> 6) + ((int)threadIdx.x & 15);
   const int ep_rr = 4 * (((int)threadIdx.x & 63) >> 4);
   const bool ep_ok = (int)threadIdx.x < NT * 64 && ep_col < a.ncols;
-  if constexpr (EPI == EPI_QKV) qkv_fetch_ids<DT, R>(a, mat, row0, ep_col, ep_rr, ep_ok, qin);
+  if constexpr (epi_qkv(EPI)) qkv_fetch_ids<DT, R, EPI == EPI_QKV_PAGED>(a, mat, row0, ep_col, ep_rr, ep_ok, qin);
 
   u32x4 w[D][U][R][4];
 #pragma unroll
@@ -607,7 +626,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   }
 
 
-  if constexpr (EPI == EPI_QKV) qkv_fetch_tab<DT, R>(a, mat, row0, ep_rr, ep_ok, qin);
+  if constexpr (epi_qkv(EPI)) qkv_fetch_tab<DT, R>(a, mat, row0, ep_rr, ep_ok, qin);
 
   // The MFMAs of one k-group accumulate in fp32 from zero; with ACC64 each
   // group's tile is then added into fp64 accumulators, so that fp32 rounding
@@ -705,8 +724,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         for (int e = 0; e < 4; ++e)
           if (row + e < a.rows[0]) x[row + e] = xres[e] + v[0][e];
       }
-    } else if constexpr (EPI == EPI_QKV) {
-      if (col < a.ncols) qkv_store<DT, R>(a, mat, row0, v, col, 4 * (ln >> 4), qin);
+    } else if constexpr (epi_qkv(EPI)) {
+      if (col < a.ncols) qkv_store<DT, R, EPI == EPI_QKV_PAGED>(a, mat, row0, v, col, 4 * (ln >> 4), qin);
     } else {
       if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
     }
@@ -750,7 +769,7 @@ __global__ __launch_bounds__(64 * WR * WC) void k_gemm_tile(GemmArgs a) {
       constexpr int H = RTW / 2;
       mat[r] = r < H ? 0 : 1;
       row0[r] = 16 * ((rg * WR + wr) * H + (r % H));
-    } else if constexpr (EPI == EPI_QKV) {
+    } else if constexpr (epi_qkv(EPI)) {
       const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
       int m = 0, t = (rg * WR + wr) * RTW + r;
       if (t >= tq) {
@@ -819,13 +838,13 @@ __global__ __launch_bounds__(64 * WR * WC) void k_gemm_tile(GemmArgs a) {
         const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
         gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
       }
-    } else if constexpr (EPI == EPI_QKV) {
+    } else if constexpr (epi_qkv(EPI)) {
 #pragma unroll
       for (int r = 0; r < RTW; ++r) {
         QkvIn<1> in;
-        qkv_fetch_ids<DT, 1>(a, &mat[r], &row0[r], col, rr, true, in);
+        qkv_fetch_ids<DT, 1, EPI == EPI_QKV_PAGED>(a, &mat[r], &row0[r], col, rr, true, in);
         qkv_fetch_tab<DT, 1>(a, &mat[r], &row0[r], rr, true, in);
-        qkv_store<DT, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
+        qkv_store<DT, 1, EPI == EPI_QKV_PAGED>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
       }
     } else {
 #pragma unroll
@@ -883,7 +902,7 @@ __global__ __launch_bounds__(64 * LG_NW) void k_gemm_lds(GemmArgs a) {
       const int w = t / RTW, k = t % RTW;
       m = k < H ? 0 : 1;
       r0 = 16 * (rg * (RTG / 2) + w * H + k % H);
-    } else if constexpr (EPI == EPI_QKV) {
+    } else if constexpr (epi_qkv(EPI)) {
       const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
       int mm = 0, u = rg * RTG + t;
       if (u >= tq) {
@@ -996,13 +1015,13 @@ __global__ __launch_bounds__(64 * LG_NW) void k_gemm_lds(GemmArgs a) {
         const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
         gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
       }
-    } else if constexpr (EPI == EPI_QKV) {
+    } else if constexpr (epi_qkv(EPI)) {
 #pragma unroll
       for (int r = 0; r < RTW; ++r) {
         QkvIn<1> in;
-        qkv_fetch_ids<DT, 1>(a, &mat[r], &row0[r], col, rr, true, in);
+        qkv_fetch_ids<DT, 1, EPI == EPI_QKV_PAGED>(a, &mat[r], &row0[r], col, rr, true, in);
         qkv_fetch_tab<DT, 1>(a, &mat[r], &row0[r], rr, true, in);
-        qkv_store<DT, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
+        qkv_store<DT, 1, EPI == EPI_QKV_PAGED>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
       }
     } else if (EPI == EPI_RESID && nks > 1) {
       // K split: this split's fp32 partial, summed into the residual later
@@ -1147,7 +1166,7 @@ hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
 template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   // row tiles of 16 (SwiGLU: of one of its two matrices)
-  const int tiles16 = EPI == EPI_QKV ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 16 : (a.rows[0] + 15) / 16;
+  const int tiles16 = epi_qkv(EPI) ? (a.n_heads + 2 * a.n_kv) * a.head_dim / 16 : (a.rows[0] + 15) / 16;
   const int tiles = (a.ncols + 15) / 16;
   const int b = DT == HS_F32 ? 4 : 2;
   const size_t xs = (size_t)a.ncols * a.K * b;
@@ -1182,6 +1201,8 @@ template <int DT>
 hipError_t gemm_dt(int pro, int epi, const GemmArgs &a, hipStream_t st) {
   if (pro == PRO_COMBINE && epi == EPI_RESID) return gemm_combine<DT>(a, st);
   if (pro == PRO_NORM && epi == EPI_QKV) return gemm_shape<DT, PRO_NORM, EPI_QKV>(a, st);
+  if constexpr (DT != HS_F32)  // pooled caches hold 16-bit storage only
+    if (pro == PRO_NORM && epi == EPI_QKV_PAGED) return gemm_shape<DT, PRO_NORM, EPI_QKV_PAGED>(a, st);
   if (pro == PRO_NORM && epi == EPI_SWIGLU) return gemm_shape<DT, PRO_NORM, EPI_SWIGLU>(a, st);
   if (pro == PRO_NORM && epi == EPI_STORE) return gemm_shape<DT, PRO_NORM, EPI_STORE>(a, st);
   if (pro == PRO_PLAIN && epi == EPI_RESID) return gemm_shape<DT, PRO_PLAIN, EPI_RESID>(a, st);

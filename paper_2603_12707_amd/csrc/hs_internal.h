@@ -28,6 +28,22 @@ struct PackedRows {
   int tcu[PACK_MAX + 1];
 };
 
+// Where the cache rows of request (slot) r live.  Its positions are cut into
+// blocks of bt[r] positions; block k starts at element tab[toff[r] + k] of the
+// cache buffer (negative: not allocated) and holds, for every (layer l, K|V s,
+// KV head j), bt[r] consecutive rows of head_dim elements:
+//   element(l, s, j, p, e) = tab[toff[r] + p / bt[r]]
+//                            + (((l * 2 + s) * n_kv + j) * bt[r] + p % bt[r]) * head_dim + e.
+// A contiguous cache is one block per request (bt = capacity).  In a decode
+// step, column c is request act[c].
+struct KvRef {
+  void *buf;
+  const int64_t *tab;
+  const int *toff, *bt, *cap, *len, *act;
+  int nreq, ntab;  // entries of toff / bt / cap / len, and of tab
+  int paged;       // 0: one block per request (toff[r] = r, bt = cap, act[c] = c)
+};
+
 struct GemmArgs {
   const void *w[3];
   const void *bias[3];
@@ -56,15 +72,11 @@ struct GemmArgs {
   int k_split;  // set by the launcher
   // q/k/v epilogue: RoPE and KV append
   int head_dim, n_heads, n_kv;
-  void *kv;
-  const int64_t *kv_base;
-  const int *kv_cap;
-  const int *kv_len;
+  KvRef kv;
   int layer;
-  int prefill;         // 0: decode (column = request, position = len); 1: prefill rows described by pk
-  PackedRows pk;
-  int kv_nreq;         // entries of kv_base / kv_cap
-  const int *rope_pos; // decode: [ncols]; prefill M-RoPE: [3][rope_ld] (section-major); prefill 1-D: NULL
+  int prefill;           // 0: decode (column = request, position = len); 1: prefill rows described by *pk
+  const PackedRows *pk;  // device copy of the pass's rows (prefill)
+  const int *rope_pos; // decode: [requests]; prefill M-RoPE: [3][rope_ld] (section-major); prefill 1-D: NULL
   int rope_ld;
   int rope_m3;
   int sec0, sec1;      // M-RoPE section boundaries (pairs)
@@ -92,20 +104,20 @@ constexpr int attn_batch(int group) { return group <= 2 ? 8 : 4; }
 constexpr bool attn_uses_mma(int dtype, int group) { return dtype != HS_F32 && group >= 4; }
 constexpr int ATTN_MMA_BATCH = 2;
 constexpr int ATTN_MAX_SPLITS = 256;
-enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+// EPI_QKV_PAGED: the q/k/v epilogue for a cache of several blocks per request
+enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_QKV_PAGED = 4 };
+constexpr bool epi_qkv(int e) { return e == EPI_QKV || e == EPI_QKV_PAGED; }
 
 struct AttnArgs {
   const void *q;
   int ld_q;
-  const void *kv;
-  const int64_t *kv_base;
-  const int *kv_cap;
-  const int *kv_len;
+  KvRef kv;
   int layer;
   int n_heads, n_kv;
-  int prefill;     // 0: decode (query = request, length = len + 1); 1: prefill rows described by pk
-  PackedRows pk;   // prefill: query row r of request i has length r - cu[i] + 1
-  int S;           // positions per split
+  int prefill;     // 0: decode (query = column c, request act[c], length = len + 1); 1: prefill rows in *pk
+  const PackedRows *pk;  // device copy; query row r of request i has length r - cu[i] + 1
+  int prefill_tiles;     // prefill: query tiles in all (pk->tcu[pk->n])
+  int S;           // positions per split (a split never crosses a block of the request)
   int n_split;     // splits per (query, kv head)
   float *part_o;   // [nq][n_heads][n_split][head_dim]
   float *part_ml;  // [nq][n_heads][n_split][2]
@@ -121,20 +133,56 @@ hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, v
 int64_t packed_elems(int dtype, int64_t rows, int64_t cols);
 hipError_t launch_attention(int dtype, int head_dim, int group, int nq, const AttnArgs &a, hipStream_t st);
 hipError_t launch_combine(int dtype, int head_dim, int nq, const AttnArgs &a, hipStream_t st);
-// causal prefill attention over the packed rows of a.pk (nrows in all), 16-bit storage
+// causal prefill attention over the packed rows of *a.pk (nrows in all), 16-bit storage; query
+// tiles of 16 / group rows
+int attn_prefill_rows_per_tile(int group);
 bool attn_prefill_on_mma(int dtype);
 hipError_t launch_attention_prefill(int dtype, int head_dim, int group, int nrows, const AttnArgs &a,
                                     hipStream_t st);
-hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x,
-                        int *status, hipStream_t st);
+// x[c] = E[tokens[act[c]]] (act NULL: tokens[c])
+hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, const int *act, int n,
+                        float *x, int *status, hipStream_t st);
 hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *embed, int vocab, int d,
                                const int *ids, int s_text, float *x, int *status, hipStream_t st);
-hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
-                         int advance, hipStream_t st);
-hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st);
-// len[req] = s_ctx and the next RoPE position; pos_thw: [3][ld] section-major, this request's s_ctx columns
-hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, int ld,
+// row c's argmax to tokens_out[act[c]] (act NULL: [c]); with advance, that
+// request's length and RoPE position += 1
+hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, const int *act, int *len,
+                         int *rope_pos, int advance, hipStream_t st);
+hipError_t launch_advance(int *len, int *rope_pos, const int *act, int n, hipStream_t st);
+// len[req] = s_ctx, the next RoPE position, ready[req] = 1; pos_thw: [3][ld]
+// section-major, this request's s_ctx columns
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int *ready, int req, int s_ctx, const int *pos_thw, int ld,
                                  hipStream_t st);
+
+// Block pool of a KV handle: a stack of free block ids on the device, and per
+// request the count of blocks it holds (its table entries toff[r] ..).
+struct KvPool {
+  int64_t *tab;
+  const int *toff, *cap;
+  int *len, *rope, *ready, *nblk, *stack, *top, *status;
+  const int *act;
+  int bt;              // positions per block
+  int64_t block_elems; // elements per block
+};
+// requests and the lengths their blocks must cover
+struct KvReserve {
+  int n;
+  int req[PACK_MAX];
+  int target[PACK_MAX];
+};
+// Gives requests the blocks that cover positions [0, target): the listed ones
+// (decode_n == 0), or the decode step's columns act[0 .. decode_n) with target
+// len + 1 (capped at capacity).  A shortfall sets status bit 4 and leaves
+// those requests' entries unallocated.
+hipError_t launch_kv_reserve(const KvPool &p, const KvReserve &r, int decode_n, hipStream_t st);
+// returns request req's blocks to the stack and empties it (length 0, not ready)
+hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st);
+// *p = v, in stream order
+hipError_t launch_set_int(int *p, int v, hipStream_t st);
+// act = the ready requests in order (n requests)
+hipError_t launch_build_act(const int *ready, int n, int *act, hipStream_t st);
+// *dst = v, in stream order (the rows of a prefill pass, for the kernels that read them)
+hipError_t launch_set_packed(PackedRows *dst, const PackedRows &v, hipStream_t st);
 // out[i] = x[pk.cu[i + 1] - 1] for the pk.n requests (rows of d floats)
 hipError_t launch_gather_last(const float *x, int d, const PackedRows &pk, float *out, hipStream_t st);
 
@@ -159,6 +207,7 @@ struct hs_model {
   float *splitk = nullptr;  // [SPLITK_MAX][max_batch][d] residual GEMM partials
   int64_t splitk_floats = 0;
   float *xlast = nullptr;   // [PACK_MAX][d] last rows of the requests of a prefill pass
+  hs::PackedRows *pk_dev = nullptr;  // the rows of the current prefill pass
   float *logits = nullptr;  // [max_batch][V] (used when the caller passes no logits buffer)
   float *part_o = nullptr;
   float *part_ml = nullptr;
@@ -175,6 +224,16 @@ struct hs_kv {
   std::vector<int64_t> base;
   std::vector<char> ready;
   int max_cap = 0;
-  int64_t *d_base = nullptr;
+  int64_t *d_base = nullptr;  // block table (contiguous: one block start per request)
   int *d_cap = nullptr, *d_len = nullptr, *d_rope = nullptr;
+  int *d_toff = nullptr, *d_bt = nullptr, *d_act = nullptr, *d_ready = nullptr;
+  int ntab = 0;
+  int n_active = 0;  // decode columns
+  // block pool (handles from hs_kv_pool_create)
+  bool pool = false;
+  int block_tokens = 0, n_blocks = 0, max_blocks = 0, free_blocks = 0;
+  int64_t block_elems = 0;
+  int *d_stack = nullptr, *d_top = nullptr, *d_nblk = nullptr;
+  std::vector<int> nblk;     // blocks held per request (host mirror)
+  std::vector<int> act_host; // decode columns' requests (host mirror of d_act)
 };

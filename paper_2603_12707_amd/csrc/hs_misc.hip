@@ -38,9 +38,10 @@ __device__ __forceinline__ void copy_row(const void *__restrict__ src, float *__
 }
 
 template <int DT>
-__global__ __launch_bounds__(256) void k_embed(const void *E, int V, int d, const int *tok, float *x, int *status) {
+__global__ __launch_bounds__(256) void k_embed(const void *E, int V, int d, const int *tok, const int *act, float *x,
+                                               int *status) {
   const int b = blockIdx.x;
-  int t = tok[b];
+  int t = tok[act ? act[b] : b];
   if (t < 0 || t >= V) {
     if (threadIdx.x == 0) atomicOr(status, 1);
     t = 0;
@@ -73,8 +74,8 @@ __global__ __launch_bounds__(256) void k_prefill_rows(const void *emb, int n_v, 
 
 // Greedy selection: largest logit, lowest index among equals (NaN never wins).
 // Each thread scans indices i = tid + 1024 k in order, eight loads at a time.
-__global__ __launch_bounds__(1024) void k_argmax(const float *__restrict__ logits, int V, int ld, int *out, int *len,
-                                                 int *rope, int advance) {
+__global__ __launch_bounds__(1024) void k_argmax(const float *__restrict__ logits, int V, int ld, int *out,
+                                                 const int *act, int *len, int *rope, int advance) {
   const int b = blockIdx.x;
   const float *lg = logits + (int64_t)b * ld;
   float bv = -INFINITY;
@@ -116,24 +117,26 @@ __global__ __launch_bounds__(1024) void k_argmax(const float *__restrict__ logit
         bv = s_v[w];
         bi = s_i[w];
       }
-    out[b] = bi == 0x7FFFFFFF ? 0 : bi;
+    const int r = act ? act[b] : b;
+    out[r] = bi == 0x7FFFFFFF ? 0 : bi;
     if (advance) {
-      len[b] += 1;
-      rope[b] += 1;
+      len[r] += 1;
+      rope[r] += 1;
     }
   }
 }
 
-__global__ void k_advance(int *len, int *rope, int n) {
+__global__ void k_advance(int *len, int *rope, const int *act, int n) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < n) {
-    len[b] += 1;
-    rope[b] += 1;
+    const int r = act ? act[b] : b;
+    len[r] += 1;
+    rope[r] += 1;
   }
 }
 
-__global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int req, int s_ctx, const int *pos_thw,
-                                                        int ld) {
+__global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int *ready, int req, int s_ctx,
+                                                        const int *pos_thw, int ld) {
   int mx = s_ctx - 1;
   if (pos_thw) {
     mx = 0x80000000;
@@ -147,7 +150,111 @@ __global__ __launch_bounds__(256) void k_prefill_finish(int *len, int *rope, int
   if (threadIdx.x == 0) {
     len[req] = s_ctx;
     rope[req] = mx + 1;
+    ready[req] = 1;
   }
+}
+
+// exclusive prefix sum over the 256 threads of the work group; *total gets the sum
+__device__ int block_scan(int v, int *s_tmp, int *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = v;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int o = __shfl_up(inc, off);
+    if (lane >= off) inc += o;
+  }
+  if (lane == 63) s_tmp[wave] = inc;
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < 4; ++w) {
+    before += w < wave ? s_tmp[w] : 0;
+    all += s_tmp[w];
+  }
+  __syncthreads();
+  *total = all;
+  return before + inc - v;
+}
+
+// Block allocation: each listed request takes the blocks between what it holds
+// and what covers its target length, from the top of the free stack, in list
+// order (a prefix sum hands out disjoint stack ranges, so no atomics).
+__global__ __launch_bounds__(256) void k_kv_reserve(KvPool p, KvReserve r, int decode_n) {
+  __shared__ int s_tmp[4];
+  __shared__ int s_top, s_used;
+  if (threadIdx.x == 0) s_top = *p.top;
+  __syncthreads();
+  const int n = decode_n > 0 ? decode_n : r.n;
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    const int c = c0 + threadIdx.x;
+    int req = -1, need = 0, held = 0;
+    if (c < n) {
+      req = decode_n > 0 ? p.act[c] : r.req[c];
+      const int target = decode_n > 0 ? min(p.len[req] + 1, p.cap[req]) : r.target[c];
+      held = p.nblk[req];
+      need = max(0, (target + p.bt - 1) / p.bt - held);
+    }
+    int total;
+    const int off = block_scan(need, s_tmp, &total);
+    const int top = s_top;
+    if (threadIdx.x == 0) s_used = 0;
+    __syncthreads();
+    // offsets grow along the list, so the requests served are a prefix of it
+    if (need > 0) {
+      if (off + need <= top) {
+        for (int k = 0; k < need; ++k) {
+          const int blk = p.stack[top - 1 - off - k];
+          p.tab[p.toff[req] + held + k] = (int64_t)blk * p.block_elems;
+        }
+        p.nblk[req] = held + need;
+        atomicMax(&s_used, off + need);
+      } else {
+        atomicOr(p.status, 4);  // pool exhausted: the request keeps unallocated entries
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) s_top = top - s_used;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *p.top = s_top;
+}
+
+__global__ __launch_bounds__(256) void k_kv_release(KvPool p, int req) {
+  const int held = p.nblk[req], top = *p.top;
+  for (int k = threadIdx.x; k < held; k += 256) {
+    const int64_t start = p.tab[p.toff[req] + k];
+    p.stack[top + k] = (int)(start / p.block_elems);
+    p.tab[p.toff[req] + k] = -1;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    *p.top = top + held;
+    p.nblk[req] = 0;
+    p.len[req] = 0;
+    p.rope[req] = 0;
+    p.ready[req] = 0;
+  }
+}
+
+__global__ void k_set_int(int *p, int v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
+__global__ __launch_bounds__(256) void k_build_act(const int *ready, int n, int *act) {
+  __shared__ int s_tmp[4];
+  int base = 0;
+  for (int c0 = 0; c0 < n; c0 += 256) {
+    const int c = c0 + threadIdx.x;
+    const int f = c < n && ready[c] ? 1 : 0;
+    int total;
+    const int off = block_scan(f, s_tmp, &total);
+    if (f) act[base + off] = c;
+    base += total;
+  }
+}
+
+__global__ __launch_bounds__(128) void k_set_packed(PackedRows v, PackedRows *dst) {
+  constexpr int N = (int)(sizeof(PackedRows) / 4);
+  const int *src = (const int *)&v;
+  for (int i = threadIdx.x; i < N; i += 128) ((int *)dst)[i] = src[i];
 }
 
 __global__ __launch_bounds__(256) void k_gather_last(const float *x, int d, PackedRows pk, float *out) {
@@ -158,13 +265,13 @@ __global__ __launch_bounds__(256) void k_gather_last(const float *x, int d, Pack
 
 }  // namespace
 
-hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, int n, float *x, int *status,
-                        hipStream_t st) {
+hipError_t launch_embed(int dtype, const void *embed, int vocab, int d, const int *tokens, const int *act, int n,
+                        float *x, int *status, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   switch (dtype) {
-    case HS_F32: HS_LAUNCH(k_embed<HS_F32>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
-    case HS_F16: HS_LAUNCH(k_embed<HS_F16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
-    case HS_BF16: HS_LAUNCH(k_embed<HS_BF16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, x, status); break;
+    case HS_F32: HS_LAUNCH(k_embed<HS_F32>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, act, x, status); break;
+    case HS_F16: HS_LAUNCH(k_embed<HS_F16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, act, x, status); break;
+    case HS_BF16: HS_LAUNCH(k_embed<HS_BF16>, dim3(n), dim3(256), 0, st, embed, vocab, d, tokens, act, x, status); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -183,22 +290,49 @@ hipError_t launch_prefill_rows(int dtype, const void *emb, int n_v, const void *
   return hipGetLastError();
 }
 
-hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, int *len, int *rope_pos,
-                         int advance, hipStream_t st) {
+hipError_t launch_argmax(const float *logits, int vocab, int ld, int n, int *tokens_out, const int *act, int *len,
+                         int *rope_pos, int advance, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  HS_LAUNCH(k_argmax, dim3(n), dim3(1024), 0, st, logits, vocab, ld, tokens_out, len, rope_pos, advance);
+  HS_LAUNCH(k_argmax, dim3(n), dim3(1024), 0, st, logits, vocab, ld, tokens_out, act, len, rope_pos, advance);
   return hipGetLastError();
 }
 
-hipError_t launch_advance(int *len, int *rope_pos, int n, hipStream_t st) {
+hipError_t launch_advance(int *len, int *rope_pos, const int *act, int n, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  HS_LAUNCH(k_advance, dim3((n + 255) / 256), dim3(256), 0, st, len, rope_pos, n);
+  HS_LAUNCH(k_advance, dim3((n + 255) / 256), dim3(256), 0, st, len, rope_pos, act, n);
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_finish(int *len, int *rope_pos, int req, int s_ctx, const int *pos_thw, int ld,
+hipError_t launch_kv_reserve(const KvPool &p, const KvReserve &r, int decode_n, hipStream_t st) {
+  if (decode_n <= 0 && r.n <= 0) return hipSuccess;
+  HS_LAUNCH(k_kv_reserve, dim3(1), dim3(256), 0, st, p, r, decode_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st) {
+  HS_LAUNCH(k_kv_release, dim3(1), dim3(256), 0, st, p, req);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_int(int *p, int v, hipStream_t st) {
+  HS_LAUNCH(k_set_int, dim3(1), dim3(64), 0, st, p, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_build_act(const int *ready, int n, int *act, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  HS_LAUNCH(k_build_act, dim3(1), dim3(256), 0, st, ready, n, act);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_finish(int *len, int *rope_pos, int *ready, int req, int s_ctx, const int *pos_thw, int ld,
                                  hipStream_t st) {
-  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, req, s_ctx, pos_thw, ld);
+  HS_LAUNCH(k_prefill_finish, dim3(1), dim3(256), 0, st, len, rope_pos, ready, req, s_ctx, pos_thw, ld);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_packed(PackedRows *dst, const PackedRows &v, hipStream_t st) {
+  HS_LAUNCH(k_set_packed, dim3(1), dim3(128), 0, st, v, dst);
   return hipGetLastError();
 }
 

@@ -21,7 +21,8 @@ HS_ROPE_1D, HS_ROPE_M3 = 0, 1
 EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "hs_kv_alloc", "hs_kv_free",
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
            "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync",
-           "hs_prefill_batch", "hs_model_reserve_rows")
+           "hs_prefill_batch", "hs_model_reserve_rows", "hs_kv_pool_create", "hs_kv_admit", "hs_kv_release",
+           "hs_kv_pool_blocks")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
         "hs_prefill_embeddings": [P, P, I32, P, P, I32, P, P, P, P],
         "hs_prefill_batch": [P, P, I32, P, P, P, P, P, P, P, P],
         "hs_model_reserve_rows": [P, I64],
+        "hs_kv_pool_create": [P, I32, I32, P, U64, ctypes.POINTER(P)],
+        "hs_kv_admit": [P, I32, I32, I32, P],
+        "hs_kv_release": [P, I32, P],
+        "hs_kv_pool_blocks": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],
         "hs_decode_step": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
@@ -324,3 +329,36 @@ class KVCache:
             self.close()
         except Exception:
             pass
+
+
+class KVPool(KVCache):
+    """Block-granular KV cache: `slots` request slots over n_blocks blocks of
+    block_tokens positions in a caller-owned (or fresh) uint8 device tensor.
+    Requests are admitted into empty slots, prefilled and decoded like
+    KVCache requests (slot = request number) and released when done."""
+
+    def __init__(self, model: Model, slots: int, block_tokens: int, n_blocks: int, buf=None):
+        import torch
+        self.model = model
+        self.batch = slots
+        self.block_tokens = block_tokens
+        block_bytes = hs_kv_bytes(model.cfg, 0, block_tokens)[0]
+        if buf is None:
+            buf = torch.empty(n_blocks * block_bytes, dtype=torch.uint8, device="cuda")
+        self.buf = buf
+        h = ctypes.c_void_p()
+        _call("hs_kv_pool_create", model.handle, slots, block_tokens, _ptr(buf), buf.numel() * buf.element_size(),
+              ctypes.byref(h))
+        self.handle = h
+
+    def admit(self, slot: int, n_v: int, capacity: int) -> None:
+        _call("hs_kv_admit", self.handle, slot, n_v, capacity, _stream())
+
+    def release(self, slot: int) -> None:
+        _call("hs_kv_release", self.handle, slot, _stream())
+
+    def blocks(self) -> tuple:
+        """(free, total) blocks."""
+        f, n = ctypes.c_int32(), ctypes.c_int32()
+        _call("hs_kv_pool_blocks", self.handle, ctypes.byref(f), ctypes.byref(n))
+        return f.value, n.value

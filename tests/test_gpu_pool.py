@@ -1,0 +1,280 @@
+"""Block-granular KV pool (hs_kv_pool_create / hs_kv_admit / hs_kv_release):
+parity with the oracle across block boundaries, continuous batching (a slot
+released and refilled between decode steps), bit-identical layer-0 cache rows
+against a contiguous cache, graph replays that take blocks on the device, and
+the capacity checks."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import LOGIT_TOL, Pair, rel_err, small_cfg, token_ok
+
+pytestmark = pytest.mark.gpu
+
+BT = 64  # positions per block
+
+
+class PoolRun:
+    """A pooled cache on the GPU and one oracle sequence per live slot."""
+
+    def __init__(self, cfg, slots, n_blocks, max_ctx=256):
+        import paper_2603_12707_amd as hs
+        self.cfg = cfg
+        self.pair = Pair(cfg, max_batch=slots, max_ctx=max_ctx)
+        self.pool = hs.KVPool(self.pair.gpu, slots, BT, n_blocks)
+        self.slots = slots
+        self.seqs = {}   # slot -> oracle sequence
+        self.next = {}   # slot -> token to feed next (the oracle's)
+        self.near = 0
+
+    def admit_and_prefill(self, entries, key):
+        """entries: [(slot, n_v, s_text, cap)] prefilled in one batch call;
+        `key` salts the request inputs."""
+        V = self.cfg["vocab"]
+        inputs = []
+        for slot, n_v, s_text, cap in entries:
+            self.pool.admit(slot, n_v, cap)
+            emb, ids, pos = self.pair.request_inputs(key + slot, n_v, s_text)
+            s = self.pair.ora.new_seq(cap)
+            ref = s.prefill(emb if n_v else None, ids, pos)
+            self.seqs[slot] = s
+            inputs.append((emb, ids, pos, ref))
+        embs = [e for e, _, _, _ in inputs if e.shape[0]]
+        idss = [i for _, i, _, _ in inputs if i.shape[0]]
+        lg = torch.empty(len(entries), V, dtype=torch.float32, device="cuda")
+        toks = self.pool.prefill_batch([e[0] for e in entries], torch.cat(embs).cuda() if embs else None,
+                                       torch.cat(idss).cuda() if idss else None, [e[2] for e in entries],
+                                       last_logits=lg)
+        torch.cuda.synchronize()
+        for k, (slot, *_rest) in enumerate(entries):
+            ref_logits, ref_tok = inputs[k][3]
+            g = lg[k].cpu().numpy()
+            assert rel_err(g, ref_logits) <= LOGIT_TOL, (slot, rel_err(g, ref_logits))
+            ok, tie = token_ok(int(toks[k].item()), g, ref_logits)
+            assert ok, (slot, int(toks[k].item()), ref_tok)
+            self.near += tie
+            self.next[slot] = ref_tok
+
+    def release(self, slot):
+        self.pool.release(slot)
+        del self.seqs[slot]
+        del self.next[slot]
+
+    def decode(self, n_steps):
+        V = self.cfg["vocab"]
+        live = sorted(self.seqs)
+        tin = torch.zeros(self.slots, dtype=torch.int32, device="cuda")
+        tout = torch.full((self.slots,), -7, dtype=torch.int32, device="cuda")
+        logits = torch.empty(len(live), V, dtype=torch.float32, device="cuda")
+        for step in range(n_steps):
+            tin.copy_(torch.tensor([self.next.get(s, 0) for s in range(self.slots)], dtype=torch.int32))
+            self.pool.decode(tin, tout, logits)
+            torch.cuda.synchronize()
+            g_tok, g_log = tout.cpu().tolist(), logits.cpu().numpy()
+            for k, slot in enumerate(live):  # logits rows follow slot order
+                r_log, _, r_tok = self.seqs[slot].decode(self.next[slot])
+                assert rel_err(g_log[k], r_log) <= LOGIT_TOL, (step, slot, rel_err(g_log[k], r_log))
+                ok, tie = token_ok(g_tok[slot], g_log[k], r_log)
+                assert ok, (step, slot, g_tok[slot], r_tok)
+                self.near += tie
+                self.next[slot] = r_tok
+            assert all(g_tok[s] == -7 for s in range(self.slots) if s not in self.seqs), g_tok
+
+
+def _used(lengths):
+    return sum((n + BT - 1) // BT for n in lengths)
+
+
+def test_pool_parity_across_blocks_and_continuous_batching():
+    """Three requests in slots 0, 2, 3 of five, contexts 62, 64 and 127
+    positions (64-position blocks): the decode steps cross block boundaries.
+    Then slot 2 is released, a new request is admitted into it (reusing the
+    freed blocks) and prefilled while the others wait, and all decode on."""
+    cfg = small_cfg(n_layers=2, dtype="bf16")
+    run = PoolRun(cfg, slots=5, n_blocks=16)
+    assert run.pool.blocks() == (16, 16)
+    run.admit_and_prefill([(3, 100, 27, 140), (0, 40, 22, 90), (2, 0, 64, 90)], key=0)
+    assert run.pool.lengths() == [62, 0, 64, 127, 0]
+    assert run.pool.blocks() == (16 - _used([62, 64, 127]), 16)
+    run.decode(4)
+    assert run.pool.lengths() == [66, 0, 68, 131, 0]
+    assert run.pool.blocks() == (16 - _used([66, 68, 131]), 16)
+    run.release(2)
+    assert run.pool.blocks() == (16 - _used([66, 131]), 16)
+    run.admit_and_prefill([(2, 17, 110, 140)], key=50)
+    assert run.pool.lengths() == [66, 0, 127, 131, 0]
+    run.decode(3)
+    assert run.pool.lengths() == [69, 0, 130, 134, 0]
+    assert run.pool.blocks() == (16 - _used([69, 130, 134]), 16)
+    assert run.pair.gpu.status() == 0
+    assert run.near <= 2
+
+
+def test_pool_gqa7_mrope():
+    """Pooled cache with 7 query heads per KV head (matrix-core decode
+    attention, block-aligned splits) and M-RoPE."""
+    cfg = small_cfg(n_heads=14, n_kv_heads=2, head_dim=64, dtype="bf16", rope_kind=1, mrope_section=(8, 12, 12),
+                    qkv_bias=1, rope_theta=1e6, rms_eps=1e-6)
+    import paper_2603_12707_amd as hs
+    pair = Pair(cfg, max_batch=3, max_ctx=400)
+    pool = hs.KVPool(pair.gpu, 3, BT, 20)
+    V = cfg["vocab"]
+    lens, seqs, nxt = {0: (121, 70), 1: (60, 3)}, {}, {}
+    embs, idss, poss = [], [], []
+    for slot, (n_v, s_text) in lens.items():
+        pool.admit(slot, n_v, 300)
+        emb, ids, pos = pair.request_inputs(slot, n_v, s_text)
+        seqs[slot] = pair.ora.new_seq(300)
+        nxt[slot] = seqs[slot].prefill(emb, ids, pos)
+        embs.append(emb)
+        idss.append(ids)
+        poss.append(pos)
+    lg = torch.empty(2, V, dtype=torch.float32, device="cuda")
+    toks = pool.prefill_batch([0, 1], torch.cat(embs).cuda(), torch.cat(idss).cuda(), [70, 3],
+                              torch.cat(poss, dim=1).contiguous().cuda(), last_logits=lg)
+    torch.cuda.synchronize()
+    cur = {}
+    for k, slot in enumerate([0, 1]):
+        ref_logits, ref_tok = nxt[slot]
+        assert rel_err(lg[k].cpu().numpy(), ref_logits) <= LOGIT_TOL
+        cur[slot] = ref_tok
+    tin = torch.zeros(3, dtype=torch.int32, device="cuda")
+    tout = torch.zeros(3, dtype=torch.int32, device="cuda")
+    logits = torch.empty(2, V, dtype=torch.float32, device="cuda")
+    for step in range(6):
+        tin.copy_(torch.tensor([cur[0], cur[1], 0], dtype=torch.int32))
+        pool.decode(tin, tout, logits)
+        torch.cuda.synchronize()
+        for k, slot in enumerate([0, 1]):
+            r_log, _, r_tok = seqs[slot].decode(cur[slot])
+            assert rel_err(logits[k].cpu().numpy(), r_log) <= LOGIT_TOL, (step, slot)
+            cur[slot] = r_tok
+    assert pool.lengths() == [197, 69, 0]
+
+
+def test_pool_layer0_rows_bit_identical_to_contiguous_cache():
+    """The same requests, prefilled and decoded with the same tokens, in a
+    contiguous cache and in a pool: the layer-0 K/V rows (which depend on
+    each position's input alone) read back bit for bit equal, across the
+    blocks the pool spread them over."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=1, dtype="f16")
+    shapes = [(30, 50), (0, 70), (64, 1)]  # contexts 80, 70, 65
+    caps = [n + s + 70 for n, s in shapes]
+    pair = Pair(cfg, max_batch=3, max_ctx=max(caps))
+    kv = hs.KVCache(pair.gpu, [n for n, _ in shapes], caps)
+    pool = hs.KVPool(pair.gpu, 3, BT, 12)
+    for slot, (n_v, _) in enumerate(shapes):
+        pool.admit(slot, n_v, caps[slot])
+    inputs = [pair.request_inputs(r, n, s) for r, (n, s) in enumerate(shapes)]
+    emb = torch.cat([e for e, _, _ in inputs if e.shape[0]]).cuda()
+    ids = torch.cat([i for _, i, _ in inputs]).cuda()
+    first_a = kv.prefill_batch([0, 1, 2], emb, ids, [s for _, s in shapes])
+    first_b = pool.prefill_batch([0, 1, 2], emb, ids, [s for _, s in shapes])
+    torch.cuda.synchronize()
+    assert first_a.tolist() == first_b.tolist()
+    tin = first_a.clone()
+    ta, tb = torch.empty_like(tin), torch.empty_like(tin)
+    for _ in range(65):  # every request crosses at least one block boundary
+        kv.decode(tin, ta)
+        pool.decode(tin, tb)
+        tin = ta.clone()
+    torch.cuda.synchronize()
+    assert kv.lengths() == pool.lengths()
+    hd = cfg["head_dim"]
+    for r, n in enumerate(kv.lengths()):
+        for sel in (0, 1):
+            for h in range(cfg["n_kv_heads"]):
+                a = torch.empty(n, hd, dtype=torch.float16)
+                b = torch.empty(n, hd, dtype=torch.float16)
+                kv.read(r, 0, sel, h, 0, n, a)
+                pool.read(r, 0, sel, h, 0, n, b)
+                assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (r, sel, h)
+
+
+def test_pool_graph_replays_take_blocks_on_the_device():
+    """Two decode steps captured once, replayed four times: the requests
+    cross block boundaries inside the replays, and the caches, lengths and
+    free blocks match an identical pool driven by eager calls bit for bit."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=1, dtype="bf16")
+    pair = Pair(cfg, max_batch=2, max_ctx=200)
+    pools = [hs.KVPool(pair.gpu, 2, BT, 8) for _ in range(2)]
+    shapes = [(20, 40), (0, 61)]  # contexts 60, 61: blocks end at 64
+    inputs = [pair.request_inputs(r, n, s) for r, (n, s) in enumerate(shapes)]
+    firsts = []
+    for p in pools:
+        for slot, (n_v, _) in enumerate(shapes):
+            p.admit(slot, n_v, 150)
+        firsts.append(p.prefill_batch([0, 1], inputs[0][0].cuda(), torch.cat([inputs[0][1], inputs[1][1]]).cuda(),
+                                      [40, 61]))
+    torch.cuda.synchronize()
+    eager, graphed = pools
+    ta, tb = firsts[0].clone(), torch.empty_like(firsts[0])
+    ga, gb = firsts[1].clone(), torch.empty_like(firsts[1])
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            graphed.decode(ga, gb)
+            graphed.decode(gb, ga)
+    torch.cuda.current_stream().wait_stream(s)
+    graphed.sync()
+    assert graphed.lengths() == [60, 61]  # capture ran nothing
+    for rep in range(4):
+        g.replay()
+        for _ in range(2):
+            eager.decode(ta, tb)
+            ta, tb = tb, ta
+        torch.cuda.synchronize()
+        assert ga.tolist() == ta.tolist(), rep
+    graphed.sync()
+    assert graphed.lengths() == eager.lengths() == [68, 69]
+    assert graphed.blocks() == eager.blocks() == (8 - 4, 8)
+    hd = cfg["head_dim"]
+    for r, n in enumerate(eager.lengths()):
+        a = torch.empty(n, hd, dtype=torch.bfloat16)
+        b = torch.empty(n, hd, dtype=torch.bfloat16)
+        eager.read(r, 0, 1, 0, 0, n, a)
+        graphed.read(r, 0, 1, 0, 0, n, b)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), r
+
+
+def test_pool_capacity_and_admission_errors():
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=1, dtype="bf16")
+    pair = Pair(cfg, max_batch=3, max_ctx=300)
+    with pytest.raises(hs.HsError) as e:
+        hs.KVPool(pair.gpu, 3, 48, 4)                 # block size not a power of two
+    assert e.value.code == hs.HS_E_INVALID
+    pool = hs.KVPool(pair.gpu, 3, BT, 3)
+    ids = torch.randint(0, cfg["vocab"], (200,), dtype=torch.int32).cuda()
+    pool.admit(0, 0, 250)
+    with pytest.raises(hs.HsError) as e:
+        pool.admit(0, 0, 10)                          # slot in use
+    assert e.value.code == hs.HS_E_STATE
+    with pytest.raises(hs.HsError) as e:
+        pool.prefill(1, None, ids[:5])                # slot 1 holds no request
+    assert e.value.code == hs.HS_E_STATE
+    with pytest.raises(hs.HsError) as e:
+        pool.prefill(0, None, ids)                    # 200 positions: 4 blocks > 3
+    assert e.value.code == hs.HS_E_CAPACITY
+    assert pool.lengths() == [0, 0, 0] and pool.blocks() == (3, 3)
+    pool.prefill(0, None, ids[:128])                  # 2 blocks
+    pool.admit(1, 0, 100)
+    pool.prefill(1, None, ids[:64])                   # 1 block: the pool is full
+    assert pool.blocks() == (0, 3)
+    tin = torch.zeros(3, dtype=torch.int32, device="cuda")
+    tout = torch.zeros(3, dtype=torch.int32, device="cuda")
+    with pytest.raises(hs.HsError) as e:
+        pool.decode(tin, tout)                        # both enter a new block
+    assert e.value.code == hs.HS_E_CAPACITY
+    assert pool.lengths() == [128, 64, 0]
+    pool.release(1)
+    assert pool.blocks() == (1, 3)
+    pool.decode(tin, tout)                            # request 0 alone takes the free block
+    assert pool.lengths() == [129, 0, 0] and pool.blocks() == (0, 3)
+    assert pair.gpu.status() == 0
