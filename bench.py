@@ -113,7 +113,7 @@ def steps_after_context(warmup: int, steps: int) -> int:
     return warmup + steps + 1
 
 
-def setup(cfg: dict, n_steps_total: int):
+def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
     import torch
 
     import paper_2603_12707_amd as hs
@@ -136,16 +136,22 @@ def setup(cfg: dict, n_steps_total: int):
         lens = [a + b for a, b in zip(n_v, s_text)]
     caps = [n + n_steps_total for n in lens]
     model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True)
-    kv = hs.KVCache(model, n_v, caps)
+    if pool_block:  # block-granular cache: one slot per request, admitted up front
+        n_blocks = sum((c + pool_block - 1) // pool_block for c in caps)
+        kv = hs.KVPool(model, B, pool_block, n_blocks)
+        for r in range(B):
+            kv.admit(r, n_v[r], caps[r])
+    else:
+        kv = hs.KVCache(model, n_v, caps)
     first = torch.empty(B, dtype=torch.int32, device="cuda")
     t = time.time()
     if "kv_len" in cfg:
         for r in range(B):
+            kv.set_length(r, lens[r], lens[r])  # a pool takes the blocks here
             for layer in range(cfg["n_layers"]):
                 for sel in (0, 1):
                     for h in range(cfg["n_kv_heads"]):
                         kv.write(r, layer, sel, h, 0, synth.kv_block(cfg, r, layer, sel, h, lens[r], device="cuda"))
-            kv.set_length(r, lens[r], lens[r])
         first.copy_(synth.decode_tokens(cfg, 0, B, device="cuda"))
     else:
         # inputs first, packed request by request; then the timed prefill
@@ -209,6 +215,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="also time the decode step replayed from a HIP graph (stream capture)")
+    ap.add_argument("--kv-pool-block", type=int, default=0,
+                    help="decode from a block-granular KV pool with blocks of this many positions (0: contiguous)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -226,7 +234,8 @@ def main() -> int:
     B = cfg["batch"]
     torch.cuda.set_device(0)
     graph_steps = 2 * (max(1, args.steps // 4) + 1) if args.graph else 0
-    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps)
+    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps,
+                                       args.kv_pool_block)
 
     tin = first.clone()
     tout = torch.empty_like(tin)
@@ -338,7 +347,8 @@ def main() -> int:
         "config": {"workload": args.workload, "batch": B, "context_at_start": lens_start[0] if B == 1 else
                    [min(lens_start), max(lens_start)], "n_layers": cfg["n_layers"], "d_model": cfg["d_model"],
                    "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"], "ffn_dim": cfg["ffn_dim"],
-                   "vocab": cfg["vocab"] if has_head else None, "parallelism": "none (one GPU)"},
+                   "vocab": cfg["vocab"] if has_head else None, "parallelism": "none (one GPU)",
+                   "kv_cache": f"pool of {args.kv_pool_block}-position blocks" if args.kv_pool_block else "contiguous"},
         "hbm_gbps": round(gbs, 1),
         "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
         "bytes_per_step": total_bytes // args.steps,
