@@ -176,8 +176,8 @@ int hs_kv_free(hs_kv *kv);
  *                                 + p % block_tokens) * head_dim + e,
  * start(r, k) being the element offset of the k-th block the slot holds.
  * The handle has `slots` slots (1..4096), all empty; block_tokens is a power
- * of two in 64..4096 (attention splits never cross a block); 16-bit storage
- * only.  Blocks are handed out on the device, from a free list, as a slot's
+ * of two in 256..16384 (decode attention reads a block in whole batches of
+ * up to 256 positions); 16-bit storage only.  Blocks are handed out on the device, from a free list, as a slot's
  * length reaches them: at prefill for the context, and inside
  * hs_decode_step when a request enters a new block, so decode stays
  * graph-replayable.  hs_prefill_embeddings / hs_prefill_batch take slot

@@ -103,16 +103,15 @@ KvPool kv_pool(const hs_kv *kv) {
 
 int blocks_for(const hs_kv *kv, int len) { return (len + kv->block_tokens - 1) / kv->block_tokens; }
 
-// The split policy, with splits that never cross a block of a pooled cache:
-// a power of two between 64 (a multiple of every attention kernel's step)
-// and the block size.
-void kv_split_policy(const hs_config &c, bool pool, int block_tokens, int nq, int max_len, int *S, int *ns) {
+// The split policy; a pooled cache's splits are whole multiples of
+// POOL_SPAN positions, the longest batch of loads of any attention kernel, so
+// that no batch crosses a block (blocks are multiples of it too).
+constexpr int POOL_SPAN = 256;
+void kv_split_policy(const hs_config &c, bool pool, int nq, int max_len, int *S, int *ns) {
   split_policy(nq, c.n_kv_heads, c.n_heads / c.n_kv_heads, c.head_dim, c.dtype, max_len, S, ns);
   if (!pool) return;
-  int s = 64;
-  while (s < *S && s < block_tokens) s *= 2;
-  *S = s;
-  *ns = (max_len + s - 1) / s;
+  *S = (*S + POOL_SPAN - 1) / POOL_SPAN * POOL_SPAN;
+  *ns = (max_len + *S - 1) / *S;
 }
 
 // the ready requests, in order, as the decode columns (pooled caches)
@@ -328,7 +327,7 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out, int *blo
     return fail(HS_E_CAPACITY, "decode: the pool has %d free blocks, the step needs %d", kv->free_blocks, need);
   if (blocks_needed) *blocks_needed = need;
   int S, ns;
-  kv_split_policy(c, kv->pool, kv->block_tokens, B, kv->max_cap, &S, &ns);
+  kv_split_policy(c, kv->pool, B, kv->max_cap, &S, &ns);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
   *out = Step{m, kv, B, 0, PackedRows{}, kv->d_rope, B, S, ns, st};
@@ -688,8 +687,8 @@ int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *de
   const hs_config &c = m->cfg;
   if (c.dtype == HS_F32) return fail(HS_E_INVALID, "hs_kv_pool_create: pooled caches take 16-bit storage");
   if (slots <= 0 || slots > 4096) return fail(HS_E_INVALID, "hs_kv_pool_create: slots must be in 1..4096");
-  if (block_tokens < 64 || block_tokens > 4096 || (block_tokens & (block_tokens - 1)))
-    return fail(HS_E_INVALID, "hs_kv_pool_create: block_tokens must be a power of two in 64..4096");
+  if (block_tokens < POOL_SPAN || block_tokens > 16384 || (block_tokens & (block_tokens - 1)))
+    return fail(HS_E_INVALID, "hs_kv_pool_create: block_tokens must be a power of two in 256..16384");
   if (((uintptr_t)dev_buf) % 16) return fail(HS_E_INVALID, "hs_kv_pool_create: buffer must be 16-byte aligned");
   const int64_t block_elems = kv_request_elems(c, block_tokens);
   const uint64_t block_bytes = (uint64_t)block_elems * dtype_bytes(c.dtype);
@@ -701,7 +700,7 @@ int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *de
   int64_t entries = m->part_entries;
   for (int nq = 1; nq <= std::min(slots, m->max_batch); ++nq) {
     int S, ns;
-    kv_split_policy(c, true, block_tokens, nq, m->max_ctx, &S, &ns);
+    kv_split_policy(c, true, nq, m->max_ctx, &S, &ns);
     if (ns > 1) entries = std::max(entries, (int64_t)nq * c.n_heads * ns);
   }
   if (entries > m->part_entries) {

@@ -72,17 +72,24 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tg = lane / LPT, c = lane % LPT;
-  // the split lies in one block of the request
-  int64_t ko, vo;
+  // one block per request: the split's rows are one range.  Several blocks:
+  // each batch of loads (a whole number of which fills a block) reads the
+  // block holding it, whose start is read one batch ahead.
+  int64_t ko = 0, vo = 0;
+  int bt = 0, toff = 0;
+  int64_t kin = 0, vin = 0, b_next = 0;
   if constexpr (PAGED) {
-    ko = kv_rows(a.kv, req, a.layer, 0, a.n_kv, j, t0, HD);
-    vo = kv_rows(a.kv, req, a.layer, 1, a.n_kv, j, t0, HD);
+    bt = a.kv.bt[req];
+    toff = a.kv.toff[req];
+    kin = (int64_t)((a.layer * 2) * a.n_kv + j) * bt * HD;
+    vin = kin + (int64_t)a.n_kv * bt * HD;
+    b_next = a.kv.tab[toff + t0 / bt];
   } else {
     const int64_t b = a.kv.tab[req];
     ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
     vo = ko + (int64_t)a.n_kv * cap * HD;
   }
-  const uint32_t nbytes = ko < 0 ? 0u : (uint32_t)n * HD * SB;
+  const uint32_t nbytes = (uint32_t)n * HD * SB;
   const rsrc_t kr = make_rsrc((const S *)a.kv.buf + max(ko, (int64_t)0), nbytes);
   const rsrc_t vr = make_rsrc((const S *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
@@ -103,11 +110,23 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
     // all K and V chunks of the batch are requested before any is used;
     // positions past the split read zeros
     u32x4 kc[UB], vc[UB];
+    rsrc_t kb = kr, vb = vr;
+    int rel = 0;
+    if constexpr (PAGED) {
+      const int64_t b0 = b_next;
+      const int pb = t0 + it0 * STEP, pn = pb + UB * STEP;
+      b_next = pn < t0 + n ? a.kv.tab[toff + pn / bt] : 0;
+      const int64_t at = max(b0, (int64_t)0) + (int64_t)(pb % bt) * HD;
+      const uint32_t bytes = b0 < 0 ? 0u : (uint32_t)min(UB * STEP, n - it0 * STEP) * HD * SB;
+      kb = make_rsrc((const S *)a.kv.buf + at + kin, bytes);
+      vb = make_rsrc((const S *)a.kv.buf + at + vin, bytes);
+      rel = it0 * STEP;
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const uint32_t off = (uint32_t)((it0 + u) * STEP + wave * TPW + tg) * (HD * SB) + (uint32_t)c * 16u;
-      kc[u] = bld16_stream(kr, off);
-      vc[u] = bld16_stream(vr, off);
+      const uint32_t off = (uint32_t)((it0 + u) * STEP - rel + wave * TPW + tg) * (HD * SB) + (uint32_t)c * 16u;
+      kc[u] = bld16_stream(kb, off);
+      vc[u] = bld16_stream(vb, off);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
@@ -244,17 +263,24 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lg = lane >> 4;
-  // the split lies in one block of the request
-  int64_t ko, vo;
+  // one block per request: the split's rows are one range.  Several blocks:
+  // each batch of loads (a whole number of which fills a block) reads the
+  // block holding it, whose start is read one batch ahead.
+  int64_t ko = 0, vo = 0;
+  int bt = 0, toff = 0;
+  int64_t kin = 0, vin = 0, b_next = 0;
   if constexpr (PAGED) {
-    ko = kv_rows(a.kv, req, a.layer, 0, a.n_kv, j, t0, HD);
-    vo = kv_rows(a.kv, req, a.layer, 1, a.n_kv, j, t0, HD);
+    bt = a.kv.bt[req];
+    toff = a.kv.toff[req];
+    kin = (int64_t)((a.layer * 2) * a.n_kv + j) * bt * HD;
+    vin = kin + (int64_t)a.n_kv * bt * HD;
+    b_next = a.kv.tab[toff + t0 / bt];
   } else {
     const int64_t b = a.kv.tab[req];
     ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
     vo = ko + (int64_t)a.n_kv * cap * HD;
   }
-  const uint32_t nbytes = ko < 0 ? 0u : (uint32_t)n * HD * SB;
+  const uint32_t nbytes = (uint32_t)n * HD * SB;
   const rsrc_t kr = make_rsrc((const uint16_t *)a.kv.buf + max(ko, (int64_t)0), nbytes);
   const rsrc_t vr = make_rsrc((const uint16_t *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
@@ -274,15 +300,27 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
     // every K and V chunk of the batch is requested before any is used;
     // positions past the split read zeros
     u32x4 kc[UB][KK], vc[UB][4];
+    rsrc_t kb = kr, vb = vr;
+    int rel = 0;
+    if constexpr (PAGED) {
+      const int64_t b0 = b_next;
+      const int pb = t0 + it0 * STEP, pn = pb + UB * STEP;
+      b_next = pn < t0 + n ? a.kv.tab[toff + pn / bt] : 0;
+      const int64_t at = max(b0, (int64_t)0) + (int64_t)(pb % bt) * HD;
+      const uint32_t bytes = b0 < 0 ? 0u : (uint32_t)min(UB * STEP, n - it0 * STEP) * HD * SB;
+      kb = make_rsrc((const uint16_t *)a.kv.buf + at + kin, bytes);
+      vb = make_rsrc((const uint16_t *)a.kv.buf + at + vin, bytes);
+      rel = it0 * STEP;
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int p0 = ((it0 + u) * NW + wave) * 16;
+      const int p0 = ((it0 + u) * NW + wave) * 16 - rel;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        kc[u][kk] = bld16_stream(kr, (uint32_t)((p0 + li) * HD + (kk * 4 + lg) * 8) * SB);
+        kc[u][kk] = bld16_stream(kb, (uint32_t)((p0 + li) * HD + (kk * 4 + lg) * 8) * SB);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        vc[u][i] = bld16_stream(vr, li < CPR ? (uint32_t)((p0 + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
+        vc[u][i] = bld16_stream(vb, li < CPR ? (uint32_t)((p0 + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {

@@ -117,7 +117,7 @@ struct AttnArgs {
   int prefill;     // 0: decode (query = column c, request act[c], length = len + 1); 1: prefill rows in *pk
   const PackedRows *pk;  // device copy; query row r of request i has length r - cu[i] + 1
   int prefill_tiles;     // prefill: query tiles in all (pk->tcu[pk->n])
-  int S;           // positions per split (a split never crosses a block of the request)
+  int S;           // positions per split (pooled caches: a multiple of 256)
   int n_split;     // splits per (query, kv head)
   float *part_o;   // [nq][n_heads][n_split][head_dim]
   float *part_ml;  // [nq][n_heads][n_split][2]

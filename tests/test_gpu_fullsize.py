@@ -45,6 +45,7 @@ def _weights(cfg):
 def _fill_both(cfg, kv, req, seq, length, rope_pos):
     """Writes the same synthetic cache rows [0, length) of request req into
     the GPU cache and into the oracle sequence."""
+    kv.set_length(req, length, rope_pos)  # a pooled cache takes the blocks here
     for layer in range(cfg["n_layers"]):
         for sel in (0, 1):
             for h in range(cfg["n_kv_heads"]):
@@ -52,7 +53,6 @@ def _fill_both(cfg, kv, req, seq, length, rope_pos):
                 kv.write(req, layer, sel, h, 0, rows)
                 if seq is not None:
                     seq.write_kv(layer, sel, h, 0, rows.float().cpu())
-    kv.set_length(req, length, rope_pos)
     if seq is not None:
         seq.set_len(length, rope_pos)
 
@@ -216,17 +216,25 @@ def test_qwen7b_b16_sampled_requests_mrope(qwen):
     model.close()
 
 
-def test_qwen_layer_b256_sampled_requests():
+@pytest.mark.parametrize("pool_block", [0, 256])
+def test_qwen_layer_b256_sampled_requests(pool_block):
     """One Qwen-shaped layer, batch 256, KV lengths U[1024, 8192]: the
     residual stream after the layer and the appended rows, for sampled
-    requests, over two appending steps."""
+    requests, over two appending steps; in a contiguous cache and in a pool
+    of 256-position blocks (decode splits of several thousand positions
+    read dozens of blocks)."""
     import paper_2603_12707_amd as hs
     cfg = configs.get("qwen_layer_b256")
     w_cpu, w_gpu = _weights(cfg)
     lens = synth.kv_lengths(cfg)
     caps = [n + 4 for n in lens]
     model = hs.Model(cfg, w_gpu, max_batch=256, max_ctx=max(caps), packed=True)
-    kv = hs.KVCache(model, [0] * 256, caps)
+    if pool_block:
+        kv = hs.KVPool(model, 256, pool_block, sum((c + pool_block - 1) // pool_block for c in caps))
+        for r in range(256):
+            kv.admit(r, 0, caps[r])
+    else:
+        kv = hs.KVCache(model, [0] * 256, caps)
     sample = [0, 100, int(np.argmax(lens)), 255]
     om = O.Model(cfg, w_cpu)
     seqs = {}

@@ -13,13 +13,13 @@ from helpers import LOGIT_TOL, Pair, rel_err, small_cfg, token_ok
 
 pytestmark = pytest.mark.gpu
 
-BT = 64  # positions per block
+BT = 256  # positions per block
 
 
 class PoolRun:
     """A pooled cache on the GPU and one oracle sequence per live slot."""
 
-    def __init__(self, cfg, slots, n_blocks, max_ctx=256):
+    def __init__(self, cfg, slots, n_blocks, max_ctx=512):
         import paper_2603_12707_amd as hs
         self.cfg = cfg
         self.pair = Pair(cfg, max_batch=slots, max_ctx=max_ctx)
@@ -88,40 +88,41 @@ def _used(lengths):
 
 
 def test_pool_parity_across_blocks_and_continuous_batching():
-    """Three requests in slots 0, 2, 3 of five, contexts 62, 64 and 127
-    positions (64-position blocks): the decode steps cross block boundaries.
-    Then slot 2 is released, a new request is admitted into it (reusing the
-    freed blocks) and prefilled while the others wait, and all decode on."""
+    """Three requests in slots 0, 2, 3 of five, contexts 254, 256 and 299
+    positions (256-position blocks): the decode steps cross block
+    boundaries.  Then slot 2 is released, a new request is admitted into it
+    (reusing the freed blocks) and prefilled while the others wait, and all
+    decode on."""
     cfg = small_cfg(n_layers=2, dtype="bf16")
     run = PoolRun(cfg, slots=5, n_blocks=16)
     assert run.pool.blocks() == (16, 16)
-    run.admit_and_prefill([(3, 100, 27, 140), (0, 40, 22, 90), (2, 0, 64, 90)], key=0)
-    assert run.pool.lengths() == [62, 0, 64, 127, 0]
-    assert run.pool.blocks() == (16 - _used([62, 64, 127]), 16)
+    run.admit_and_prefill([(3, 200, 99, 340), (0, 40, 214, 300), (2, 0, 256, 300)], key=0)
+    assert run.pool.lengths() == [254, 0, 256, 299, 0]
+    assert run.pool.blocks() == (16 - _used([254, 256, 299]), 16)
     run.decode(4)
-    assert run.pool.lengths() == [66, 0, 68, 131, 0]
-    assert run.pool.blocks() == (16 - _used([66, 68, 131]), 16)
+    assert run.pool.lengths() == [258, 0, 260, 303, 0]
+    assert run.pool.blocks() == (16 - _used([258, 260, 303]), 16)
     run.release(2)
-    assert run.pool.blocks() == (16 - _used([66, 131]), 16)
-    run.admit_and_prefill([(2, 17, 110, 140)], key=50)
-    assert run.pool.lengths() == [66, 0, 127, 131, 0]
+    assert run.pool.blocks() == (16 - _used([258, 303]), 16)
+    run.admit_and_prefill([(2, 17, 240, 300)], key=50)
+    assert run.pool.lengths() == [258, 0, 257, 303, 0]
     run.decode(3)
-    assert run.pool.lengths() == [69, 0, 130, 134, 0]
-    assert run.pool.blocks() == (16 - _used([69, 130, 134]), 16)
+    assert run.pool.lengths() == [261, 0, 260, 306, 0]
+    assert run.pool.blocks() == (16 - _used([261, 260, 306]), 16)
     assert run.pair.gpu.status() == 0
     assert run.near <= 2
 
 
 def test_pool_gqa7_mrope():
     """Pooled cache with 7 query heads per KV head (matrix-core decode
-    attention, block-aligned splits) and M-RoPE."""
+    attention reading the blocks batch by batch) and M-RoPE."""
     cfg = small_cfg(n_heads=14, n_kv_heads=2, head_dim=64, dtype="bf16", rope_kind=1, mrope_section=(8, 12, 12),
                     qkv_bias=1, rope_theta=1e6, rms_eps=1e-6)
     import paper_2603_12707_amd as hs
     pair = Pair(cfg, max_batch=3, max_ctx=400)
-    pool = hs.KVPool(pair.gpu, 3, BT, 20)
+    pool = hs.KVPool(pair.gpu, 3, BT, 6)
     V = cfg["vocab"]
-    lens, seqs, nxt = {0: (121, 70), 1: (60, 3)}, {}, {}
+    lens, seqs, nxt = {0: (121, 134), 1: (60, 3)}, {}, {}
     embs, idss, poss = [], [], []
     for slot, (n_v, s_text) in lens.items():
         pool.admit(slot, n_v, 300)
@@ -132,7 +133,7 @@ def test_pool_gqa7_mrope():
         idss.append(ids)
         poss.append(pos)
     lg = torch.empty(2, V, dtype=torch.float32, device="cuda")
-    toks = pool.prefill_batch([0, 1], torch.cat(embs).cuda(), torch.cat(idss).cuda(), [70, 3],
+    toks = pool.prefill_batch([0, 1], torch.cat(embs).cuda(), torch.cat(idss).cuda(), [134, 3],
                               torch.cat(poss, dim=1).contiguous().cuda(), last_logits=lg)
     torch.cuda.synchronize()
     cur = {}
@@ -151,7 +152,7 @@ def test_pool_gqa7_mrope():
             r_log, _, r_tok = seqs[slot].decode(cur[slot])
             assert rel_err(logits[k].cpu().numpy(), r_log) <= LOGIT_TOL, (step, slot)
             cur[slot] = r_tok
-    assert pool.lengths() == [197, 69, 0]
+    assert pool.lengths() == [261, 69, 0]
 
 
 def test_pool_layer0_rows_bit_identical_to_contiguous_cache():
@@ -161,11 +162,11 @@ def test_pool_layer0_rows_bit_identical_to_contiguous_cache():
     blocks the pool spread them over."""
     import paper_2603_12707_amd as hs
     cfg = small_cfg(n_layers=1, dtype="f16")
-    shapes = [(30, 50), (0, 70), (64, 1)]  # contexts 80, 70, 65
-    caps = [n + s + 70 for n, s in shapes]
+    shapes = [(200, 50), (0, 240), (250, 1)]  # contexts 250, 240, 251
+    caps = [n + s + 30 for n, s in shapes]
     pair = Pair(cfg, max_batch=3, max_ctx=max(caps))
     kv = hs.KVCache(pair.gpu, [n for n, _ in shapes], caps)
-    pool = hs.KVPool(pair.gpu, 3, BT, 12)
+    pool = hs.KVPool(pair.gpu, 3, BT, 6)
     for slot, (n_v, _) in enumerate(shapes):
         pool.admit(slot, n_v, caps[slot])
     inputs = [pair.request_inputs(r, n, s) for r, (n, s) in enumerate(shapes)]
@@ -177,7 +178,7 @@ def test_pool_layer0_rows_bit_identical_to_contiguous_cache():
     assert first_a.tolist() == first_b.tolist()
     tin = first_a.clone()
     ta, tb = torch.empty_like(tin), torch.empty_like(tin)
-    for _ in range(65):  # every request crosses at least one block boundary
+    for _ in range(20):  # every request crosses a block boundary
         kv.decode(tin, ta)
         pool.decode(tin, tb)
         tin = ta.clone()
@@ -200,16 +201,16 @@ def test_pool_graph_replays_take_blocks_on_the_device():
     free blocks match an identical pool driven by eager calls bit for bit."""
     import paper_2603_12707_amd as hs
     cfg = small_cfg(n_layers=1, dtype="bf16")
-    pair = Pair(cfg, max_batch=2, max_ctx=200)
+    pair = Pair(cfg, max_batch=2, max_ctx=400)
     pools = [hs.KVPool(pair.gpu, 2, BT, 8) for _ in range(2)]
-    shapes = [(20, 40), (0, 61)]  # contexts 60, 61: blocks end at 64
+    shapes = [(20, 234), (0, 253)]  # contexts 254, 253: blocks end at 256
     inputs = [pair.request_inputs(r, n, s) for r, (n, s) in enumerate(shapes)]
     firsts = []
     for p in pools:
         for slot, (n_v, _) in enumerate(shapes):
-            p.admit(slot, n_v, 150)
+            p.admit(slot, n_v, 300)
         firsts.append(p.prefill_batch([0, 1], inputs[0][0].cuda(), torch.cat([inputs[0][1], inputs[1][1]]).cuda(),
-                                      [40, 61]))
+                                      [234, 253]))
     torch.cuda.synchronize()
     eager, graphed = pools
     ta, tb = firsts[0].clone(), torch.empty_like(firsts[0])
@@ -223,7 +224,7 @@ def test_pool_graph_replays_take_blocks_on_the_device():
             graphed.decode(gb, ga)
     torch.cuda.current_stream().wait_stream(s)
     graphed.sync()
-    assert graphed.lengths() == [60, 61]  # capture ran nothing
+    assert graphed.lengths() == [254, 253]  # capture ran nothing
     for rep in range(4):
         g.replay()
         for _ in range(2):
@@ -232,7 +233,7 @@ def test_pool_graph_replays_take_blocks_on_the_device():
         torch.cuda.synchronize()
         assert ga.tolist() == ta.tolist(), rep
     graphed.sync()
-    assert graphed.lengths() == eager.lengths() == [68, 69]
+    assert graphed.lengths() == eager.lengths() == [262, 261]
     assert graphed.blocks() == eager.blocks() == (8 - 4, 8)
     hd = cfg["head_dim"]
     for r, n in enumerate(eager.lengths()):
@@ -246,13 +247,16 @@ def test_pool_graph_replays_take_blocks_on_the_device():
 def test_pool_capacity_and_admission_errors():
     import paper_2603_12707_amd as hs
     cfg = small_cfg(n_layers=1, dtype="bf16")
-    pair = Pair(cfg, max_batch=3, max_ctx=300)
+    pair = Pair(cfg, max_batch=3, max_ctx=1024)
     with pytest.raises(hs.HsError) as e:
-        hs.KVPool(pair.gpu, 3, 48, 4)                 # block size not a power of two
+        hs.KVPool(pair.gpu, 3, 384, 4)                # block size not a power of two
+    assert e.value.code == hs.HS_E_INVALID
+    with pytest.raises(hs.HsError) as e:
+        hs.KVPool(pair.gpu, 3, 128, 4)                # below one batch of attention loads
     assert e.value.code == hs.HS_E_INVALID
     pool = hs.KVPool(pair.gpu, 3, BT, 3)
-    ids = torch.randint(0, cfg["vocab"], (200,), dtype=torch.int32).cuda()
-    pool.admit(0, 0, 250)
+    ids = torch.randint(0, cfg["vocab"], (800,), dtype=torch.int32).cuda()
+    pool.admit(0, 0, 900)
     with pytest.raises(hs.HsError) as e:
         pool.admit(0, 0, 10)                          # slot in use
     assert e.value.code == hs.HS_E_STATE
@@ -260,21 +264,21 @@ def test_pool_capacity_and_admission_errors():
         pool.prefill(1, None, ids[:5])                # slot 1 holds no request
     assert e.value.code == hs.HS_E_STATE
     with pytest.raises(hs.HsError) as e:
-        pool.prefill(0, None, ids)                    # 200 positions: 4 blocks > 3
+        pool.prefill(0, None, ids)                    # 800 positions: 4 blocks > 3
     assert e.value.code == hs.HS_E_CAPACITY
     assert pool.lengths() == [0, 0, 0] and pool.blocks() == (3, 3)
-    pool.prefill(0, None, ids[:128])                  # 2 blocks
-    pool.admit(1, 0, 100)
-    pool.prefill(1, None, ids[:64])                   # 1 block: the pool is full
+    pool.prefill(0, None, ids[:512])                  # 2 blocks
+    pool.admit(1, 0, 400)
+    pool.prefill(1, None, ids[:256])                  # 1 block: the pool is full
     assert pool.blocks() == (0, 3)
     tin = torch.zeros(3, dtype=torch.int32, device="cuda")
     tout = torch.zeros(3, dtype=torch.int32, device="cuda")
     with pytest.raises(hs.HsError) as e:
         pool.decode(tin, tout)                        # both enter a new block
     assert e.value.code == hs.HS_E_CAPACITY
-    assert pool.lengths() == [128, 64, 0]
+    assert pool.lengths() == [512, 256, 0]
     pool.release(1)
     assert pool.blocks() == (1, 3)
     pool.decode(tin, tout)                            # request 0 alone takes the free block
-    assert pool.lengths() == [129, 0, 0] and pool.blocks() == (0, 3)
+    assert pool.lengths() == [513, 0, 0] and pool.blocks() == (0, 3)
     assert pair.gpu.status() == 0
