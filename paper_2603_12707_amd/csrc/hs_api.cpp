@@ -114,13 +114,20 @@ void kv_split_policy(const hs_config &c, bool pool, int nq, int max_len, int *S,
   *ns = (max_len + *S - 1) / *S;
 }
 
+// the decode columns' dispatch order, longest first; every request grows by
+// one position per step, so it holds until the batch changes
+hipError_t rebuild_order(hs_kv *kv, hipStream_t st) {
+  return launch_build_order(kv->d_len, kv->pool ? kv->d_act : nullptr, kv->n_active, kv->d_order, st);
+}
+
 // the ready requests, in order, as the decode columns (pooled caches)
 hipError_t rebuild_active(hs_kv *kv, hipStream_t st) {
   kv->act_host.clear();
   for (int r = 0; r < kv->batch; ++r)
     if (kv->ready[r]) kv->act_host.push_back(r);
   kv->n_active = (int)kv->act_host.size();
-  return launch_build_act(kv->d_ready, kv->batch, kv->d_act, st);
+  const hipError_t e = launch_build_act(kv->d_ready, kv->batch, kv->d_act, st);
+  return e != hipSuccess ? e : rebuild_order(kv, st);
 }
 
 void free_model(hs_model *m) {
@@ -202,6 +209,7 @@ struct Step {
     a.part_o = m->part_o;
     a.part_ml = m->part_ml;
     a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
+    a.order = !prefill && ncols > 1 ? kv->d_order : nullptr;
     a.out = m->attn;
     return a;
   }
@@ -437,7 +445,7 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     roff += rows;
     i0 += pk.n;
   }
-  if (kv->pool) HIP_TRY(rebuild_active(kv, st));
+  HIP_TRY(kv->pool ? rebuild_active(kv, st) : rebuild_order(kv, st));
   return HS_OK;
 }
 
@@ -653,11 +661,12 @@ int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *c
   bool ok = hipMalloc(&kv->d_base, batch * 8) == hipSuccess && hipMalloc(&kv->d_cap, batch * 4) == hipSuccess &&
             hipMalloc(&kv->d_len, batch * 4) == hipSuccess && hipMalloc(&kv->d_rope, batch * 4) == hipSuccess &&
             hipMalloc(&kv->d_toff, batch * 4) == hipSuccess && hipMalloc(&kv->d_act, batch * 4) == hipSuccess &&
-            hipMalloc(&kv->d_ready, batch * 4) == hipSuccess;
+            hipMalloc(&kv->d_ready, batch * 4) == hipSuccess && hipMalloc(&kv->d_order, batch * 4) == hipSuccess;
   ok = ok && hipMemcpy(kv->d_base, kv->base.data(), batch * 8, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(kv->d_cap, kv->cap.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(kv->d_toff, ident.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(kv->d_act, ident.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
+       hipMemcpy(kv->d_order, ident.data(), batch * 4, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemset(kv->d_len, 0, batch * 4) == hipSuccess && hipMemset(kv->d_rope, 0, batch * 4) == hipSuccess &&
        hipMemset(kv->d_ready, 0, batch * 4) == hipSuccess;
   kv->d_bt = kv->d_cap;
@@ -671,7 +680,7 @@ int hs_kv_alloc(hs_model *m, int32_t batch, const int32_t *n_v, const int32_t *c
 
 int hs_kv_free(hs_kv *kv) {
   if (!kv) return fail(HS_E_INVALID, "hs_kv_free: NULL");
-  void *ptrs[] = {kv->d_base, kv->d_cap,  kv->d_len,   kv->d_rope, kv->d_toff, kv->d_act,
+  void *ptrs[] = {kv->d_base,  kv->d_cap,   kv->d_len,  kv->d_rope, kv->d_toff, kv->d_act, kv->d_order,
                   kv->d_ready, kv->d_stack, kv->d_top, kv->d_nblk, kv->d_bt == kv->d_cap ? nullptr : kv->d_bt};
   for (void *p : ptrs)
     if (p) (void)hipFree(p);
@@ -747,6 +756,7 @@ int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *de
             hipMalloc(&kv->d_len, sb) == hipSuccess && hipMalloc(&kv->d_rope, sb) == hipSuccess &&
             hipMalloc(&kv->d_toff, sb) == hipSuccess && hipMalloc(&kv->d_bt, sb) == hipSuccess &&
             hipMalloc(&kv->d_act, sb) == hipSuccess && hipMalloc(&kv->d_ready, sb) == hipSuccess &&
+            hipMalloc(&kv->d_order, sb) == hipSuccess &&
             hipMalloc(&kv->d_nblk, sb) == hipSuccess && hipMalloc(&kv->d_stack, n_blocks * 4) == hipSuccess &&
             hipMalloc(&kv->d_top, 4) == hipSuccess;
   ok = ok && hipMemcpy(kv->d_base, tab.data(), (size_t)kv->ntab * 8, hipMemcpyHostToDevice) == hipSuccess &&
@@ -756,6 +766,7 @@ int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *de
        hipMemcpy(kv->d_top, &top, 4, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemset(kv->d_cap, 0, sb) == hipSuccess && hipMemset(kv->d_len, 0, sb) == hipSuccess &&
        hipMemset(kv->d_rope, 0, sb) == hipSuccess && hipMemset(kv->d_act, 0, sb) == hipSuccess &&
+       hipMemset(kv->d_order, 0, sb) == hipSuccess &&
        hipMemset(kv->d_ready, 0, sb) == hipSuccess && hipMemset(kv->d_nblk, 0, sb) == hipSuccess;
   if (!ok) {
     hs_kv_free(kv);
@@ -1026,10 +1037,8 @@ int hs_kv_set_length(hs_kv *kv, int32_t req, int32_t len, int32_t rope_pos) {
   kv->len[req] = len;
   kv->rope[req] = rope_pos;
   kv->ready[req] = ready;
-  if (kv->pool) {
-    HIP_TRY(rebuild_active(kv, nullptr));
-    HIP_TRY(hipDeviceSynchronize());
-  }
+  HIP_TRY(kv->pool ? rebuild_active(kv, nullptr) : rebuild_order(kv, nullptr));
+  HIP_TRY(hipDeviceSynchronize());
   return HS_OK;
 }
 

@@ -42,7 +42,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   constexpr int TPW = 64 / LPT;           // positions per wave-wide load
   constexpr int STEP = NW * TPW;          // positions per work-group iteration
   constexpr int UB = attn_batch(G);       // iterations per batch of loads
-  const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
+  // decode: the longest requests' work groups are dispatched first
+  const int split = blockIdx.x, j = blockIdx.y, qi = a.order ? a.order[blockIdx.z] : (int)blockIdx.z;
   int req, L;
   if (!a.prefill) {
     req = PAGED ? a.kv.act[qi] : qi;
@@ -233,7 +234,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   constexpr int KK = HD / 32;         // 32-wide k steps of the scores
   constexpr int UB = ATTN_MMA_BATCH;  // tiles per batch of loads
   constexpr int STEP = NW * 16;       // positions per work-group iteration
-  const int split = blockIdx.x, j = blockIdx.y, qi = blockIdx.z;
+  // decode: the longest requests' work groups are dispatched first
+  const int split = blockIdx.x, j = blockIdx.y, qi = a.order ? a.order[blockIdx.z] : (int)blockIdx.z;
   int req, L;
   if (!a.prefill) {
     req = PAGED ? a.kv.act[qi] : qi;

@@ -118,6 +118,7 @@ struct AttnArgs {
   const PackedRows *pk;  // device copy; query row r of request i has length r - cu[i] + 1
   int prefill_tiles;     // prefill: query tiles in all (pk->tcu[pk->n])
   int S;           // positions per split (pooled caches: a multiple of 256)
+  const int *order;  // decode: work-group row z serves column order[z] (longest first); NULL: z
   int n_split;     // splits per (query, kv head)
   float *part_o;   // [nq][n_heads][n_split][head_dim]
   float *part_ml;  // [nq][n_heads][n_split][2]
@@ -177,6 +178,9 @@ struct KvReserve {
 hipError_t launch_kv_reserve(const KvPool &p, const KvReserve &r, int decode_n, hipStream_t st);
 // returns request req's blocks to the stack and empties it (length 0, not ready)
 hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st);
+// order = the n decode columns by decreasing length (ties: lower column
+// first); column c is request act[c] (act NULL: c)
+hipError_t launch_build_order(const int *len, const int *act, int n, int *order, hipStream_t st);
 // *p = v, in stream order
 hipError_t launch_set_int(int *p, int v, hipStream_t st);
 // act = the ready requests in order (n requests)
@@ -227,6 +231,7 @@ struct hs_kv {
   int64_t *d_base = nullptr;  // block table (contiguous: one block start per request)
   int *d_cap = nullptr, *d_len = nullptr, *d_rope = nullptr;
   int *d_toff = nullptr, *d_bt = nullptr, *d_act = nullptr, *d_ready = nullptr;
+  int *d_order = nullptr;  // decode columns, longest first
   int ntab = 0;
   int n_active = 0;  // decode columns
   // block pool (handles from hs_kv_pool_create)

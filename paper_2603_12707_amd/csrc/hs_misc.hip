@@ -234,6 +234,21 @@ __global__ __launch_bounds__(256) void k_kv_release(KvPool p, int req) {
   }
 }
 
+// Column c's rank is the number of columns ahead of it: longer, or as long
+// with a lower index.  n^2 comparisons in one work group (n <= a few
+// thousand, once per change of the batch).
+__global__ __launch_bounds__(256) void k_build_order(const int *len, const int *act, int n, int *order) {
+  for (int c = threadIdx.x; c < n; c += 256) {
+    const int lc = len[act ? act[c] : c];
+    int rank = 0;
+    for (int o = 0; o < n; ++o) {
+      const int lo = len[act ? act[o] : o];
+      rank += lo > lc || (lo == lc && o < c);
+    }
+    order[rank] = c;
+  }
+}
+
 __global__ void k_set_int(int *p, int v) {
   if (threadIdx.x == 0) *p = v;
 }
@@ -311,6 +326,12 @@ hipError_t launch_kv_reserve(const KvPool &p, const KvReserve &r, int decode_n, 
 
 hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st) {
   HS_LAUNCH(k_kv_release, dim3(1), dim3(256), 0, st, p, req);
+  return hipGetLastError();
+}
+
+hipError_t launch_build_order(const int *len, const int *act, int n, int *order, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  HS_LAUNCH(k_build_order, dim3(1), dim3(256), 0, st, len, act, n, order);
   return hipGetLastError();
 }
 
