@@ -189,6 +189,8 @@ struct Step {
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
+    g.splitk_ws = m->splitk;
+    g.splitk_cap = m->splitk_floats;
     return launch_gemm(c.dtype, PRO_NORM, kv->pool ? EPI_QKV_PAGED : EPI_QKV, g, st);
   }
 
@@ -554,7 +556,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
     if (ns > 1) entries = std::max(entries, (int64_t)nq * nh * ns);
   }
   m->part_entries = entries;
-  m->splitk_floats = (int64_t)SPLITK_MAX * max_batch * c.d_model;
+  m->splitk_floats = (int64_t)SPLITK_MAX * max_batch * std::max(c.d_model, (c.n_heads + 2 * c.n_kv_heads) * c.head_dim);
 
   struct Alloc {
     void **p;

@@ -55,6 +55,11 @@ __global__ __launch_bounds__(256) void k_pack(const void *src, void *dst, int64_
 // q/k/v: R consecutive tiles of the q, k, v matrices taken in turn (their
 // rows packed in head-paired order); SwiGLU pairs row j of the gate and of
 // the up projection; the other epilogues take R consecutive tiles.
+// rows of a K-split GEMM's partials: the residual rows, or q|k|v rows in turn
+__host__ __device__ inline int split_rows(const GemmArgs &a, int epi) {
+  return epi_qkv(epi) ? (a.n_heads + 2 * a.n_kv) * a.head_dim : a.rows[0];
+}
+
 template <int EPI, int R>
 __device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int *row0) {
   if constexpr (epi_qkv(EPI)) {
@@ -1015,6 +1020,18 @@ __global__ __launch_bounds__(64 * LG_NW) void k_gemm_lds(GemmArgs a) {
         const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
         gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
       }
+    } else if ((EPI == EPI_RESID || epi_qkv(EPI)) && nks > 1) {
+      // K split: this split's fp32 partial over the output rows (q/k/v:
+      // the q, k and v rows in turn), finished by a second kernel
+      const int prows = split_rows(a, EPI);
+      float *o = a.splitk_ws + ((int64_t)ks * a.ncols + col) * prows;
+#pragma unroll
+      for (int r = 0; r < RTW; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = 16 * (rg * RTG + wr * RTW + r) + rr + e;
+          if (row < prows) o[row] = acc[r][c][e];
+        }
     } else if constexpr (epi_qkv(EPI)) {
 #pragma unroll
       for (int r = 0; r < RTW; ++r) {
@@ -1023,21 +1040,42 @@ __global__ __launch_bounds__(64 * LG_NW) void k_gemm_lds(GemmArgs a) {
         qkv_fetch_tab<DT, 1>(a, &mat[r], &row0[r], rr, true, in);
         qkv_store<DT, 1, EPI == EPI_QKV_PAGED>(a, &mat[r], &row0[r], &acc[r][c], col, rr, in);
       }
-    } else if (EPI == EPI_RESID && nks > 1) {
-      // K split: this split's fp32 partial, summed into the residual later
-      float *o = a.splitk_ws + ((int64_t)ks * a.ncols + col) * a.rows[0];
-#pragma unroll
-      for (int r = 0; r < RTW; ++r)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int row = row0[r] + rr + e;
-          if (row < a.rows[0]) o[row] = acc[r][c][e];
-        }
     } else {
 #pragma unroll
       for (int r = 0; r < RTW; ++r) gemm_epilogue<DT, EPI, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr);
     }
   }
+}
+
+// The q/k/v epilogue after a K split: sums the partials of four q|k|v rows
+// of one column in split order, then bias, RoPE, R(q) and the K/V append as
+// in the GEMM's own epilogue.
+template <int DT, bool PAGED>
+__global__ __launch_bounds__(256) void k_qkv_split_epilogue(GemmArgs a) {
+  const int prows = split_rows(a, EPI_QKV), n4 = prows / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)a.ncols * n4) return;
+  const int col = (int)(i / n4), row = (int)(i % n4) * 4;
+  const int64_t slice = (int64_t)a.ncols * prows;
+  const float *part = a.splitk_ws + (int64_t)col * prows + row;
+  f32x4 v = *(const f32x4 *)part;
+  for (int k = 1; k < a.k_split; ++k) v += *(const f32x4 *)(part + k * slice);
+  // the row's matrix and tile, as the GEMM maps q|k|v row tiles
+  const int tq = a.n_heads * a.head_dim / 16, tk = a.n_kv * a.head_dim / 16;
+  int m = 0, t = row / 16;
+  if (t >= tq) {
+    t -= tq;
+    m = 1;
+    if (t >= tk) {
+      t -= tk;
+      m = 2;
+    }
+  }
+  const int r0 = 16 * t, rr = row % 16;
+  QkvIn<1> in;
+  qkv_fetch_ids<DT, 1, PAGED>(a, &m, &r0, col, rr, true, in);
+  qkv_fetch_tab<DT, 1>(a, &m, &r0, rr, true, in);
+  qkv_store<DT, 1, PAGED>(a, &m, &r0, &v, col, rr, in);
 }
 
 // x[col][row] += the K-split partials of (col, row), in split order; four
@@ -1130,9 +1168,14 @@ hipError_t gemm_lds_launch(const GemmArgs &a, int tiles16, int k_split, hipStrea
   HS_LAUNCH((k_gemm_lds<DT, EPI, RTG, CTG>), dim3(blocks), dim3(64 * LG_NW), 0, st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || k_split <= 1) return e;
-  const int64_t n = (int64_t)a.ncols * (a.rows[0] / 4);
-  HS_LAUNCH(k_splitk_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.splitk_ws, k_split, a.ncols,
-            a.rows[0], a.resid, a.ld_resid);
+  const int64_t n = (int64_t)a.ncols * (split_rows(a, EPI) / 4);
+  if constexpr (epi_qkv(EPI)) {
+    HS_LAUNCH((k_qkv_split_epilogue<DT, EPI == EPI_QKV_PAGED>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+              g);
+  } else {
+    HS_LAUNCH(k_splitk_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.splitk_ws, k_split, a.ncols,
+              a.rows[0], a.resid, a.ld_resid);
+  }
   return hipGetLastError();
 }
 
@@ -1147,14 +1190,15 @@ template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
   int ng, nc;
   const int blocks = lds_groups<EPI, 8, 8>(p, tiles16, 1, ng, nc);
-  if constexpr (EPI == EPI_RESID) {
+  if constexpr (EPI == EPI_RESID || epi_qkv(EPI)) {
     const int nkb = (p.K / Ty<DT>::CE + 15) / 16;
     int ks = blocks < SPLITK_BELOW ? std::min(std::min(SPLITK_MAX, (SPLITK_TARGET + blocks - 1) / blocks), nkb / 4) : 1;
     if (ks > 1) {
       const int per = (nkb + ks - 1) / ks;
       ks = (nkb + per - 1) / per;  // no empty split
     }
-    if (ks > 1 && p.splitk_ws && p.rows[0] % 4 == 0 && (int64_t)ks * p.ncols * p.rows[0] <= p.splitk_cap)
+    const int prows = split_rows(p, EPI);
+    if (ks > 1 && p.splitk_ws && prows % 4 == 0 && (int64_t)ks * p.ncols * prows <= p.splitk_cap)
       return gemm_lds_launch<DT, EPI, 8, 8>(p, tiles16, ks, st);
   }
   if (blocks >= LDS_MIN_GROUPS) return gemm_lds_launch<DT, EPI, 8, 8>(p, tiles16, 1, st);

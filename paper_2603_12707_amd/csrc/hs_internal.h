@@ -208,7 +208,7 @@ struct hs_model {
   void *attn = nullptr;     // [max_rows][n_h * d_h] attention output
   void *act = nullptr;      // [max_rows][F] SwiGLU output
   void *hnorm = nullptr;    // [max_rows][d] normalised rows for GEMMs over many columns
-  float *splitk = nullptr;  // [SPLITK_MAX][max_batch][d] residual GEMM partials
+  float *splitk = nullptr;  // [SPLITK_MAX][max_batch][max(d, q|k|v rows)] K-split GEMM partials
   int64_t splitk_floats = 0;
   float *xlast = nullptr;   // [PACK_MAX][d] last rows of the requests of a prefill pass
   hs::PackedRows *pk_dev = nullptr;  // the rows of the current prefill pass

@@ -194,6 +194,18 @@ def test_many_columns_split_k(dtype):
     assert near <= 2
 
 
+def test_many_columns_split_k_qkv():
+    """40 requests and K = 1024: the q/k/v GEMM (GQA-2, with bias) splits K
+    and a second kernel sums the partials before the bias, RoPE and the K/V
+    append."""
+    cfg = small_cfg(n_layers=1, d_model=1024, n_heads=8, n_kv_heads=4, head_dim=128, ffn_dim=1024, dtype="bf16",
+                    qkv_bias=1)
+    n_v = [(7 * b) % 19 for b in range(40)]
+    s_text = [1 + (5 * b) % 9 for b in range(40)]
+    near = _run_pair(cfg, n_v, s_text, 2)
+    assert near <= 2
+
+
 @pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
 def test_long_context_many_splits(n_v, dtype):
     """Contexts long enough for many attention splits in decode: at most 8
