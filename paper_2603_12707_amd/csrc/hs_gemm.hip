@@ -1179,16 +1179,21 @@ hipError_t gemm_lds_launch(const GemmArgs &a, int tiles16, int k_split, hipStrea
   return hipGetLastError();
 }
 
-// Many columns.  A residual GEMM with fewer than SPLITK_BELOW work groups
+// Many columns.  Where the work-group tile of 16 x 8 row x column tiles (wave
+// tiles of 4 x 4, half the LDS reads per MFMA) still gives LDS_BIG_GROUPS
+// work groups, it is taken (prefill gate/up at 640 rows: 159 against 191 us).
+// A GEMM (residual or q/k/v) with fewer than SPLITK_BELOW work groups
 // splits K (up to SPLITK_MAX ways, at least 4 k-blocks each) when the
 // partials fit the workspace.  Otherwise the LDS-staged kernel from
 // LDS_MIN_GROUPS work groups up, and below that the register-tiled kernel,
 // whose smaller work groups spread narrow matrices over more CUs (measured
 // crossover: between 64 and 80 work groups of the LDS kernel).
-constexpr int LDS_MIN_GROUPS = 72, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
+constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 384, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
 template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
   int ng, nc;
+  if (lds_groups<EPI, 16, 8>(p, tiles16, 1, ng, nc) >= LDS_BIG_GROUPS)
+    return gemm_lds_launch<DT, EPI, 16, 8>(p, tiles16, 1, st);
   const int blocks = lds_groups<EPI, 8, 8>(p, tiles16, 1, ng, nc);
   if constexpr (EPI == EPI_RESID || epi_qkv(EPI)) {
     const int nkb = (p.K / Ty<DT>::CE + 15) / 16;
