@@ -195,6 +195,31 @@ int hs_kv_admit(hs_kv *kv, int32_t slot, int32_t n_v, int32_t capacity, hs_strea
  * is empty again.  Stream-ordered: work queued before it on `stream` still
  * sees the blocks. */
 int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream);
+/* Aligned batch handoff (§5.2 "Aligned Batch Handoff"): requests whose
+ * projected embeddings have arrived wait in arrival order until a batch for
+ * hs_prefill_batch is due.  A batch is the longest arrival-order prefix of
+ * at most `align` requests (the paper's B_align, 32 by default) whose rows
+ * fit max_rows (0: no budget; one request always fits).  It is due when it
+ * holds `align` requests, when the row budget closes it with more requests
+ * waiting, or when its oldest request has waited timeout_ms (the paper's
+ * 500 ms) -- so an under-filled batch still goes.  Times are the caller's
+ * clock in milliseconds, non-decreasing across pushes.  Host only; not
+ * thread-safe.  max_pending (>= align) bounds the queue: a push beyond it
+ * fails with HS_E_CAPACITY. */
+typedef struct hs_handoff hs_handoff;
+int hs_handoff_create(int32_t align, int64_t max_rows, int32_t max_pending, double timeout_ms, hs_handoff **out);
+int hs_handoff_free(hs_handoff *h);
+/* request `req` (>= 0), with `rows` context rows to prefill, arrived at now_ms */
+int hs_handoff_push(hs_handoff *h, int32_t req, int32_t rows, double now_ms);
+/* If a batch is due at now_ms, moves its requests (in arrival order) to
+ * reqs[0 .. *n) (room for max; HS_E_BUFFER if too small) and their row sum
+ * to *rows; else *n = 0.  *wait_ms (may be NULL) gets the time until the
+ * oldest waiting request times out (0 when due again at once, -1 when none
+ * waits). */
+int hs_handoff_pop(hs_handoff *h, double now_ms, int32_t *reqs, int32_t max, int32_t *n, int64_t *rows,
+                   double *wait_ms);
+int hs_handoff_pending(const hs_handoff *h, int32_t *n);
+
 /* Free and total blocks of a pooled cache (host mirror; exact after
  * hs_kv_sync when graph replays have taken blocks). */
 int hs_kv_pool_blocks(const hs_kv *kv, int32_t *free_blocks, int32_t *n_blocks);

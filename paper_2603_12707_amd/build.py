@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhs.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("hs_api.cpp", "hs_gemm.hip", "hs_attn.hip", "hs_misc.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("hs_api.cpp", "hs_gemm.hip", "hs_attn.hip", "hs_misc.hip", "hs_handoff.cpp")]
 DEPS = SOURCES + [os.path.join(CSRC, "hs_internal.h"), os.path.join(CSRC, "hs_device.h"),
                   os.path.join(ROOT, "include", "hs.h")]
 

@@ -9,9 +9,7 @@
 
 #include "hs_internal.h"
 
-using namespace hs;
-
-namespace {
+namespace hs {
 
 thread_local std::string g_err;
 
@@ -24,6 +22,12 @@ int fail(int code, const char *fmt, ...) {
   g_err = buf;
   return code;
 }
+
+}  // namespace hs
+
+using namespace hs;
+
+namespace {
 
 #define HIP_TRY(expr)                                                                      \
   do {                                                                                     \

@@ -192,6 +192,9 @@ hipError_t launch_gather_last(const float *x, int d, const PackedRows &pk, float
 
 bool attn_supported(int dtype, int head_dim, int group);
 
+// records the thread's error message (hs_last_error) and returns code
+int fail(int code, const char *fmt, ...);
+
 }  // namespace hs
 
 struct hs_model {

@@ -22,7 +22,8 @@ EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "
            "hs_prefill_embeddings", "hs_decode_step", "hs_model_status", "hs_kv_lengths", "hs_kv_write",
            "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync",
            "hs_prefill_batch", "hs_model_reserve_rows", "hs_kv_pool_create", "hs_kv_admit", "hs_kv_release",
-           "hs_kv_pool_blocks")
+           "hs_kv_pool_blocks", "hs_handoff_create", "hs_handoff_free", "hs_handoff_push", "hs_handoff_pop",
+           "hs_handoff_pending")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -86,6 +87,12 @@ def lib() -> ctypes.CDLL:
         "hs_kv_admit": [P, I32, I32, I32, P],
         "hs_kv_release": [P, I32, P],
         "hs_kv_pool_blocks": [P, ctypes.POINTER(I32), ctypes.POINTER(I32)],
+        "hs_handoff_create": [I32, I64, I32, ctypes.c_double, ctypes.POINTER(P)],
+        "hs_handoff_free": [P],
+        "hs_handoff_push": [P, I32, I32, ctypes.c_double],
+        "hs_handoff_pop": [P, ctypes.c_double, P, I32, ctypes.POINTER(I32), ctypes.POINTER(I64),
+                           ctypes.POINTER(ctypes.c_double)],
+        "hs_handoff_pending": [P, ctypes.POINTER(I32)],
         "hs_decode_step": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
@@ -362,3 +369,42 @@ class KVPool(KVCache):
         f, n = ctypes.c_int32(), ctypes.c_int32()
         _call("hs_kv_pool_blocks", self.handle, ctypes.byref(f), ctypes.byref(n))
         return f.value, n.value
+
+
+class Handoff:
+    """Aligned batch handoff: requests whose embeddings have arrived wait in
+    arrival order until a batch of `align` requests (or the row budget, or
+    the oldest request's timeout) is due for prefill."""
+
+    def __init__(self, align: int = 32, max_rows: int = 0, max_pending: int = 4096, timeout_ms: float = 500.0):
+        self.align = align
+        h = ctypes.c_void_p()
+        _call("hs_handoff_create", align, max_rows, max_pending, timeout_ms, ctypes.byref(h))
+        self.handle = h
+
+    def push(self, req: int, rows: int, now_ms: float) -> None:
+        _call("hs_handoff_push", self.handle, req, rows, now_ms)
+
+    def pop(self, now_ms: float):
+        """(requests of the due batch or [], their rows, ms until the next timeout or -1)."""
+        out = (ctypes.c_int32 * self.align)()
+        n, rows, wait = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_double()
+        _call("hs_handoff_pop", self.handle, now_ms, out, self.align, ctypes.byref(n), ctypes.byref(rows),
+              ctypes.byref(wait))
+        return list(out[:n.value]), rows.value, wait.value
+
+    def pending(self) -> int:
+        n = ctypes.c_int32()
+        _call("hs_handoff_pending", self.handle, ctypes.byref(n))
+        return n.value
+
+    def close(self) -> None:
+        if self.handle:
+            _call("hs_handoff_free", self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

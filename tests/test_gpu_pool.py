@@ -282,3 +282,49 @@ def test_pool_capacity_and_admission_errors():
     pool.decode(tin, tout)                            # request 0 alone takes the free block
     assert pool.lengths() == [513, 0, 0] and pool.blocks() == (0, 3)
     assert pair.gpu.status() == 0
+
+
+def test_serving_loop_handoff_pool_continuous_batching():
+    """A small serving loop: ten requests arrive over time; the aligned batch
+    handoff (B_align = 4, 100 ms timeout) releases them in batches; each
+    batch is admitted into free slots of a pool and prefilled in one packed
+    call; decode steps run over every live slot, and finished requests leave
+    and free their slots for later ones.  Every prefill and step is checked
+    against the oracle."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=2, dtype="bf16")
+    run = PoolRun(cfg, slots=6, n_blocks=12)  # six live requests of at most 2 blocks each
+    rng = np.random.default_rng(7)
+    reqs = [dict(n_v=int(rng.integers(0, 200)), s_text=int(rng.integers(1, 90)), n_dec=int(rng.integers(2, 6)),
+                 t=float(10 * i + rng.integers(0, 15))) for i in range(10)]
+    handoff = hs.Handoff(align=4, timeout_ms=100.0)
+    slot_of, left, waiting, arrived, done = {}, {}, [], 0, 0
+    now = 0.0
+    while done < len(reqs):
+        while arrived < len(reqs) and reqs[arrived]["t"] <= now:
+            r = reqs[arrived]
+            handoff.push(arrived, r["n_v"] + r["s_text"], now_ms=now)
+            arrived += 1
+        batch, _, _ = handoff.pop(now)
+        waiting += batch
+        free = [s for s in range(run.slots) if s not in run.seqs]
+        admit = []
+        while waiting and free:
+            q, s = waiting.pop(0), free.pop(0)
+            r = reqs[q]
+            slot_of[s], left[s] = q, r["n_dec"]
+            admit.append((s, r["n_v"], r["s_text"], r["n_v"] + r["s_text"] + r["n_dec"] + 1))
+        if admit:
+            run.admit_and_prefill(admit, key=1000 + int(now))
+        if run.seqs:
+            run.decode(1)
+            for s in list(run.seqs):
+                left[s] -= 1
+                if left[s] == 0:
+                    run.release(s)
+                    done += 1
+        now += 10.0
+    assert handoff.pending() == 0 and not waiting
+    assert run.pool.blocks() == (12, 12) and run.pool.lengths() == [0] * 6
+    assert run.pair.gpu.status() == 0
+    assert run.near <= 2
