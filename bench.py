@@ -105,6 +105,7 @@ def stored_traffic(workload: str, kernel: str):
 
 DEFAULT_WARMUP, DEFAULT_STEPS = 8, 120
 PREFILL_ROWS = 16384  # packed prefill rows per pass at batch > 1
+STREAM_READ_BYTES, STREAM_READ_BLOCKS = 4 << 30, (1024, 2048, 4096)
 
 
 def steps_after_context(warmup: int, steps: int) -> int:
@@ -222,13 +223,14 @@ def main() -> int:
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one MI355X: this build has no multi-GPU path (the decode step is sharded "
-              "by request across GPUs with no exchange; see the design notes). Run with --gpus 1.",
+        print("bench.py measures one MI355X: the library has no multi-GPU path (the decode step would be "
+              "sharded by request across GPUs with no exchange). Run with --gpus 1.",
               file=sys.stderr)
         return 2
 
     import torch
 
+    import paper_2603_12707_amd as hs
     from workload import configs
     cfg = configs.get(args.workload)
     B = cfg["batch"]
@@ -308,6 +310,21 @@ def main() -> int:
     torch.cuda.synchronize()
     dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
 
+    # the plain streaming-read rate of this GPU (the same loads as the weight
+    # stream), for reading roofline.frac against what HBM delivers
+    sr_buf = torch.empty(STREAM_READ_BYTES, dtype=torch.uint8, device="cuda")
+    sr_sink = torch.empty(max(STREAM_READ_BLOCKS), dtype=torch.int32, device="cuda")
+    stream_read_gbs = 0.0
+    for blocks in STREAM_READ_BLOCKS:  # the best grid
+        hs.stream_read(sr_buf, sr_sink, blocks)  # warm
+        ev0.record()
+        for _ in range(5):
+            hs.stream_read(sr_buf, sr_sink, blocks)
+        ev1.record()
+        torch.cuda.synchronize()
+        stream_read_gbs = max(stream_read_gbs, 5 * STREAM_READ_BYTES / (ev0.elapsed_time(ev1) / 1e3) / 1e9)
+    del sr_buf, sr_sink
+
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -328,7 +345,8 @@ def main() -> int:
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": KIND_NAMES[dominant], "kind": dominant,
-                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps}
+                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps,
+                "stream_read_gbps": round(stream_read_gbs, 1), "frac_of_stream_read": round(achieved / stream_read_gbs, 4)}
     kernels = {k: round(v, 2) for k, v in breakdown.items()}
 
     out = {

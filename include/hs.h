@@ -195,6 +195,13 @@ int hs_kv_admit(hs_kv *kv, int32_t slot, int32_t n_v, int32_t capacity, hs_strea
  * is empty again.  Stream-ordered: work queued before it on `stream` still
  * sees the blocks. */
 int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream);
+/* Measurement: reads `bytes` (a positive multiple of 16) of device memory at
+ * buf (16-byte aligned) with the same 16-byte non-temporal loads the kernels
+ * stream weights with, writing one word per work group to sink (device,
+ * [blocks]) so the reads cannot be skipped.  The plain HBM read rate that the
+ * kernels' own rates are compared with. */
+int hs_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int32_t blocks, hs_stream_t stream);
+
 /* Aligned batch handoff (§5.2 "Aligned Batch Handoff"): requests whose
  * projected embeddings have arrived wait in arrival order until a batch for
  * hs_prefill_batch is due.  A batch is the longest arrival-order prefix of

@@ -811,6 +811,13 @@ int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream) {
   return HS_OK;
 }
 
+int hs_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int32_t blocks, hs_stream_t stream) {
+  if (!buf || !sink || blocks <= 0 || bytes == 0 || bytes % 16 || ((uintptr_t)buf) % 16)
+    return fail(HS_E_INVALID, "hs_stream_read: bad argument");
+  HIP_TRY(launch_stream_read(buf, bytes, sink, blocks, (hipStream_t)stream));
+  return HS_OK;
+}
+
 int hs_kv_pool_blocks(const hs_kv *kv, int32_t *free_blocks, int32_t *n_blocks) {
   if (!kv || !kv->pool) return fail(HS_E_INVALID, "hs_kv_pool_blocks: not a pooled cache");
   if (free_blocks) *free_blocks = kv->free_blocks;

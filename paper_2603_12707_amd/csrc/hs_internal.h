@@ -181,6 +181,8 @@ hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st);
 // order = the n decode columns by decreasing length (ties: lower column
 // first); column c is request act[c] (act NULL: c)
 hipError_t launch_build_order(const int *len, const int *act, int n, int *order, hipStream_t st);
+// reads bytes (a multiple of 16) from buf; one word per work group to sink[blocks]
+hipError_t launch_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int blocks, hipStream_t st);
 // *p = v, in stream order
 hipError_t launch_set_int(int *p, int v, hipStream_t st);
 // act = the ready requests in order (n requests)

@@ -249,6 +249,29 @@ __global__ __launch_bounds__(256) void k_build_order(const int *len, const int *
   }
 }
 
+// A plain streaming read (the HBM read rate the kernels are measured
+// against): grid-strided 16-byte non-temporal loads, eight in flight per
+// thread, folded into one word per work group so that nothing is skipped.
+__global__ __launch_bounds__(256) void k_stream_read(const u32x4 *p, int64_t n16, uint32_t *sink) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  u32x4 acc = u32x4{0u, 0u, 0u, 0u};
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ld16_stream(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u];
+  }
+  for (; i < n16; i += stride) acc ^= ld16_stream(p + i);
+  uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+  for (int off = 32; off >= 1; off >>= 1) x ^= __shfl_xor(x, off);
+  __shared__ uint32_t s_x[4];
+  if ((threadIdx.x & 63) == 0) s_x[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = s_x[0] ^ s_x[1] ^ s_x[2] ^ s_x[3];
+}
+
 __global__ void k_set_int(int *p, int v) {
   if (threadIdx.x == 0) *p = v;
 }
@@ -332,6 +355,11 @@ hipError_t launch_kv_release(const KvPool &p, int req, hipStream_t st) {
 hipError_t launch_build_order(const int *len, const int *act, int n, int *order, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   HS_LAUNCH(k_build_order, dim3(1), dim3(256), 0, st, len, act, n, order);
+  return hipGetLastError();
+}
+
+hipError_t launch_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int blocks, hipStream_t st) {
+  HS_LAUNCH(k_stream_read, dim3(blocks), dim3(256), 0, st, (const u32x4 *)buf, (int64_t)(bytes / 16), sink);
   return hipGetLastError();
 }
 

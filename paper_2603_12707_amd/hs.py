@@ -23,7 +23,7 @@ EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "
            "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync",
            "hs_prefill_batch", "hs_model_reserve_rows", "hs_kv_pool_create", "hs_kv_admit", "hs_kv_release",
            "hs_kv_pool_blocks", "hs_handoff_create", "hs_handoff_free", "hs_handoff_push", "hs_handoff_pop",
-           "hs_handoff_pending")
+           "hs_handoff_pending", "hs_stream_read")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -93,6 +93,7 @@ def lib() -> ctypes.CDLL:
         "hs_handoff_pop": [P, ctypes.c_double, P, I32, ctypes.POINTER(I32), ctypes.POINTER(I64),
                            ctypes.POINTER(ctypes.c_double)],
         "hs_handoff_pending": [P, ctypes.POINTER(I32)],
+        "hs_stream_read": [P, U64, P, I32, P],
         "hs_decode_step": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
@@ -142,6 +143,11 @@ def hs_kv_bytes(cfg: dict, n_v: int, s_text: int) -> tuple:
 
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def stream_read(buf, sink, blocks: int) -> None:
+    """Plain streaming read of a device tensor (measurement)."""
+    _call("hs_stream_read", _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), blocks, _stream())
 
 
 def _stream():
