@@ -32,7 +32,10 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
 // partial o, its max m and its sum l, a split past the query's positions
 // writing the neutral (o = 0, m = -inf, l = 0).
 // K/V are read through buffer ranges that end at the split's last position,
-// so that no load sits behind a branch.
+// so that no load sits behind a branch.  In a cache of several blocks per
+// request (PAGED) a batch of loads always lies in one block and gets a range
+// of its own, the block's start read one batch ahead.  In decode, work-group
+// row z serves the z-th longest request (a.order).
 template <int DT, int HD, int G, int NW, bool PAGED>
 __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   using S = typename Ty<DT>::S;

@@ -176,16 +176,6 @@ __device__ __forceinline__ u32x2 bld8(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
-// First element of the K (s = 0) or V (s = 1) rows of request req, layer,
-// KV head j, from position t on; the rows are contiguous up to the end of the
-// block holding t.  -1 when that block is not allocated.
-__device__ __forceinline__ int64_t kv_rows(const KvRef &kv, int req, int layer, int s, int n_kv, int j, int t,
-                                           int hd) {
-  const int bt = kv.bt[req];
-  const int64_t b = kv.tab[kv.toff[req] + t / bt];
-  return b < 0 ? -1 : b + ((int64_t)((layer * 2 + s) * n_kv + j) * bt + t % bt) * hd;
-}
-
 // request (index into pk) of packed prefill row `row`
 __device__ __forceinline__ int packed_request(const PackedRows *pk, int row) {
   int i = 0;
