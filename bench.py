@@ -24,6 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E
+WEIGHT_COPIES = 4  # one-layer workloads: weight sets rotated over the steps (4 x 0.47 GB > 256 MB Infinity Cache)
 METRIC = "decode tokens/s at batch B + achieved HBM GB/s vs peak, 7B-shaped fp16"
 
 
@@ -121,14 +122,20 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
     from workload import synth
     B = cfg["batch"]
     t = time.time()
-    w = {}
-    for name in synth.weight_names(cfg):  # generate and pack one matrix at a time
-        t_row = synth.make_weight(cfg, name, device="cuda")
-        w[name] = hs.pack_weight(cfg, name, t_row)
-        del t_row
+    # a one-layer workload rotates copies of its weights, so that the 256 MB
+    # Infinity Cache cannot serve one step's weights to the next
+    copies = WEIGHT_COPIES if "kv_len" in cfg else 1
+    ws = []
+    for k in range(copies):
+        w = {}
+        for name in synth.weight_names(cfg):  # generate and pack one matrix at a time
+            t_row = synth.make_weight(cfg, name, device="cuda", seed=None if k == 0 else cfg["seed"] + 7919 * k)
+            w[name] = hs.pack_weight(cfg, name, t_row)
+            del t_row
+        ws.append(w)
     torch.cuda.synchronize()
-    log(f"weights generated and packed in HBM: {sum(v.numel() * v.element_size() for v in w.values()) / 1e9:.2f} GB "
-        f"in {time.time() - t:.1f} s")
+    log(f"weights generated and packed in HBM: {copies} x "
+        f"{sum(v.numel() * v.element_size() for v in ws[0].values()) / 1e9:.2f} GB in {time.time() - t:.1f} s")
     if "kv_len" in cfg:  # layer stack fed from a synthetic cache
         lens = synth.kv_lengths(cfg)
         n_v = [0] * B
@@ -136,7 +143,8 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
         n_v, s_text = synth.request_lengths(cfg)
         lens = [a + b for a, b in zip(n_v, s_text)]
     caps = [n + n_steps_total for n in lens]
-    model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True)
+    models = [hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True) for w in ws]
+    model = models[0]
     if pool_block:  # block-granular cache: one slot per request, admitted up front
         n_blocks = sum((c + pool_block - 1) // pool_block for c in caps)
         kv = hs.KVPool(model, B, pool_block, n_blocks)
@@ -174,7 +182,7 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
     ready_s = time.time() - t
     log(f"context ready for {B} request(s) in {ready_s * 1e3:.1f} ms (lengths {min(lens)}..{max(lens)})")
     setup.prefill_ms = None if "kv_len" in cfg else ready_s * 1e3 / B
-    return w, model, kv, first, lens
+    return ws, models, kv, first, lens
 
 
 def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
@@ -235,17 +243,22 @@ def main() -> int:
     cfg = configs.get(args.workload)
     B = cfg["batch"]
     torch.cuda.set_device(0)
-    graph_steps = 2 * (max(1, args.steps // 4) + 1) if args.graph else 0
-    w, model, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps,
+    copies = WEIGHT_COPIES if "kv_len" in cfg else 1
+    per_graph = max(2, copies)  # decode steps captured in one graph: the token ping-pong and the weight rotation
+    graph_steps = per_graph * (max(1, args.steps // 4) + 1) if args.graph else 0
+    ws, models, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps,
                                        args.kv_pool_block)
 
     tin = first.clone()
     tout = torch.empty_like(tin)
     has_head = cfg.get("lm_head", True)
 
+    n_step = 0
+
     def step():
-        nonlocal tin, tout
-        kv.decode(tin, tout if has_head else None)
+        nonlocal tin, tout, n_step
+        kv.decode(tin, tout if has_head else None, model=models[n_step % len(models)])
+        n_step += 1
         if has_head:
             tin, tout = tout, tin
 
@@ -263,12 +276,14 @@ def main() -> int:
 
     graph_ms = None
     if args.graph:
-        # two steps per graph (the token buffers ping-pong), replayed back to back
+        # per_graph steps per graph (token buffers ping-pong, weight sets
+        # rotate), graphs replayed back to back
         ga, gb = tin.clone(), torch.empty_like(tin)
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            kv.decode(ga, gb if has_head else None)
-            kv.decode(gb if has_head else ga, ga if has_head else None)
+            for k in range(per_graph):
+                a, b = (ga, gb) if k % 2 == 0 else (gb, ga)
+                kv.decode(a, b if has_head else None, model=models[k % len(models)])
         kv.sync()
         reps_g = max(1, args.steps // 4)
         graph.replay()  # warm
@@ -277,13 +292,19 @@ def main() -> int:
         for _ in range(reps_g):
             graph.replay()
         torch.cuda.synchronize()
-        graph_ms = (time.perf_counter() - t0) / (2 * reps_g) * 1e3
+        graph_ms = (time.perf_counter() - t0) / (per_graph * reps_g) * 1e3
         kv.sync()
-        lens_after = [n - 2 * (reps_g + 1) for n in kv.lengths()]
+        lens_after = [n - per_graph * (reps_g + 1) for n in kv.lengths()]
 
     # per-kernel breakdown, the same way for every replayable kind: each
-    # layer's launch replayed once, HIP events around the batch on the stream
-    # the library launches on (torch's current stream)
+    # layer's launch replayed once per weight copy, HIP events around the
+    # batch on the stream the library launches on (torch's current stream)
+    def replay_all(kind, passes):
+        for _ in range(passes):
+            for m in models:
+                kv.replay(kind, cfg["n_layers"], model=m)
+    launches = cfg["n_layers"] * len(models)
+
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     breakdown = {}
     for kind in ("qkv", "attn", "combine", "oproj", "gateup", "down", "head"):
@@ -292,20 +313,20 @@ def main() -> int:
         except Exception:  # combine: single split; head: no LM head
             continue
         ev0.record()
-        kv.replay(kind, cfg["n_layers"])
+        replay_all(kind, 1)
         ev1.record()
         torch.cuda.synchronize()
-        breakdown[kind] = ev0.elapsed_time(ev1) / cfg["n_layers"] * 1e3  # us per launch
+        breakdown[kind] = ev0.elapsed_time(ev1) / launches * 1e3  # us per launch
 
     # dominant kernel: the kind with the most time per step, replayed back
-    # to back over every layer's weights (4 passes)
+    # to back over every layer's weights (4 passes over each copy)
     per_step = {k: v * (1 if k == "head" else cfg["n_layers"]) for k, v in breakdown.items() if k in KIND_NAMES}
     dominant = max(per_step, key=per_step.get)
     lens_replay = kv.lengths()
-    reps = 4 * cfg["n_layers"]
-    kv.replay(dominant, cfg["n_layers"])  # warm
+    reps = 4 * launches
+    replay_all(dominant, 1)  # warm
     ev0.record()
-    kv.replay(dominant, reps)
+    replay_all(dominant, 4)
     ev1.record()
     torch.cuda.synchronize()
     dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
@@ -366,7 +387,8 @@ def main() -> int:
                    [min(lens_start), max(lens_start)], "n_layers": cfg["n_layers"], "d_model": cfg["d_model"],
                    "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"], "ffn_dim": cfg["ffn_dim"],
                    "vocab": cfg["vocab"] if has_head else None, "parallelism": "none (one GPU)",
-                   "kv_cache": f"pool of {args.kv_pool_block}-position blocks" if args.kv_pool_block else "contiguous"},
+                   "kv_cache": f"pool of {args.kv_pool_block}-position blocks" if args.kv_pool_block else "contiguous",
+                   "weight_copies": copies},
         "hbm_gbps": round(gbs, 1),
         "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
         "bytes_per_step": total_bytes // args.steps,
@@ -379,7 +401,7 @@ def main() -> int:
         out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
                         "note": "the same step replayed from a HIP graph (stream capture)"}
     if not args.no_cpu_baseline:
-        del w
+        del ws, models
         out["cpu_baseline"] = cpu_baseline(cfg, lens_start[0])
     print(json.dumps(out), flush=True)
     return 0

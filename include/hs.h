@@ -15,6 +15,9 @@
  *     the KV cache once per generated token (§2; Eq. 5, §4.3).
  *
  * Conventions
+ *   - A KV handle serves any model created with the same hs_config whose
+ *     max_ctx covers the handle's capacities (for instance copies of the
+ *     weights); calls that take both reject any other (HS_E_INVALID).
  *   - Every call returns an int status: HS_OK (0) or a negative HS_E_* code;
  *     hs_last_error() returns a thread-local message for the last failure.
  *   - Device pointers are HIP device addresses on the device that was current

@@ -94,6 +94,13 @@ int64_t kv_request_elems(const hs_config &c, int cap) {
   return 2ll * c.n_layers * c.n_kv_heads * (int64_t)c.head_dim * cap;
 }
 
+// A handle works with any model of the same configuration whose max_ctx
+// covers its capacities (each model brings its own weights and workspaces),
+// e.g. several copies of the weights.
+bool kv_matches(const hs_kv *kv, const hs_model *m) {
+  return kv && m && kv->m && std::memcmp(&kv->m->cfg, &m->cfg, sizeof(hs_config)) == 0 && kv->max_cap <= m->max_ctx;
+}
+
 KvRef kv_ref(const hs_kv *kv) {
   return KvRef{kv->buf,   kv->d_base, kv->d_toff, kv->d_bt,  kv->d_cap,
                kv->d_len, kv->d_act,  kv->batch,  kv->ntab, kv->pool ? 1 : 0};
@@ -355,7 +362,7 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out, int *blo
 int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const void *emb, const int32_t *text_ids,
                      const int32_t *s_text, const int32_t *pos_thw, float *last_logits, int32_t *first_tokens,
                      hs_stream_t stream, const char *fn) {
-  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "%s: model/handle mismatch", fn);
+  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "%s: model/handle mismatch", fn);
   if (!m->w.lm_head) return fail(HS_E_STATE, "%s: model has no LM head", fn);
   if (!first_tokens) return fail(HS_E_INVALID, "%s: first_token is NULL", fn);
   if (n <= 0 || n > kv->batch || !reqs || !s_text) return fail(HS_E_INVALID, "%s: bad request list", fn);
@@ -870,7 +877,7 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows) {
 
 int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
                    float *hidden_out, hs_stream_t stream) {
-  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_decode_step: model/handle mismatch");
+  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "hs_decode_step: model/handle mismatch");
   if (!tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_in is NULL");
   const hs_config &c = m->cfg;
   if (m->w.lm_head) {
@@ -912,7 +919,7 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
 }
 
 int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_stream_t stream) {
-  if (!m || !kv || kv->m != m) return fail(HS_E_INVALID, "hs_replay_kernels: model/handle mismatch");
+  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "hs_replay_kernels: model/handle mismatch");
   if (count < 0) return fail(HS_E_INVALID, "hs_replay_kernels: negative count");
   hipStream_t st = (hipStream_t)stream;
   Step step;

@@ -305,9 +305,10 @@ class KVCache:
               _ptr(last_logits), _ptr(first_tokens), _stream())
         return first_tokens
 
-    def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None) -> None:
-        _call("hs_decode_step", self.model.handle, self.handle, _ptr(tokens_in), _ptr(tokens_out), _ptr(logits),
-              _ptr(hidden_out), _stream())
+    def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None, model=None) -> None:
+        """One greedy step; `model` (default: the handle's) may be any model of the same configuration."""
+        _call("hs_decode_step", (model or self.model).handle, self.handle, _ptr(tokens_in), _ptr(tokens_out),
+              _ptr(logits), _ptr(hidden_out), _stream())
 
     def sync(self) -> None:
         """Host mirrors of the lengths from the device (after graph replays)."""
@@ -325,9 +326,9 @@ class KVCache:
     def read(self, req: int, layer: int, kv_sel: int, head: int, pos0: int, n: int, out) -> None:
         _call("hs_kv_read", self.handle, req, layer, kv_sel, head, pos0, n, _ptr(out), int(out.is_cuda))
 
-    def replay(self, kind: str, count: int) -> None:
+    def replay(self, kind: str, count: int, model: "Model | None" = None) -> None:
         """Launches `count` kernels of one kind back to back (measurement)."""
-        _call("hs_replay_kernels", self.model.handle, self.handle, HS_K_NAMES.index(kind), count, _stream())
+        _call("hs_replay_kernels", (model or self.model).handle, self.handle, HS_K_NAMES.index(kind), count, _stream())
 
     def set_length(self, req: int, length: int, rope_pos: int) -> None:
         _call("hs_kv_set_length", self.handle, req, length, rope_pos)
