@@ -1094,6 +1094,195 @@ __global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int k_spl
 }
 
 // ---------------------------------------------------------------------------
+// weight-stationary GEMM for a few hundred columns
+// ---------------------------------------------------------------------------
+// At 129..256 columns (decode at a large batch) every weight row meets all
+// columns, so a wave that owns WS_RT row tiles of a work unit takes their
+// weights straight from memory into registers (a ring WS_DEPTH stages deep,
+// non-temporal loads) and never shares them: only the activations go through
+// LDS.  A work group = WS_NWC consumer waves (one task of WS_RT row tiles x
+// WS_CT column tiles each) + WS_NP producer waves that stage the activations
+// of each 64-element K stage into a double buffer.  Consumers read each
+// activation sub-block from LDS a few ahead of its MFMAs (scheduling groups
+// keep the reads WS_PF operands ahead) and meet the producers at one barrier
+// per stage.  The grid is one work group per CU looping over work units
+// (row-task group, column group); the column groups of one row group land on
+// the same XCD, where the later ones read the weights from L2.  Taken for the
+// tall matrices that need no K split, gate/up and the LM head: at the
+// batch-256 Qwen-shaped layer gate/up takes 100-107 us against 146 for the
+// LDS-staged kernel.  The short ones (q/k/v, O, down) measured slower here
+// even split into 4-8 K ranges (O 47-55 us against 33, down 89 against 73):
+// each wave waits for its own weights once per stage, so with few work units
+// the latency of the weight stream is exposed.
+constexpr int WS_RT = 4, WS_CT = 8, WS_NWC = 6, WS_NP = 2, WS_DEPTH = 2, WS_PF = 3, WS_GRID = 256;
+constexpr int WS_MIN_COLS = 129, WS_MAX_COLS = 256;
+
+// one work-group barrier with the LDS writes before it complete; the global
+// loads in flight are not waited for (unlike __syncthreads)
+__device__ __forceinline__ void ws_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// row tile r of task t -> matrix and first row (SwiGLU: WS_RT/2 gate tiles,
+// then the matching up tiles)
+template <int EPI>
+__device__ __forceinline__ void ws_tile(int t, int r, int &m, int &r0) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    constexpr int H = WS_RT / 2;
+    m = r < H ? 0 : 1;
+    r0 = 16 * (t * H + r % H);
+  } else {
+    m = 0;
+    r0 = 16 * (t * WS_RT + r);
+  }
+}
+
+template <int DT, int EPI>
+__global__ __launch_bounds__(64 * (WS_NWC + WS_NP)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_gemm_ws(GemmArgs a) {
+  using S = typename Ty<DT>::S;
+  constexpr int CE = Ty<DT>::CE;
+  constexpr int SB = (int)sizeof(S);
+  constexpr int RT = WS_RT, CT = WS_CT, NWC = WS_NWC, NP = WS_NP, DEPTH = WS_DEPTH, PF = WS_PF;
+  constexpr int XE = 2 * CT, XPT = XE / NP, NB = 2 * CT;
+  constexpr int UNR = DEPTH % 2 == 0 ? DEPTH : 2 * DEPTH;  // stages per unrolled round
+  static_assert(XE % NP == 0 && PF <= NB, "stage split");
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_STORE, "tall matrices without a K split");
+  __shared__ __align__(16) u32x4 s_x[2][XE * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int li = lane & 15, lq = lane >> 4;
+  const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4, nsb = nkb * 4;
+  const int per_task = EPI == EPI_SWIGLU ? RT / 2 : RT;
+  const int n_task = ((a.rows[0] + 15) / 16 + per_task - 1) / per_task;
+  const int n_rg = (n_task + NWC - 1) / NWC, n_rg8 = (n_rg + 7) / 8 * 8;
+  const int n_cg = (a.ncols + 16 * CT - 1) / (16 * CT);
+  const int n_units = n_rg8 * n_cg;
+  const rsrc_t xres = make_rsrc(a.x, (uint32_t)a.ncols * K * SB);
+  const int g_begin = 0, g_end = nsb, nstage = (nsb + 1) / 2;
+  for (int unit = blockIdx.x; unit < n_units; unit += gridDim.x) {
+    // unit = ((row group / 8) * n_cg + column group) * 8 + row group % 8
+    const int lo = unit & 7, v = unit >> 3;
+    const int cg = v % n_cg, rg = (v / n_cg) * 8 + lo;
+    if (rg >= n_rg) continue;
+    const int cnt = min(NWC, n_task - rg * NWC);
+    const int colg0 = cg * CT * 16;
+    if (wave >= NWC) {
+      // producer: activation sub-block e = sub * CT + column tile of each stage
+      const int pw = wave - NWC;
+      u32x4 xr[XPT];
+      auto xload = [&](int st) {
+#pragma unroll
+        for (int i = 0; i < XPT; ++i) {
+          const int e = pw + NP * i, sub = e / CT, ct = e % CT, g = g_begin + st * 2 + sub;
+          const int col = colg0 + ct * 16 + li, kc = g * 4 + lq;
+          xr[i] = bld16(xres, g < g_end && col < a.ncols && kc < kchunks ? (uint32_t)(col * K + kc * CE) * SB : BUF_OOB);
+        }
+      };
+      auto xstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < XPT; ++i) s_x[buf][(pw + NP * i) * 64 + lane] = xr[i];
+      };
+      xload(0);
+      xstore(0);
+      xload(1);
+      for (int st0 = 0; st0 < nstage; st0 += 2) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          if (st0 + h < nstage) {
+            ws_barrier();
+            xstore(h ^ 1);
+            xload(st0 + h + 2);
+          }
+        }
+      }
+      ws_barrier();
+    } else if (wave < cnt) {
+      const int task = rg * NWC + wave;
+      int mat[RT], row0[RT];
+      rsrc_t wres[RT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        ws_tile<EPI>(task, r, mat[r], row0[r]);
+        wres[r] = make_rsrc((const S *)a.w[mat[r]] + (int64_t)(row0[r] >> 4) * nkb * 256 * CE,
+                            row0[r] < a.rows[mat[r]] ? (uint32_t)nkb * 4096u : 0u);
+      }
+      u32x4 wq[DEPTH][2][RT];
+      auto wload = [&](int slot, int st) {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+          const int g = g_begin + st * 2 + sub;
+#pragma unroll
+          for (int r = 0; r < RT; ++r)
+            wq[slot][sub][r] = bld16_stream(wres[r], g < g_end ? (uint32_t)g * 1024u + (uint32_t)lane * 16u : BUF_OOB);
+        }
+      };
+      f32x4 acc[RT][CT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int c = 0; c < CT; ++c) acc[r][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < DEPTH; ++s) wload(s, s);
+      auto stage = [&](int st, int slot, int buf) {
+        ws_barrier();
+        u32x4 bq[PF];
+#pragma unroll
+        for (int j = 0; j < PF; ++j) bq[j] = s_x[buf][j * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const u32x4 b = bq[j % PF];
+          if (j + PF < NB) bq[j % PF] = s_x[buf][(j + PF) * 64 + lane];
+          const int sub = j / CT, c = j % CT;
+#pragma unroll
+          for (int r = 0; r < RT; ++r) acc[r][c] = mma<DT>(wq[slot][sub][r], b, acc[r][c]);
+        }
+        // PF operand reads ahead, then RT MFMAs and one read per operand
+        __builtin_amdgcn_sched_group_barrier(0x100, PF, 0);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          __builtin_amdgcn_sched_group_barrier(0x008, RT, 0);
+          if (j + PF < NB) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        wload(slot, st + DEPTH);
+      };
+      // whole rounds of UNR stages with no guard, so that the waits for the
+      // weight ring count its loads exactly; then the remaining stages
+      int st0 = 0;
+      for (; st0 + UNR <= nstage; st0 += UNR) {
+#pragma unroll
+        for (int h = 0; h < UNR; ++h) stage(st0 + h, h % DEPTH, h & 1);
+      }
+#pragma unroll
+      for (int h = 0; h < UNR; ++h)
+        if (st0 + h < nstage) stage(st0 + h, h % DEPTH, h & 1);
+      ws_barrier();
+
+      const int rr = 4 * lq;
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        const int col = colg0 + c * 16 + li;
+        if (col >= a.ncols) continue;
+        if constexpr (EPI == EPI_SWIGLU) {
+          constexpr int H = RT / 2;
+#pragma unroll
+          for (int r = 0; r < H; ++r) {
+            const int m2[2] = {0, 1}, r2[2] = {row0[r], row0[r + H]};
+            const f32x4 v2[2] = {acc[r][c], acc[r + H][c]};
+            gemm_epilogue<DT, EPI_SWIGLU, 2>(a, m2, r2, v2, col, rr);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < RT; ++r) gemm_epilogue<DT, EPI, 1>(a, &mat[r], &row0[r], &acc[r][c], col, rr);
+        }
+      }
+    } else {
+      // no task in this unit: the same barriers
+      for (int st = 0; st < nstage; ++st) ws_barrier();
+      ws_barrier();
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launch shapes
 // ---------------------------------------------------------------------------
 constexpr int XS_MAX_BYTES = 32 * 1024;  // LDS for normalised activations
@@ -1160,22 +1349,35 @@ int lds_groups(const GemmArgs &a, int tiles16, int k_split, int &n_groups, int &
   return nu > 1 ? (n_groups + 7) / 8 * 8 * nu : n_groups;
 }
 
+// after a GEMM that split K: the kernel that sums the partials into the
+// residual stream, or into the q/k/v epilogue
+template <int DT, int EPI>
+hipError_t split_finish(const GemmArgs &g, hipStream_t st) {
+  const int64_t n = (int64_t)g.ncols * (split_rows(g, EPI) / 4);
+  if constexpr (epi_qkv(EPI)) {
+    HS_LAUNCH((k_qkv_split_epilogue<DT, EPI == EPI_QKV_PAGED>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+              g);
+  } else {
+    HS_LAUNCH(k_splitk_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, g.splitk_ws, g.k_split, g.ncols,
+              g.rows[0], g.resid, g.ld_resid);
+  }
+  return hipGetLastError();
+}
+
 template <int DT, int EPI, int RTG, int CTG>
 hipError_t gemm_lds_launch(const GemmArgs &a, int tiles16, int k_split, hipStream_t st) {
   GemmArgs g = a;
   g.k_split = k_split;
   const int blocks = lds_groups<EPI, RTG, CTG>(a, tiles16, k_split, g.n_groups, g.n_colg);
   HS_LAUNCH((k_gemm_lds<DT, EPI, RTG, CTG>), dim3(blocks), dim3(64 * LG_NW), 0, st, g);
-  hipError_t e = hipGetLastError();
+  const hipError_t e = hipGetLastError();
   if (e != hipSuccess || k_split <= 1) return e;
-  const int64_t n = (int64_t)a.ncols * (split_rows(a, EPI) / 4);
-  if constexpr (epi_qkv(EPI)) {
-    HS_LAUNCH((k_qkv_split_epilogue<DT, EPI == EPI_QKV_PAGED>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-              g);
-  } else {
-    HS_LAUNCH(k_splitk_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a.splitk_ws, k_split, a.ncols,
-              a.rows[0], a.resid, a.ld_resid);
-  }
+  return split_finish<DT, EPI>(g, st);
+}
+
+template <int DT, int EPI>
+hipError_t gemm_ws_launch(const GemmArgs &a, hipStream_t st) {
+  HS_LAUNCH((k_gemm_ws<DT, EPI>), dim3(WS_GRID), dim3(64 * (WS_NWC + WS_NP)), 0, st, a);
   return hipGetLastError();
 }
 
@@ -1191,6 +1393,8 @@ hipError_t gemm_lds_launch(const GemmArgs &a, int tiles16, int k_split, hipStrea
 constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 384, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
 template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
+  if constexpr (DT != HS_F32 && (EPI == EPI_SWIGLU || EPI == EPI_STORE))
+    if (p.ncols >= WS_MIN_COLS && p.ncols <= WS_MAX_COLS) return gemm_ws_launch<DT, EPI>(p, st);
   int ng, nc;
   if (lds_groups<EPI, 16, 8>(p, tiles16, 1, ng, nc) >= LDS_BIG_GROUPS)
     return gemm_lds_launch<DT, EPI, 16, 8>(p, tiles16, 1, st);

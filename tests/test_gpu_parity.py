@@ -206,6 +206,21 @@ def test_many_columns_split_k_qkv():
     assert near <= 2
 
 
+@pytest.mark.parametrize("d_model,n_heads,n_kv_heads,qkv_bias,dtype", [(1024, 8, 2, 1, "bf16"), (512, 4, 4, 0, "f16")])
+def test_weight_stationary_columns(d_model, n_heads, n_kv_heads, qkv_bias, dtype):
+    """150 requests (129..256 columns): gate/up and the LM head take the
+    weight-stationary GEMM (two column groups, the second ragged; F = 1000
+    leaves a ragged last gate/up task and V = 997 a ragged LM head), while
+    q/k/v, O and down stay on the LDS-staged kernel (at d = 1024 with K
+    split two ways)."""
+    cfg = small_cfg(n_layers=1, d_model=d_model, n_heads=n_heads, n_kv_heads=n_kv_heads, head_dim=128, ffn_dim=1000,
+                    dtype=dtype, qkv_bias=qkv_bias)
+    n_v = [(13 * b) % 11 for b in range(150)]
+    s_text = [1 + (5 * b) % 4 for b in range(150)]
+    near = _run_pair(cfg, n_v, s_text, 2)
+    assert near <= 3
+
+
 @pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
 def test_long_context_many_splits(n_v, dtype):
     """Contexts long enough for many attention splits in decode: at most 8
