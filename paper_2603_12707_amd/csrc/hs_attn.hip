@@ -97,10 +97,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   const rsrc_t kr = make_rsrc((const S *)a.kv.buf + max(ko, (int64_t)0), nbytes);
   const rsrc_t vr = make_rsrc((const S *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
-  float qf[G][CE];
+  // the query chunks are requested first and unpacked once the batch's K/V
+  // loads are in flight, so their latency overlaps
+  u32x4 qraw[G];
 #pragma unroll
-  for (int h = 0; h < G; ++h)
-    unpack<DT>(ld16((const S *)a.q + (int64_t)qi * a.ld_q + (j * G + h) * HD + c * CE), qf[h]);
+  for (int h = 0; h < G; ++h) qraw[h] = ld16((const S *)a.q + (int64_t)qi * a.ld_q + (j * G + h) * HD + c * CE);
+  float qf[G][CE];
 
   float m[G], l[G], o[G][CE];
 #pragma unroll
@@ -132,6 +134,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
       kc[u] = bld16_stream(kb, off);
       vc[u] = bld16_stream(vb, off);
     }
+    // opaque to the compiler: keeps the unpack (and its wait) here, behind the loads
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      asm volatile("" : "+v"(qraw[h]));
+      unpack<DT>(qraw[h], qf[h]);
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int tt = (it0 + u) * STEP + wave * TPW + tg;
@@ -145,16 +153,17 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < CE; ++e) d += qf[h][e] * kf[e];
         d = group_sum<LPT>(d);
-        if (valid) {
-          const float sc = d * a.scale;
-          const float mn = fmaxf(m[h], sc);
-          const float corr = merge_weight(m[h], mn);
-          const float p = expf(sc - mn);
-          l[h] = l[h] * corr + p;
+        // branch-free update: a position past the split (zero K/V rows)
+        // leaves the state as it is (a branch here let the compiler move a
+        // V load behind it, with a wait for every load in flight)
+        const float sc = valid ? d * a.scale : -INFINITY;
+        const float mn = fmaxf(m[h], sc);
+        const float corr = merge_weight(m[h], mn);
+        const float p = valid ? expf(sc - mn) : 0.f;
+        l[h] = l[h] * corr + p;
 #pragma unroll
-          for (int e = 0; e < CE; ++e) o[h][e] = o[h][e] * corr + p * vf[e];
-          m[h] = mn;
-        }
+        for (int e = 0; e < CE; ++e) o[h][e] = o[h][e] * corr + p * vf[e];
+        m[h] = mn;
       }
     }
   }
