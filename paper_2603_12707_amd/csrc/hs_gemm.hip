@@ -1383,14 +1383,16 @@ hipError_t gemm_ws_launch(const GemmArgs &a, hipStream_t st) {
 
 // Many columns.  Where the work-group tile of 16 x 8 row x column tiles (wave
 // tiles of 4 x 4, half the LDS reads per MFMA) still gives LDS_BIG_GROUPS
-// work groups, it is taken (prefill gate/up at 640 rows: 159 against 191 us).
+// work groups, it is taken (prefill gate/up at 640 rows: 159 against 191 us;
+// with the threshold at 200 instead of 384 the 640-row q/k/v takes it too,
+// and the LLaVA-shaped prefill went from 21.1 to 20.2 ms).
 // A GEMM (residual or q/k/v) with fewer than SPLITK_BELOW work groups
 // splits K (up to SPLITK_MAX ways, at least 4 k-blocks each) when the
 // partials fit the workspace.  Otherwise the LDS-staged kernel from
 // LDS_MIN_GROUPS work groups up, and below that the register-tiled kernel,
 // whose smaller work groups spread narrow matrices over more CUs (measured
 // crossover: between 64 and 80 work groups of the LDS kernel).
-constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 384, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
+constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 200, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
 template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
   if constexpr (DT != HS_F32 && (EPI == EPI_SWIGLU || EPI == EPI_STORE))
