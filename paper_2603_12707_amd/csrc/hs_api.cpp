@@ -247,7 +247,7 @@ struct Step {
     return launch_combine(c.dtype, c.head_dim, ncols, attn_args(l), st);
   }
 
-  hipError_t residual(const void *w, int K, const void *x) const {
+  hipError_t residual(const void *w, int K, const void *x, int x_packed) const {
     const hs_config &c = m->cfg;
     GemmArgs o{};
     o.w[0] = w;
@@ -255,6 +255,7 @@ struct Step {
     o.K = K;
     o.ncols = ncols;
     o.x = x;
+    o.x_packed = x_packed;
     o.resid = m->x;
     o.ld_resid = c.d_model;
     o.splitk_ws = m->splitk;
@@ -264,7 +265,7 @@ struct Step {
 
   hipError_t oproj(int l) const {
     const hs_config &c = m->cfg;
-    if (!combine_fused()) return residual(m->layers[l].wo, c.n_heads * c.head_dim, m->attn);
+    if (!combine_fused()) return residual(m->layers[l].wo, c.n_heads * c.head_dim, m->attn, 0);
     GemmArgs o{};
     o.w[0] = m->layers[l].wo;
     o.rows[0] = c.d_model;
@@ -294,11 +295,16 @@ struct Step {
     u.h_work = m->hnorm;
     u.eps = c.rms_eps;
     u.out = m->act;
+    // in the layout the down projection reads
+    u.out_packed = gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0;
     u.ld_out = c.ffn_dim;
     return launch_gemm(c.dtype, PRO_NORM, EPI_SWIGLU, u, st);
   }
 
-  hipError_t down(int l) const { return residual(m->layers[l].w_down, m->cfg.ffn_dim, m->act); }
+  hipError_t down(int l) const {
+    const hs_config &c = m->cfg;
+    return residual(m->layers[l].w_down, c.ffn_dim, m->act, gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0);
+  }
 
   // final RMSNorm + LM head over ncols rows starting at x_rows
   hipError_t head(const float *x_rows, float *logits) const {
@@ -576,8 +582,8 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       {(void **)&m->x, (size_t)rows * c.d_model * 4},
       {&m->q, (size_t)rows * nh * hd * b},
       {&m->attn, (size_t)rows * nh * hd * b},
-      {&m->act, (size_t)rows * c.ffn_dim * b},
-      {&m->hnorm, (size_t)rows * c.d_model * b},
+      {&m->act, (size_t)act_elems(rows, c.ffn_dim) * b},
+      {&m->hnorm, (size_t)act_elems(rows, c.d_model) * b},
       {(void **)&m->splitk, (size_t)m->splitk_floats * 4},
       {(void **)&m->xlast, (size_t)PACK_MAX * c.d_model * 4},
       {(void **)&m->pk_dev, sizeof(PackedRows)},
@@ -854,7 +860,7 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows) {
   const int b = dtype_bytes(c.dtype), nhd = c.n_heads * c.head_dim;
   void *fresh[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
   const size_t bytes[5] = {(size_t)rows * c.d_model * 4, (size_t)rows * nhd * b, (size_t)rows * nhd * b,
-                           (size_t)rows * c.ffn_dim * b, (size_t)rows * c.d_model * b};
+                           (size_t)act_elems(rows, c.ffn_dim) * b, (size_t)act_elems(rows, c.d_model) * b};
   for (int i = 0; i < 5; ++i)
     if (hipMalloc(&fresh[i], bytes[i]) != hipSuccess) {
       for (void *p : fresh)

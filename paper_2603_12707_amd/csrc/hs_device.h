@@ -148,6 +148,16 @@ __device__ __forceinline__ u32x4 ld16_stream(const void *p) {
   return __builtin_nontemporal_load((const u32x4 *)p);
 }
 
+// Packed activation layout (16-bit storage): column c, element k of a matrix
+// of K-long columns sits where the MFMA B operand wants it -- per 16-column
+// tile and 128-element k-block, four 1 KB sub-blocks of 32 elements, lane
+// 16 * (k / 8 mod 4) + c mod 16 holding 8 consecutive elements -- so a wave
+// reads one sub-block of a column tile as 1 KB of consecutive bytes.
+__host__ __device__ inline int64_t packed_x_index(int c, int k, int nkb) {
+  return ((((int64_t)(c >> 4) * nkb + (k >> 7)) * 4 + ((k >> 5) & 3)) * 64 + (((k >> 3) & 3) << 4) + (c & 15)) * 8 +
+         (k & 7);
+}
+
 // ---------------------------------------------------------------------------
 // raw buffer reads
 // ---------------------------------------------------------------------------

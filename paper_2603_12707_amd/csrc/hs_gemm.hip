@@ -91,10 +91,12 @@ __device__ __forceinline__ void tile_map(const GemmArgs &a, int g, int *mat, int
   }
 }
 
-template <int DT, int EPI, int R>
+// PK: the SwiGLU output goes to the packed activation layout where a.out_packed
+// says so (the down projection reads it so, which happens at 2..32 columns,
+// the widths k_gemm serves; the kernels for wider GEMMs never write it)
+template <int DT, int EPI, int R, bool PK = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat, const int *row0, const f32x4 *v,
                                               int col, int rr) {
-  constexpr int B = DT == HS_F32 ? 4 : 2;
   if constexpr (EPI == EPI_STORE) {
     float *o = (float *)a.out + (int64_t)col * a.ld_out;
 #pragma unroll
@@ -114,13 +116,15 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &a, const int *mat,
         if (row < a.rows[mat[r]]) x[row] += v[r][e];
       }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    void *o = (char *)a.out + (int64_t)col * a.ld_out * B;
+    const bool packed = PK && a.out_packed;
+    const int nkb_o = (a.rows[0] / 8 + 15) / 16;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int j = row0[0] + rr + e;
       if (j < a.rows[0]) {
         const float g = v[0][e], u = v[1][e];
-        st_elem<DT>(o, j, g / (1.0f + expf(-g)) * u);
+        const int64_t at = packed ? packed_x_index(col, j, nkb_o) : (int64_t)col * a.ld_out + j;
+        st_elem<DT>(a.out, at, g / (1.0f + expf(-g)) * u);
       }
     }
   }
@@ -336,17 +340,21 @@ __device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
 // squares in fp64 -- the normalisation the GEMM prologue applies when it
 // stages its columns itself, done once for GEMMs over more columns.
 template <int DT>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gain, float eps, int K, void *h) {
+__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gain, float eps, int K, void *h,
+                                                int packed) {
   const float *xr = x + (int64_t)blockIdx.x * K;
   __shared__ double s_part[4];
   double ss = 0.0;
   for (int k = threadIdx.x * 4; k < K; k += 1024) ss += sumsq_f64(*(const f32x4 *)(xr + k));
   const float rs = (float)(1.0 / sqrt(block_sum<4>(ss, s_part) / (double)K + (double)eps));
+  const int nkb = (K / 8 + 15) / 16;
   for (int k = threadIdx.x * 4; k < K; k += 1024) {
     float g[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) g[e] = ld_elem<DT>(gain, k + e);
-    put_h<DT>((unsigned char *)h, (int64_t)blockIdx.x * K + k, *(const f32x4 *)(xr + k), rs, g);
+    // (packed: the 4 elements stay consecutive, k being a multiple of 4)
+    const int64_t at = packed ? packed_x_index((int)blockIdx.x, k, nkb) : (int64_t)blockIdx.x * K + k;
+    put_h<DT>((unsigned char *)h, at, *(const f32x4 *)(xr + k), rs, g);
   }
 }
 
@@ -365,7 +373,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gai
 // rebuilt from its split partials), or from the activation rows in global
 // memory (PRO_PLAIN, XS = 0), requested with the weights.  The waves' partial
 // tiles are summed in a fixed order through LDS and handed to the epilogue.
-template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI>
+// PK: the SwiGLU output in the packed layout; XP: activations read from
+// memory in the packed layout (a.out_packed, a.x_packed)
+template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI, bool PK, bool XP>
 __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   static_assert(PRO == PRO_PLAIN || XS == 1, "only plain activations are read from global memory");
   using S = typename Ty<DT>::S;
@@ -414,7 +424,9 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   const rsrc_t gr = make_rsrc(a.gain, PRO == PRO_NORM ? (uint32_t)K * SB : 0u);
   // x of the work group's columns: fp32 residual rows (PRO_NORM) or activation rows
   const rsrc_t xr = PRO == PRO_NORM ? make_rsrc((const float *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * 4u)
-                                    : make_rsrc((const S *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * SB);
+                    : XP          ? make_rsrc((const S *)a.x + (int64_t)(col0 >> 4) * nkb * 256 * CE,
+                                              (uint32_t)((nst + 15) >> 4) * nkb * 4096u)
+                                  : make_rsrc((const S *)a.x + (int64_t)col0 * K, (uint32_t)nst * K * SB);
   __shared__ double s_part[NW];
   extern __shared__ __align__(16) unsigned char s_x[];  // XS: activations [nst][K]
 
@@ -532,7 +544,12 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       const u32x4 v = *(const u32x4 *)((const S *)s_x + (ok ? (int64_t)c * K + (int64_t)kc * CE : 0));
       return ok ? v : u32x4{0u, 0u, 0u, 0u};
     } else {
-      return bld16(xr, ok ? (uint32_t)(c * K + kc * CE) * SB : BUF_OOB);
+      // packed: chunk kc of column tile col0 / 16 + t is lane 16 * (kc mod 4) + li
+      // of sub-block kc / 4
+      const uint32_t at = XP ? ((((uint32_t)(t * nkb) + (uint32_t)(kc >> 4)) * 4u + (uint32_t)((kc >> 2) & 3)) * 64u +
+                                (uint32_t)((kc & 3) * 16 + li)) * 16u
+                             : (uint32_t)(c * K + kc * CE) * SB;
+      return bld16(xr, ok ? at : BUF_OOB);
     }
   };
 
@@ -732,7 +749,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     } else if constexpr (epi_qkv(EPI)) {
       if (col < a.ncols) qkv_store<DT, R, EPI == EPI_QKV_PAGED>(a, mat, row0, v, col, 4 * (ln >> 4), qin);
     } else {
-      if (col < a.ncols) gemm_epilogue<DT, EPI, R>(a, mat, row0, v, col, 4 * (ln >> 4));
+      if (col < a.ncols) gemm_epilogue<DT, EPI, R, PK>(a, mat, row0, v, col, 4 * (ln >> 4));
     }
   }
 }
@@ -1293,7 +1310,26 @@ hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_
   g.n_groups = n_groups;
   g.n_colg = (a.ncols + 16 * NT - 1) / (16 * NT);
   const int blocks = g.n_colg > 1 ? (n_groups + 7) / 8 * 8 * g.n_colg : n_groups;
-  HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI>), dim3(blocks), dim3(64 * NW), shmem, st, g);
+  // the packed layouts get instantiations of their own, so the usual
+  // row-major loads and stores carry no branch
+  if constexpr (DT != HS_F32) {
+    if constexpr (EPI == EPI_SWIGLU)
+      if (a.out_packed) {
+        if constexpr (XS == 0)
+          if (a.x_packed) {
+            HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI, true, true>), dim3(blocks), dim3(64 * NW), shmem, st, g);
+            return hipGetLastError();
+          }
+        HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI, true, false>), dim3(blocks), dim3(64 * NW), shmem, st, g);
+        return hipGetLastError();
+      }
+    if constexpr (XS == 0)
+      if (a.x_packed) {
+        HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI, false, true>), dim3(blocks), dim3(64 * NW), shmem, st, g);
+        return hipGetLastError();
+      }
+  }
+  HS_LAUNCH((k_gemm<DT, R, NT, NW, U, PRO, XS, EPI, false, false>), dim3(blocks), dim3(64 * NW), shmem, st, g);
   return hipGetLastError();
 }
 
@@ -1434,8 +1470,11 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   GemmArgs p = a;
   if constexpr (PRO == PRO_NORM) {
     // more columns than the prologue stages: normalise them once, then read
-    // them as plain activations
-    HS_LAUNCH(k_rmsnorm<DT>, dim3(a.ncols), dim3(256), 0, st, (const float *)a.x, a.gain, a.eps, a.K, a.h_work);
+    // them as plain activations (in the packed layout where the GEMM reads
+    // them through MFMA-operand loads)
+    p.x_packed = gemm_x_packed(DT, a.ncols, a.K) ? 1 : 0;
+    HS_LAUNCH(k_rmsnorm<DT>, dim3(a.ncols), dim3(256), 0, st, (const float *)a.x, a.gain, a.eps, a.K, a.h_work,
+              p.x_packed);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     p.x = a.h_work;
@@ -1465,6 +1504,17 @@ hipError_t gemm_dt(int pro, int epi, const GemmArgs &a, hipStream_t st) {
 }
 
 }  // namespace
+
+bool gemm_x_packed(int dtype, int ncols, int K) {
+  // the launch shape's choice: activations staged in LDS (one column tile
+  // that fits the copy), from memory (two column tiles at most), or the
+  // tiled kernels
+  if (dtype == HS_F32 || ncols <= 0) return false;
+  const int tiles = (ncols + 15) / 16;
+  return tiles <= 2 && !(tiles <= 1 && (size_t)ncols * K * 2 <= XS_MAX_BYTES);
+}
+
+int64_t act_elems(int64_t rows, int64_t K) { return std::max(rows * K, (int64_t)32 * ((K + 127) / 128 * 128)); }
 
 hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st) {
   if (a.ncols <= 0 || a.rows[0] <= 0) return hipSuccess;

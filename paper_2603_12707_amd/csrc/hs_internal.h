@@ -56,6 +56,7 @@ struct GemmArgs {
   const void *x;
   const void *gain;
   float eps;
+  int x_packed;          // x in the packed activation layout (packed_x_index) instead of rows
   void *h_work;          // PRO_NORM over many columns: normalised rows, model dtype [ncols][K]
   const float *part_o;   // [ncols][n_heads][n_split][head_dim]
   const float *part_ml;  // [ncols][n_heads][n_split][2]
@@ -63,6 +64,7 @@ struct GemmArgs {
   // epilogue outputs
   void *out;    // logits fp32 / SwiGLU output / q after RoPE, row stride ld_out
   int ld_out;
+  int out_packed;  // SwiGLU output in the packed activation layout (K = rows[0])
   float *resid; // residual stream fp32 [ncols][ld_resid], updated in place
   int ld_resid;
   // residual epilogue split over K: fp32 partials [k_split][ncols][rows[0]]
@@ -127,6 +129,13 @@ struct AttnArgs {
 };
 
 hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream_t st);
+// whether a GEMM over ncols columns with K-long 16-bit activations reads them
+// from memory through MFMA-operand loads (2..32 columns that the LDS copy
+// cannot hold); its producer then writes them in the packed activation layout
+bool gemm_x_packed(int dtype, int ncols, int K);
+// elements an activation buffer of `rows` rows of K needs, the packed layout
+// of up to 32 columns included
+int64_t act_elems(int64_t rows, int64_t K);
 // whether launch_gemm takes PRO_COMBINE for these shapes
 bool gemm_combine_fusable(int dtype, int ncols, int K, int n_heads, int n_split);
 hipError_t launch_pack(int dtype, const void *src, int64_t rows, int64_t cols, void *dst, int pair_hd,

@@ -146,6 +146,21 @@ def test_column_tiles(B):
     assert near <= 2
 
 
+def test_packed_activation_layout():
+    """24 requests at d = 1024 (GQA-4 with bias, F = 1000): the q/k/v, gate/up,
+    down and LM head GEMMs read their activations from memory in the packed
+    MFMA-operand layout, written by the RMSNorm and by the SwiGLU epilogue
+    (F pads to 1024 there).  The prefills, 2..31 rows each, mix the producer
+    and consumer paths: a small prefill stages q/k/v and gate/up activations
+    in LDS while its down projection reads the packed layout."""
+    cfg = small_cfg(n_layers=1, d_model=1024, n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=1000, dtype="bf16",
+                    qkv_bias=1)
+    n_v = [(9 * b) % 27 for b in range(24)]
+    s_text = [2 + (5 * b) % 3 for b in range(24)]
+    near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 2
+
+
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 def test_packed_prefill_mha(dtype):
     """Six requests of mixed shapes (no vision rows, no text, one row)
