@@ -224,6 +224,8 @@ struct Step {
     a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
     a.order = !prefill && ncols > 1 ? kv->d_order : nullptr;
     a.out = m->attn;
+    // in the layout the O projection reads
+    a.out_packed = gemm_x_packed(c.dtype, ncols, c.n_heads * c.head_dim) ? 1 : 0;
     return a;
   }
 
@@ -265,7 +267,8 @@ struct Step {
 
   hipError_t oproj(int l) const {
     const hs_config &c = m->cfg;
-    if (!combine_fused()) return residual(m->layers[l].wo, c.n_heads * c.head_dim, m->attn, 0);
+    const int ko = c.n_heads * c.head_dim;
+    if (!combine_fused()) return residual(m->layers[l].wo, ko, m->attn, gemm_x_packed(c.dtype, ncols, ko) ? 1 : 0);
     GemmArgs o{};
     o.w[0] = m->layers[l].wo;
     o.rows[0] = c.d_model;
@@ -581,7 +584,7 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
   } allocs[] = {
       {(void **)&m->x, (size_t)rows * c.d_model * 4},
       {&m->q, (size_t)rows * nh * hd * b},
-      {&m->attn, (size_t)rows * nh * hd * b},
+      {&m->attn, (size_t)act_elems(rows, nh * hd) * b},
       {&m->act, (size_t)act_elems(rows, c.ffn_dim) * b},
       {&m->hnorm, (size_t)act_elems(rows, c.d_model) * b},
       {(void **)&m->splitk, (size_t)m->splitk_floats * 4},
@@ -859,7 +862,7 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows) {
   const hs_config &c = m->cfg;
   const int b = dtype_bytes(c.dtype), nhd = c.n_heads * c.head_dim;
   void *fresh[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
-  const size_t bytes[5] = {(size_t)rows * c.d_model * 4, (size_t)rows * nhd * b, (size_t)rows * nhd * b,
+  const size_t bytes[5] = {(size_t)rows * c.d_model * 4, (size_t)rows * nhd * b, (size_t)act_elems(rows, nhd) * b,
                            (size_t)act_elems(rows, c.ffn_dim) * b, (size_t)act_elems(rows, c.d_model) * b};
   for (int i = 0; i < 5; ++i)
     if (hipMalloc(&fresh[i], bytes[i]) != hipSuccess) {

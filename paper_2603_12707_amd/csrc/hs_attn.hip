@@ -21,6 +21,13 @@ __device__ __forceinline__ float merge_weight(float m_part, float m_all) {
   return m_part == -INFINITY ? 0.f : expf(m_part - m_all);
 }
 
+// element (row, c) of the combined output: rows of n_heads * head_dim, or the
+// packed activation layout the O projection reads at 2..32 columns
+__device__ __forceinline__ int64_t attn_out_at(const AttnArgs &a, int64_t row, int c, int hd) {
+  const int K = a.n_heads * hd;
+  return a.out_packed ? packed_x_index((int)row, c, (K / 8 + 15) / 16) : row * K + c;
+}
+
 // One work group = (split, KV head j, query).  Each of its NW waves walks
 // its share of the split's positions (LPT lanes per position, one 16-byte
 // chunk of the K row and of the V row per lane), requesting the chunks of UB
@@ -209,7 +216,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
       den += wt * s_l[w][h];
     }
     if (a.n_split == 1) {
-      st_elem<DT>(a.out, (qh + h) * HD + e, num / den);
+      st_elem<DT>(a.out, attn_out_at(a, qi, (j * G + h) * HD + e, HD), num / den);
     } else {
       a.part_o[((qh + h) * a.n_split + split) * HD + e] = num;
       if (e == 0) {
@@ -413,7 +420,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
       den += wt * s_l[w][h];
     }
     if (a.n_split == 1) {
-      st_elem<DT>(a.out, (qh + h) * HD + e, num / den);
+      st_elem<DT>(a.out, attn_out_at(a, qi, (j * G + h) * HD + e, HD), num / den);
     } else {
       a.part_o[((qh + h) * a.n_split + split) * HD + e] = num;
       if (e == 0) {
@@ -539,13 +546,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   }
   if (!slot) return;
   // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
-  const int64_t orow = ((int64_t)(roff + sq) * a.n_heads + j * G + sh) * HD;
+  const int64_t orow = roff + sq;
+  const int ocol = (j * G + sh) * HD;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int d = (4 * lg + i) * 8 + dt;
-      if (d < HD) st_elem<DT>(a.out, orow + d, o[dt][i] / l);
+      if (d < HD) st_elem<DT>(a.out, attn_out_at(a, orow, ocol + d, HD), o[dt][i] / l);
     }
 }
 
@@ -594,7 +602,7 @@ __global__ __launch_bounds__(HD) void k_combine(AttnArgs a) {
       num += s_w[sp] * a.part_o[(base + sp) * HD + e];
     }
   }
-  st_elem<DT>(a.out, ((int64_t)qi * a.n_heads + h) * HD + e, num / den);
+  st_elem<DT>(a.out, attn_out_at(a, qi, h * HD + e, HD), num / den);
 }
 
 template <int DT, int HD, bool PAGED>

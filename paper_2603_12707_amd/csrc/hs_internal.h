@@ -125,6 +125,7 @@ struct AttnArgs {
   float *part_o;   // [nq][n_heads][n_split][head_dim]
   float *part_ml;  // [nq][n_heads][n_split][2]
   float scale;
+  int out_packed;  // out in the packed activation layout (the O projection reads it so)
   void *out;       // combined output, model dtype [nq][n_heads * head_dim]
 };
 
