@@ -113,6 +113,22 @@ def test_pool_parity_across_blocks_and_continuous_batching():
     assert run.near <= 2
 
 
+def test_pool_packed_activations_and_wide_prefill():
+    """20 requests in 22 slots at d = 1024 (GQA-4 with bias, F = 1000): one
+    prefill call packs their ~150 rows (gate/up and the LM head on the
+    weight-stationary kernel), and the 20-column decode steps read packed
+    activations while the q/k/v epilogue appends into the blocks."""
+    cfg = small_cfg(n_layers=1, d_model=1024, n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=1000, dtype="bf16",
+                    qkv_bias=1)
+    run = PoolRun(cfg, slots=22, n_blocks=24, max_ctx=64)
+    entries = [(s, (5 * s) % 11, 2 + s % 3, 24) for s in range(1, 21)]
+    run.admit_and_prefill(entries, key=7)
+    run.decode(3)
+    assert run.pool.lengths() == [0] + [n + t + 3 for _, n, t, _ in entries] + [0]
+    assert run.pair.gpu.status() == 0
+    assert run.near <= 2
+
+
 def test_pool_gqa7_mrope():
     """Pooled cache with 7 query heads per KV head (matrix-core decode
     attention reading the blocks batch by batch) and M-RoPE."""
