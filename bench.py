@@ -185,6 +185,17 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
     return ws, models, kv, first, lens
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
     """The oracle, single-threaded on one host core, decoding n_tokens for one
     request of the workload from a synthetic cache of ctx positions.  Its
@@ -203,16 +214,25 @@ def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
     seq.set_len(ctx, ctx)
     log(f"oracle inputs ready in {time.time() - t:.1f} s")
     tok = int(synth.decode_tokens(cfg, 0, 1)[0])
-    t = time.perf_counter()
-    for _ in range(n_tokens):
-        _, _, nxt = seq.decode(tok)
-        tok = nxt if cfg.get("lm_head", True) else tok
-    el = time.perf_counter() - t
+    # timed on one host core (the process is pinned to it meanwhile)
+    allowed = os.sched_getaffinity(0)
+    core = min(allowed)
+    os.sched_setaffinity(0, {core})
+    try:
+        t = time.perf_counter()
+        for _ in range(n_tokens):
+            _, _, nxt = seq.decode(tok)
+            tok = nxt if cfg.get("lm_head", True) else tok
+        el = time.perf_counter() - t
+    finally:
+        os.sched_setaffinity(0, allowed)
     log(f"oracle: {n_tokens} tokens in {el:.1f} s")
     del w_cpu
     return {"value": n_tokens / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_tokens} greedy decode steps of one request of the workload from a synthetic "
-                      f"{ctx}-position KV cache, single-threaded plain C oracle (fp64 accumulation) on one host core"}
+                      f"{ctx}-position KV cache, single-threaded plain C oracle (fp64 accumulation), pinned to one "
+                      f"host core",
+            "cpu_model": cpu_model(), "host_cpus_available": len(allowed), "pinned_core": core}
 
 
 def main() -> int:
