@@ -1134,8 +1134,8 @@ __global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int k_spl
 constexpr int WS_RT = 4, WS_CT = 8, WS_NWC = 6, WS_NP = 2, WS_DEPTH = 2, WS_PF = 3, WS_GRID = 256;
 constexpr int WS_MIN_COLS = 129, WS_MAX_COLS = 256;
 
-// one work-group barrier with the LDS writes before it complete; the global
-// loads in flight are not waited for (unlike __syncthreads)
+// one work-group barrier once this wave's LDS accesses are complete; the
+// global loads in flight (the weight ring) are not waited for
 __device__ __forceinline__ void ws_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // row tile r of task t -> matrix and first row (SwiGLU: WS_RT/2 gate tiles,
