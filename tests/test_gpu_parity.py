@@ -294,23 +294,34 @@ def test_prefill_then_decode_matches_longer_prefill(rope_kind):
     assert rel_err(la[0].cpu().numpy(), lb.cpu().numpy()) <= 2e-3
 
 
-def test_decode_step_replays_from_a_hip_graph():
+@pytest.mark.parametrize("case", ["three", "packed", "wide"])
+def test_decode_step_replays_from_a_hip_graph(case):
     """hs_decode_step recorded by stream capture (two steps, ping-ponging the
     token buffers) and replayed gives, replay after replay, the tokens and
     logits of eager calls on an identical cache; eager work and
-    synchronisation run between the replays."""
+    synchronisation run between the replays.  Cases: 3 requests (activations
+    staged in LDS), 20 requests at d = 1024 (packed activations read from
+    memory), 150 requests (the weight-stationary gate/up and LM head)."""
     import paper_2603_12707_amd as hs
-    cfg = small_cfg(dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
-    n_v, s_text = [30, 9, 50], [5, 40, 2]
+    if case == "three":
+        cfg = small_cfg(dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
+        n_v, s_text = [30, 9, 50], [5, 40, 2]
+    elif case == "packed":
+        cfg = small_cfg(n_layers=1, d_model=1024, n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=1000, dtype="bf16")
+        n_v, s_text = [(9 * b) % 27 for b in range(20)], [2 + b % 3 for b in range(20)]
+    else:
+        cfg = small_cfg(n_layers=1, dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
+        n_v, s_text = [(13 * b) % 11 for b in range(150)], [1 + (5 * b) % 4 for b in range(150)]
+    B = len(n_v)
     caps = [n + s + 12 for n, s in zip(n_v, s_text)]
-    pair = Pair(cfg, max_batch=3, max_ctx=max(caps))
+    pair = Pair(cfg, max_batch=B, max_ctx=max(caps))
     handles = []
     for _ in range(2):
         kv = hs.KVCache(pair.gpu, n_v, caps)
-        first = torch.empty(3, dtype=torch.int32, device="cuda")
-        for r in range(3):
+        first = torch.empty(B, dtype=torch.int32, device="cuda")
+        for r in range(B):
             emb, ids, _ = pair.request_inputs(r, n_v[r], s_text[r])
-            kv.prefill(r, emb.cuda(), ids.cuda(), first_token=first[r:r + 1])
+            kv.prefill(r, emb.cuda() if n_v[r] else None, ids.cuda(), first_token=first[r:r + 1])
         handles.append((kv, first))
     torch.cuda.synchronize()
     V = cfg["vocab"]
@@ -318,7 +329,7 @@ def test_decode_step_replays_from_a_hip_graph():
     kv_e, t_e = handles[0]
     a, b = t_e.clone(), torch.empty_like(t_e)
     ref_tok, ref_log = [], []
-    lg = torch.empty(3, V, device="cuda")
+    lg = torch.empty(B, V, device="cuda")
     for _ in range(8):
         kv_e.decode(a, b, lg)
         ref_tok.append(b.cpu().clone())
@@ -327,7 +338,7 @@ def test_decode_step_replays_from_a_hip_graph():
     # captured: two steps per graph, replayed four times
     kv_g, t_g = handles[1]
     ga, gb = t_g.clone(), torch.empty_like(t_g)
-    lg1, lg2 = torch.empty(3, V, device="cuda"), torch.empty(3, V, device="cuda")
+    lg1, lg2 = torch.empty(B, V, device="cuda"), torch.empty(B, V, device="cuda")
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         kv_g.decode(ga, gb, lg1)
