@@ -433,12 +433,16 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
 
 // Prefill attention on the matrix cores (causal: row r of the request attends
 // to rows 0..r).  The 16 MFMA columns hold QPT = 16 / G consecutive query rows
-// x the G query heads of KV head j; a wave takes one such query tile and walks
-// the key tiles of 16 positions up to its last query row, masking the keys
-// past each row.  Operand layouts and the p = hi + lo split are those of
-// k_attn_mma; each wave finishes its own queries (no splits, no merge), so
-// the K/V rows a tile loads serve QPT x G (query, head) pairs at once instead
-// of one.
+// x the G query heads of KV head j; a work group takes one such query tile and
+// its NW waves walk the key tiles of 16 positions up to the tile's last query
+// row between them, masking the keys past each row, each wave with its own
+// online softmax; the waves' states merge through LDS at the end.  Operand
+// layouts and the p = hi + lo split are those of k_attn_mma, so the K/V rows a
+// tile loads serve QPT x G (query, head) pairs at once instead of one.
+// Slack (in units of the natural-log score) by which a column's scores may
+// pass the running maximum before it is raised: exp(s - m) stays below e^8.
+constexpr float RESCALE_SLACK = 8.f;
+
 template <int DT, int HD, int G, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   static_assert(DT != HS_F32 && G <= 16 && (HD == 64 || HD == 128), "16-bit storage, at most 16 heads per group");
@@ -450,10 +454,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lg = lane >> 4;
-  const int j = blockIdx.y;
-  // the wave's query tile: tile t - tcu[i] of packed request i
-  const int t = (int)blockIdx.x * NW + wave;
-  if (t >= a.prefill_tiles) return;  // whole wave; no barrier below
+  // The work group's item w = (KV head j, query tile t).  Work groups are
+  // dealt to the 8 XCDs round robin; the order below gives each XCD one run
+  // of consecutive items, so that the query tiles of a head, which all read
+  // its K/V rows, share that XCD's L2.  Within a head the last query tile
+  // comes first, so that the long causal rows start early.  tile t - tcu[i]
+  // belongs to packed request i.  The NW waves take the tile's key tiles
+  // round robin, each with its own online softmax, and merge at the end.
+  const int total = a.prefill_tiles * a.n_kv, nq = total >> 3, nr = total & 7;
+  const int xcd = (int)blockIdx.x & 7;
+  const int w = (xcd < nr ? xcd * (nq + 1) : nr * (nq + 1) + (xcd - nr) * nq) + ((int)blockIdx.x >> 3);
+  const int j = w / a.prefill_tiles;
+  const int t = a.prefill_tiles - 1 - (w - j * a.prefill_tiles);
   const PackedRows *pk = a.pk;
   int pi = 0;
   for (int k = 1; k < pk->n; ++k) pi += t >= pk->tcu[k];
@@ -480,11 +492,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kt0 = 0; kt0 < n_kt; kt0 += UB) {
+  // Key tiles in batches of UB per wave: the wave takes tiles kt0 + u NW +
+  // wave.  Past the tile's last key every load is empty and reads as zero.
+  constexpr int STEP = UB * NW;
+  for (int kt0 = 0; kt0 < n_kt; kt0 += STEP) {
     u32x4 kc[UB][KK], vc[UB][4];
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      const int p0 = (kt0 + u) * 16, blk = p0 / bt, pb = p0 - blk * bt;
+      const int p0 = (kt0 + u * NW + wave) * 16, blk = p0 / bt, pb = p0 - blk * bt;
       const int64_t b0 = p0 <= qlast ? a.kv.tab[toff + blk] : -1;
       // rows of the block up to the tile's last query position; past them, zeros
       const uint32_t nbytes = b0 < 0 ? 0u : (uint32_t)min(bt, qlast + 1 - blk * bt) * HD * SB;
@@ -497,54 +512,93 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
       for (int i = 0; i < 4; ++i)
         vc[u][i] = bld16(vr, li < CPR ? (uint32_t)((pb + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
     }
+    // scores of the batch's key tiles, their chains interleaved (past qlast
+    // every score is masked and the state stays as it is)
+    f32x4 sc[UB];
 #pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      const int p0 = (kt0 + u) * 16;
-      f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < UB; ++u) sc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) sc = mma<DT>(kc[u][kk], qb[kk], sc);
-      float sv[4];
-      float tmax = -INFINITY;
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int u = 0; u < UB; ++u) sc[u] = mma<DT>(kc[u][kk], qb[kk], sc[u]);
+    float sv[UB][4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < UB; ++u)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        sv[i] = slot && p0 + 4 * lg + i <= sq ? sc[i] * a.scale : -INFINITY;
-        tmax = fmaxf(tmax, sv[i]);
+        const int p = (kt0 + u * NW + wave) * 16 + 4 * lg + i;
+        sv[u][i] = slot && p <= sq ? sc[u][i] * a.scale : -INFINITY;
+        tmax = fmaxf(tmax, sv[u][i]);
       }
+    // o / l does not depend on the reference m as long as exp(s - m) stays in
+    // range.  m, the same for the four lanes of a column, is raised to the
+    // column's maximum (and o, l rescaled) only when some score of the wave
+    // passes it by more than RESCALE_SLACK.
+    if (__ballot(tmax > m + RESCALE_SLACK)) {
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
       const float mn = fmaxf(m, tmax);
       const float corr = m == -INFINITY ? 0.f : __expf(m - mn);
-      float pr[4];
+      l *= corr;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pr[i] = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mn);
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= corr;
+      m = mn;
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
       u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u};
-      float ps = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr[i]) : f32_to_bf16(pr[i]);
+        const float pr = sv[u][i] == -INFINITY ? 0.f : __expf(sv[u][i] - m);
+        const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr) : f32_to_bf16(pr);
         const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
-        const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr[i] - hf) : f32_to_bf16(pr[i] - hf);
-        ps += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));
+        const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr - hf) : f32_to_bf16(pr - hf);
+        l += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));  // this lane's keys only
         ph[i >> 1] |= hb << (16 * (i & 1));
         pl[i >> 1] |= lb << (16 * (i & 1));
       }
-      ps += __shfl_xor(ps, 16);
-      ps += __shfl_xor(ps, 32);
-      l = l * corr + ps;
-      m = mn;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
-        o[dt] *= corr;
-        const int w = dt >> 1, sh2 = 16 * (dt & 1);
+        // the 16-bit element dt of keys 4 lg .. 4 lg + 3, low half first
+        const int w = dt >> 1;
+        const uint32_t sel = dt & 1 ? 0x07060302u : 0x05040100u;
         u32x2 av;
-        av[0] = ((vc[u][0][w] >> sh2) & 0xFFFFu) | (((vc[u][1][w] >> sh2) & 0xFFFFu) << 16);
-        av[1] = ((vc[u][2][w] >> sh2) & 0xFFFFu) | (((vc[u][3][w] >> sh2) & 0xFFFFu) << 16);
+        av[0] = __builtin_amdgcn_perm(vc[u][1][w], vc[u][0][w], sel);
+        av[1] = __builtin_amdgcn_perm(vc[u][3][w], vc[u][2][w], sel);
         o[dt] = mma16<DT>(av, ph, o[dt]);
         o[dt] = mma16<DT>(av, pl, o[dt]);
       }
     }
   }
-  if (!slot) return;
+  // l so far covers this lane's keys; the column's sum adds the four lanes
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  // merge the waves' states in wave order: M = max m_w, o = sum_w e^(m_w - M) o_w,
+  // l = sum_w e^(m_w - M) l_w
+  __shared__ float s_ml[NW][2][64];
+  __shared__ f32x4 s_o[NW][8][64];
+  s_ml[wave][0][lane] = m;
+  s_ml[wave][1][lane] = l;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) s_o[wave][dt][lane] = o[dt];
+  __syncthreads();
+  if (wave != 0 || !slot) return;
+  float M = s_ml[0][0][lane];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) M = fmaxf(M, s_ml[w][0][lane]);
+  float L = 0.f;
+  f32x4 O[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const float mw = s_ml[w][0][lane];
+    const float wt = mw == -INFINITY ? 0.f : __expf(mw - M);
+    L += wt * s_ml[w][1][lane];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) O[dt] += wt * s_o[w][dt][lane];
+  }
   // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
   const int64_t orow = roff + sq;
   const int ocol = (j * G + sh) * HD;
@@ -553,7 +607,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int d = (4 * lg + i) * 8 + dt;
-      if (d < HD) st_elem<DT>(a.out, attn_out_at(a, orow, ocol + d, HD), o[dt][i] / l);
+      if (d < HD) st_elem<DT>(a.out, attn_out_at(a, orow, ocol + d, HD), O[dt][i] / L);
     }
 }
 
@@ -661,8 +715,8 @@ hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
 
 template <int DT, int HD>
 hipError_t prefill_hd(int group, const AttnArgs &a, hipStream_t st) {
-  constexpr int NW = 4;
-  const dim3 grid((a.prefill_tiles + NW - 1) / NW, a.n_kv), block(64 * NW);
+  constexpr int NW = 4;  // waves per query tile, taking its key tiles round robin
+  const dim3 grid(a.prefill_tiles * a.n_kv), block(64 * NW);
   switch (group) {
     case 1: HS_LAUNCH((k_attn_prefill<DT, HD, 1, NW>), grid, block, 0, st, a); break;
     case 2: HS_LAUNCH((k_attn_prefill<DT, HD, 2, NW>), grid, block, 0, st, a); break;
