@@ -23,17 +23,17 @@ def _packed_inputs(inputs, order):
             torch.cat(pos, dim=1).contiguous().cuda() if pos else None)
 
 
-def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False, packed=None):
+def _run_pair(cfg, n_v_list, s_text_list, n_dec, extra_cap=0, free_running=False, packed=None, weights=None):
     """Prefills every request on both sides, then runs n_dec decode steps for
     the whole batch (teacher-forced on the oracle's tokens unless
     free_running).  With packed = {"order": [...], "rows": R}, the GPU side
     prefills all requests in one hs_prefill_batch call, in that order, with
     the row workspaces grown to R rows (0: as created).  Returns the number
-    of near ties."""
+    of near ties.  `weights` (CPU tensors) replaces the seeded weights."""
     import paper_2603_12707_amd as hs
     B = len(n_v_list)
     caps = [n + s + n_dec + extra_cap for n, s in zip(n_v_list, s_text_list)]
-    pair = Pair(cfg, max_batch=B, max_ctx=max(caps))
+    pair = Pair(cfg, max_batch=B, max_ctx=max(caps), weights_cpu=weights)
     kv = hs.KVCache(pair.gpu, n_v_list, caps)
     seqs, cur_ref, cur_gpu = [], [], []
     near = 0
@@ -183,6 +183,24 @@ def test_packed_prefill_gqa7_mrope_bias():
     n_v = [70, 16, 121, 9]
     s_text = [12, 12, 3, 31]
     near = _run_pair(cfg, n_v, s_text, 3, packed={"order": [2, 0, 3, 1], "rows": 512})
+    assert near <= 1
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("packed", [False, True])
+def test_prefill_wide_score_range(dtype, packed):
+    """The q and k projections scaled by 8, so that attention scores spread
+    over tens of units (std ~10): the prefill attention's running maximum,
+    raised only when a score passes it by more than its slack, is raised
+    past the first key tiles too, with o and l already accumulated."""
+    cfg = small_cfg(n_layers=1, dtype=dtype)
+    w = synth.make_weights(cfg)
+    for name in ("layers.0.wq", "layers.0.wk"):
+        w[name] = w[name] * 8
+    n_v = [300, 0, 61]
+    s_text = [20, 150, 9]
+    near = _run_pair(cfg, n_v, s_text, 2, weights=w,
+                     packed={"order": [1, 2, 0], "rows": 512} if packed else None)
     assert near <= 1
 
 
