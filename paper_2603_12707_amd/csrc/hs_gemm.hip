@@ -338,23 +338,44 @@ __device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
 // RMSNorm of fp32 residual rows into the storage dtype, one work group per
 // row: h = R(x * rs * gain), rs = 1 / sqrt(mean(x^2) + eps) with the sum of
 // squares in fp64 -- the normalisation the GEMM prologue applies when it
-// stages its columns itself, done once for GEMMs over more columns.
+// stages its columns itself, done once for GEMMs over more columns.  The
+// row's first 4096 elements and their gains are requested together and stay
+// in registers from the sum of squares to the scaling (one memory round trip);
+// a longer row reads the rest twice.
 template <int DT>
 __global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gain, float eps, int K, void *h,
                                                 int packed) {
+  constexpr int NV = 4;  // 16-byte chunks per thread held in registers
+  constexpr int SB = DT == HS_F32 ? 4 : 2;
   const float *xr = x + (int64_t)blockIdx.x * K;
+  const rsrc_t xq = make_rsrc(xr, (uint32_t)K * 4u);
+  const rsrc_t gr = make_rsrc(gain, (uint32_t)K * SB);
   __shared__ double s_part[4];
+  f32x4 xv[NV];
+  float gv[NV][4];
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int k = (u * 256 + (int)threadIdx.x) * 4;
+    xv[u] = __builtin_bit_cast(f32x4, bld16(xq, k < K ? (uint32_t)k * 4u : BUF_OOB));
+    gain4<DT>(gr, k, k < K, gv[u]);
+  }
   double ss = 0.0;
-  for (int k = threadIdx.x * 4; k < K; k += 1024) ss += sumsq_f64(*(const f32x4 *)(xr + k));
+#pragma unroll
+  for (int u = 0; u < NV; ++u) ss += sumsq_f64(xv[u]);  // zeros past K
+  for (int k = (NV * 256 + (int)threadIdx.x) * 4; k < K; k += 1024) ss += sumsq_f64(*(const f32x4 *)(xr + k));
   const float rs = (float)(1.0 / sqrt(block_sum<4>(ss, s_part) / (double)K + (double)eps));
   const int nkb = (K / 8 + 15) / 16;
-  for (int k = threadIdx.x * 4; k < K; k += 1024) {
-    float g[4];
+  // (packed: the 4 elements stay consecutive, k being a multiple of 4)
+  auto at = [&](int k) { return packed ? packed_x_index((int)blockIdx.x, k, nkb) : (int64_t)blockIdx.x * K + k; };
 #pragma unroll
-    for (int e = 0; e < 4; ++e) g[e] = ld_elem<DT>(gain, k + e);
-    // (packed: the 4 elements stay consecutive, k being a multiple of 4)
-    const int64_t at = packed ? packed_x_index((int)blockIdx.x, k, nkb) : (int64_t)blockIdx.x * K + k;
-    put_h<DT>((unsigned char *)h, at, *(const f32x4 *)(xr + k), rs, g);
+  for (int u = 0; u < NV; ++u) {
+    const int k = (u * 256 + (int)threadIdx.x) * 4;
+    if (k < K) put_h<DT>((unsigned char *)h, at(k), xv[u], rs, gv[u]);
+  }
+  for (int k = (NV * 256 + (int)threadIdx.x) * 4; k < K; k += 1024) {
+    float g[4];
+    gain4<DT>(gr, k, true, g);
+    put_h<DT>((unsigned char *)h, at(k), *(const f32x4 *)(xr + k), rs, g);
   }
 }
 
