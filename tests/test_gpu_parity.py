@@ -254,6 +254,20 @@ def test_weight_stationary_columns(d_model, n_heads, n_kv_heads, qkv_bias, dtype
     assert near <= 3
 
 
+@pytest.mark.parametrize("B", [2, 6])
+def test_rows_longer_than_one_pass(B):
+    """d = 4608: the RMSNorm holds a row's first 4096 elements in registers
+    and reads the remaining 512 in a second pass -- in the GEMM prologue at 2
+    columns, in the separate normalisation kernel at 6 columns and in
+    prefill."""
+    cfg = small_cfg(n_layers=1, d_model=4608, n_heads=4, n_kv_heads=4, head_dim=128, ffn_dim=512, vocab=512,
+                    dtype="bf16")
+    n_v = [(7 * b) % 13 for b in range(B)]
+    s_text = [2 + b % 3 for b in range(B)]
+    near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 1
+
+
 @pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
 def test_long_context_many_splits(n_v, dtype):
     """Contexts long enough for many attention splits in decode: at most 8
