@@ -1442,19 +1442,25 @@ hipError_t gemm_ws_launch(const GemmArgs &a, hipStream_t st) {
 // tiles of 4 x 4, half the LDS reads per MFMA) still gives LDS_BIG_GROUPS
 // work groups, it is taken (prefill gate/up at 640 rows: 159 against 191 us;
 // with the threshold at 200 instead of 384 the 640-row q/k/v takes it too,
-// and the LLaVA-shaped prefill went from 21.1 to 20.2 ms).
+// and the LLaVA-shaped prefill went from 21.1 to 20.2 ms).  From
+// WIDE_COLS columns on, 16 x 16 tiles (wave tiles of 4 x 8: 0.375 KB of LDS
+// reads per MFMA instead of 0.5; 128 KB of LDS) where they give as many work
+// groups; below that the 256-column groups pad too much (gate/up at 640
+// rows: 240 against 172 us).
 // A GEMM (residual or q/k/v) with fewer than SPLITK_BELOW work groups
 // splits K (up to SPLITK_MAX ways, at least 4 k-blocks each) when the
 // partials fit the workspace.  Otherwise the LDS-staged kernel from
 // LDS_MIN_GROUPS work groups up, and below that the register-tiled kernel,
 // whose smaller work groups spread narrow matrices over more CUs (measured
 // crossover: between 64 and 80 work groups of the LDS kernel).
-constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 200, SPLITK_BELOW = 128, SPLITK_TARGET = 256;
+constexpr int LDS_MIN_GROUPS = 72, LDS_BIG_GROUPS = 200, SPLITK_BELOW = 128, SPLITK_TARGET = 256, WIDE_COLS = 2048;
 template <int DT, int EPI>
 hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
   if constexpr (DT != HS_F32 && (EPI == EPI_SWIGLU || EPI == EPI_STORE))
     if (p.ncols >= WS_MIN_COLS && p.ncols <= WS_MAX_COLS) return gemm_ws_launch<DT, EPI>(p, st);
   int ng, nc;
+  if (p.ncols >= WIDE_COLS && lds_groups<EPI, 16, 16>(p, tiles16, 1, ng, nc) >= LDS_BIG_GROUPS)
+    return gemm_lds_launch<DT, EPI, 16, 16>(p, tiles16, 1, st);
   if (lds_groups<EPI, 16, 8>(p, tiles16, 1, ng, nc) >= LDS_BIG_GROUPS)
     return gemm_lds_launch<DT, EPI, 16, 8>(p, tiles16, 1, st);
   const int blocks = lds_groups<EPI, 8, 8>(p, tiles16, 1, ng, nc);
