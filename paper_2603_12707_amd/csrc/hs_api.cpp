@@ -219,6 +219,8 @@ struct Step {
     a.prefill = prefill;
     a.pk = m->pk_dev;
     a.prefill_tiles = pk.tcu[pk.n];
+    a.prefill_pairs = 0;
+    for (int i = 0; i < pk.n; ++i) a.prefill_pairs += (pk.tcu[i + 1] - pk.tcu[i] + 1) / 2;
     a.S = S;
     a.n_split = n_split;
     a.part_o = m->part_o;

@@ -432,68 +432,93 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
 }
 
 // Prefill attention on the matrix cores (causal: row r of the request attends
-// to rows 0..r).  The 16 MFMA columns hold QPT = 16 / G consecutive query rows
-// x the G query heads of KV head j; a work group takes one such query tile and
-// its NW waves walk the key tiles of 16 positions up to the tile's last query
-// row between them, masking the keys past each row, each wave with its own
-// online softmax; the waves' states merge through LDS at the end.  Operand
-// layouts and the p = hi + lo split are those of k_attn_mma, so the K/V rows a
-// tile loads serve QPT x G (query, head) pairs at once instead of one.
+// to rows 0..r).  The 16 MFMA columns of a query tile hold QPT = 16 / G
+// consecutive query rows x the G query heads of KV head j.  A work group
+// takes two consecutive query tiles of one request; its NW waves walk the key
+// tiles of 16 positions up to the pair's last row between them, each K/V tile
+// loaded once for both query tiles, masking the keys past each row, each wave
+// with an online softmax per query tile; the waves' states merge through LDS
+// at the end.  Operand layouts and the p = hi + lo split are those of
+// k_attn_mma, so the K/V rows a wave loads serve 2 x QPT x G (query, head)
+// pairs at once.
 // Slack (in units of the natural-log score) by which a column's scores may
 // pass the running maximum before it is raised: exp(s - m) stays below e^8.
 constexpr float RESCALE_SLACK = 8.f;
 
 template <int DT, int HD, int G, int NW>
-__global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
   static_assert(DT != HS_F32 && G <= 16 && (HD == 64 || HD == 128), "16-bit storage, at most 16 heads per group");
   constexpr int SB = 2;
   constexpr int CPR = HD / 8;
   constexpr int KK = HD / 32;
   constexpr int UB = ATTN_MMA_BATCH;
   constexpr int QPT = 16 / G;  // query rows per tile
+  constexpr int QT = 2;        // query tiles per work group
+  static_assert(NW >= QT, "one merging wave per query tile");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lg = lane >> 4;
-  // The work group's item w = (KV head j, query tile t).  Work groups are
+  // The work group's item w = (KV head j, tile pair pp).  Work groups are
   // dealt to the 8 XCDs round robin; the order below gives each XCD one run
   // of consecutive items, so that the query tiles of a head, which all read
-  // its K/V rows, share that XCD's L2.  Within a head the last query tile
-  // comes first, so that the long causal rows start early.  tile t - tcu[i]
-  // belongs to packed request i.  The NW waves take the tile's key tiles
-  // round robin, each with its own online softmax, and merge at the end.
-  const int total = a.prefill_tiles * a.n_kv, nq = total >> 3, nr = total & 7;
+  // its K/V rows, share that XCD's L2.  Within a head the last pairs come
+  // first, so that the long causal rows start early.
+  const int np = a.prefill_pairs;
+  const int total = np * a.n_kv, nq = total >> 3, nr = total & 7;
   const int xcd = (int)blockIdx.x & 7;
   const int w = (xcd < nr ? xcd * (nq + 1) : nr * (nq + 1) + (xcd - nr) * nq) + ((int)blockIdx.x >> 3);
-  const int j = w / a.prefill_tiles;
-  const int t = a.prefill_tiles - 1 - (w - j * a.prefill_tiles);
+  const int j = w / np;
+  const int pp = np - 1 - (w - j * np);
+  // packed request i holds pairs [pbase_i, pbase_i + ceil(tiles_i / 2))
   const PackedRows *pk = a.pk;
-  int pi = 0;
-  for (int k = 1; k < pk->n; ++k) pi += t >= pk->tcu[k];
+  int pi = 0, pbase = 0;
+  for (int k = 0; k + 1 < pk->n; ++k) {
+    const int npk = (pk->tcu[k + 1] - pk->tcu[k] + 1) >> 1;
+    if (pi == k && pp >= pbase + npk) {
+      pbase += npk;
+      pi = k + 1;
+    }
+  }
   const int roff = pk->cu[pi], nrows = pk->cu[pi + 1] - roff;
-  const int q0 = (t - pk->tcu[pi]) * QPT;
+  const int ntiles = pk->tcu[pi + 1] - pk->tcu[pi];
   const int req = pk->req[pi];
-  const int sq = q0 + li / G, sh = li % G;  // the lane column's query position and head
-  const bool slot = li < QPT * G && sq < nrows;
-  const int qlast = min(q0 + QPT - 1, nrows - 1);
-  const int n_kt = qlast / 16 + 1;  // key tiles
+  const int lt0 = 2 * (pp - pbase);  // the pair's tiles lt0, lt0 + 1 of the request (the second may not exist)
+  const int sh = li % G;             // the lane column's head
+  int sq[QT];
+  bool slot[QT];
+#pragma unroll
+  for (int s = 0; s < QT; ++s) {
+    sq[s] = (lt0 + s) * QPT + li / G;  // the lane column's query position in tile s
+    slot[s] = lt0 + s < ntiles && li < QPT * G && sq[s] < nrows;
+  }
+  const int qlast = min(min(lt0 + QT, ntiles) * QPT - 1, nrows - 1);  // the pair's last row
+  const int n_kt = qlast / 16 + 1;                                   // key tiles
   // key tiles are read block by block (a block holds a whole number of tiles)
   const int bt = a.kv.bt[req], toff = a.kv.toff[req];
   const int64_t kin = (int64_t)((a.layer * 2) * a.n_kv + j) * bt * HD, vin = kin + (int64_t)a.n_kv * bt * HD;
   const uint16_t *buf = (const uint16_t *)a.kv.buf;
 
-  u32x4 qb[KK];
+  u32x4 qb[QT][KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk)
-    qb[kk] = slot ? ld16((const uint16_t *)a.q + (int64_t)(roff + sq) * a.ld_q + (j * G + sh) * HD + (kk * 4 + lg) * 8)
-                  : u32x4{0u, 0u, 0u, 0u};
+  for (int s = 0; s < QT; ++s)
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      qb[s][kk] = slot[s] ? ld16((const uint16_t *)a.q + (int64_t)(roff + sq[s]) * a.ld_q + (j * G + sh) * HD +
+                                 (kk * 4 + lg) * 8)
+                          : u32x4{0u, 0u, 0u, 0u};
 
-  float m = -INFINITY, l = 0.f;
-  f32x4 o[8];
+  float m[QT], l[QT];
+  f32x4 o[QT][8];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < QT; ++s) {
+    m[s] = -INFINITY;
+    l[s] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) o[s][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
 
   // Key tiles in batches of UB per wave: the wave takes tiles kt0 + u NW +
-  // wave.  Past the tile's last key every load is empty and reads as zero.
+  // wave.  Past the pair's last key every load is empty and reads as zero.
   constexpr int STEP = UB * NW;
   for (int kt0 = 0; kt0 < n_kt; kt0 += STEP) {
     u32x4 kc[UB][KK], vc[UB][4];
@@ -501,7 +526,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
     for (int u = 0; u < UB; ++u) {
       const int p0 = (kt0 + u * NW + wave) * 16, blk = p0 / bt, pb = p0 - blk * bt;
       const int64_t b0 = p0 <= qlast ? a.kv.tab[toff + blk] : -1;
-      // rows of the block up to the tile's last query position; past them, zeros
+      // rows of the block up to the pair's last query position; past them, zeros
       const uint32_t nbytes = b0 < 0 ? 0u : (uint32_t)min(bt, qlast + 1 - blk * bt) * HD * SB;
       const rsrc_t kr = make_rsrc(buf + max(b0, (int64_t)0) + kin, nbytes);
       const rsrc_t vr = make_rsrc(buf + max(b0, (int64_t)0) + vin, nbytes);
@@ -512,95 +537,118 @@ __global__ __launch_bounds__(64 * NW) void k_attn_prefill(AttnArgs a) {
       for (int i = 0; i < 4; ++i)
         vc[u][i] = bld16(vr, li < CPR ? (uint32_t)((pb + 4 * lg + i) * HD + li * 8) * SB : BUF_OOB);
     }
-    // scores of the batch's key tiles, their chains interleaved (past qlast
-    // every score is masked and the state stays as it is)
-    f32x4 sc[UB];
+    // scores of the batch's key tiles for both query tiles, their chains
+    // interleaved (past a row every score is masked and the state stays)
+    f32x4 sc[QT][UB];
 #pragma unroll
-    for (int u = 0; u < UB; ++u) sc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < QT; ++s)
+#pragma unroll
+      for (int u = 0; u < UB; ++u) sc[s][u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
-      for (int u = 0; u < UB; ++u) sc[u] = mma<DT>(kc[u][kk], qb[kk], sc[u]);
-    float sv[UB][4];
-    float tmax = -INFINITY;
+      for (int s = 0; s < QT; ++s)
+#pragma unroll
+        for (int u = 0; u < UB; ++u) sc[s][u] = mma<DT>(kc[u][kk], qb[s][kk], sc[s][u]);
+    u32x2 ph[QT][UB], pl[QT][UB];
+#pragma unroll
+    for (int s = 0; s < QT; ++s) {
+      float sv[UB][4];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int p = (kt0 + u * NW + wave) * 16 + 4 * lg + i;
+          sv[u][i] = slot[s] && p <= sq[s] ? sc[s][u][i] * a.scale : -INFINITY;
+          tmax = fmaxf(tmax, sv[u][i]);
+        }
+      // o / l does not depend on the reference m as long as exp(s - m) stays
+      // in range.  m, the same for the four lanes of a column, is raised to
+      // the column's maximum (and o, l rescaled) only when some score of the
+      // wave passes it by more than RESCALE_SLACK.
+      if (__ballot(tmax > m[s] + RESCALE_SLACK)) {
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        const float mn = fmaxf(m[s], tmax);
+        const float corr = m[s] == -INFINITY ? 0.f : __expf(m[s] - mn);
+        l[s] *= corr;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) o[s][dt] *= corr;
+        m[s] = mn;
+      }
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        ph[s][u] = u32x2{0u, 0u};
+        pl[s][u] = u32x2{0u, 0u};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pr = sv[u][i] == -INFINITY ? 0.f : __expf(sv[u][i] - m[s]);
+          const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr) : f32_to_bf16(pr);
+          const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
+          const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr - hf) : f32_to_bf16(pr - hf);
+          l[s] += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));  // this lane's keys only
+          ph[s][u][i >> 1] |= hb << (16 * (i & 1));
+          pl[s][u][i >> 1] |= lb << (16 * (i & 1));
+        }
+      }
+    }
 #pragma unroll
     for (int u = 0; u < UB; ++u)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int p = (kt0 + u * NW + wave) * 16 + 4 * lg + i;
-        sv[u][i] = slot && p <= sq ? sc[u][i] * a.scale : -INFINITY;
-        tmax = fmaxf(tmax, sv[u][i]);
-      }
-    // o / l does not depend on the reference m as long as exp(s - m) stays in
-    // range.  m, the same for the four lanes of a column, is raised to the
-    // column's maximum (and o, l rescaled) only when some score of the wave
-    // passes it by more than RESCALE_SLACK.
-    if (__ballot(tmax > m + RESCALE_SLACK)) {
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float mn = fmaxf(m, tmax);
-      const float corr = m == -INFINITY ? 0.f : __expf(m - mn);
-      l *= corr;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt] *= corr;
-      m = mn;
-    }
-#pragma unroll
-    for (int u = 0; u < UB; ++u) {
-      u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float pr = sv[u][i] == -INFINITY ? 0.f : __expf(sv[u][i] - m);
-        const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr) : f32_to_bf16(pr);
-        const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
-        const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr - hf) : f32_to_bf16(pr - hf);
-        l += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));  // this lane's keys only
-        ph[i >> 1] |= hb << (16 * (i & 1));
-        pl[i >> 1] |= lb << (16 * (i & 1));
-      }
-#pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         // the 16-bit element dt of keys 4 lg .. 4 lg + 3, low half first
-        const int w = dt >> 1;
+        const int w2 = dt >> 1;
         const uint32_t sel = dt & 1 ? 0x07060302u : 0x05040100u;
         u32x2 av;
-        av[0] = __builtin_amdgcn_perm(vc[u][1][w], vc[u][0][w], sel);
-        av[1] = __builtin_amdgcn_perm(vc[u][3][w], vc[u][2][w], sel);
-        o[dt] = mma16<DT>(av, ph, o[dt]);
-        o[dt] = mma16<DT>(av, pl, o[dt]);
+        av[0] = __builtin_amdgcn_perm(vc[u][1][w2], vc[u][0][w2], sel);
+        av[1] = __builtin_amdgcn_perm(vc[u][3][w2], vc[u][2][w2], sel);
+#pragma unroll
+        for (int s = 0; s < QT; ++s) {
+          o[s][dt] = mma16<DT>(av, ph[s][u], o[s][dt]);
+          o[s][dt] = mma16<DT>(av, pl[s][u], o[s][dt]);
+        }
       }
-    }
   }
   // l so far covers this lane's keys; the column's sum adds the four lanes
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
+#pragma unroll
+  for (int s = 0; s < QT; ++s) {
+    l[s] += __shfl_xor(l[s], 16);
+    l[s] += __shfl_xor(l[s], 32);
+  }
   // merge the waves' states in wave order: M = max m_w, o = sum_w e^(m_w - M) o_w,
-  // l = sum_w e^(m_w - M) l_w
-  __shared__ float s_ml[NW][2][64];
-  __shared__ f32x4 s_o[NW][8][64];
-  s_ml[wave][0][lane] = m;
-  s_ml[wave][1][lane] = l;
+  // l = sum_w e^(m_w - M) l_w; wave s merges query tile s
+  __shared__ float s_ml[NW][QT][2][64];
+  __shared__ f32x4 s_o[NW][QT][8][64];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) s_o[wave][dt][lane] = o[dt];
+  for (int s = 0; s < QT; ++s) {
+    s_ml[wave][s][0][lane] = m[s];
+    s_ml[wave][s][1][lane] = l[s];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) s_o[wave][s][dt][lane] = o[s][dt];
+  }
   __syncthreads();
-  if (wave != 0 || !slot) return;
-  float M = s_ml[0][0][lane];
+  if (wave >= QT) return;
+  const int ms = wave;  // wave-uniform
+  const bool my_slot = ms == 0 ? slot[0] : slot[1];
+  if (!my_slot) return;
+  float M = s_ml[0][ms][0][lane];
 #pragma unroll
-  for (int w = 1; w < NW; ++w) M = fmaxf(M, s_ml[w][0][lane]);
+  for (int w2 = 1; w2 < NW; ++w2) M = fmaxf(M, s_ml[w2][ms][0][lane]);
   float L = 0.f;
   f32x4 O[8];
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) O[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    const float mw = s_ml[w][0][lane];
+  for (int w2 = 0; w2 < NW; ++w2) {
+    const float mw = s_ml[w2][ms][0][lane];
     const float wt = mw == -INFINITY ? 0.f : __expf(mw - M);
-    L += wt * s_ml[w][1][lane];
+    L += wt * s_ml[w2][ms][1][lane];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) O[dt] += wt * s_o[w][dt][lane];
+    for (int dt = 0; dt < 8; ++dt) O[dt] += wt * s_o[w2][ms][dt][lane];
   }
   // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
-  const int64_t orow = roff + sq;
+  const int64_t orow = roff + (ms == 0 ? sq[0] : sq[1]);
   const int ocol = (j * G + sh) * HD;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
@@ -716,7 +764,7 @@ hipError_t combine_dt(int head_dim, int nq, const AttnArgs &a, hipStream_t st) {
 template <int DT, int HD>
 hipError_t prefill_hd(int group, const AttnArgs &a, hipStream_t st) {
   constexpr int NW = 4;  // waves per query tile, taking its key tiles round robin
-  const dim3 grid(a.prefill_tiles * a.n_kv), block(64 * NW);
+  const dim3 grid(a.prefill_pairs * a.n_kv), block(64 * NW);
   switch (group) {
     case 1: HS_LAUNCH((k_attn_prefill<DT, HD, 1, NW>), grid, block, 0, st, a); break;
     case 2: HS_LAUNCH((k_attn_prefill<DT, HD, 2, NW>), grid, block, 0, st, a); break;

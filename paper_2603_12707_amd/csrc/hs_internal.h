@@ -119,6 +119,7 @@ struct AttnArgs {
   int prefill;     // 0: decode (query = column c, request act[c], length = len + 1); 1: prefill rows in *pk
   const PackedRows *pk;  // device copy; query row r of request i has length r - cu[i] + 1
   int prefill_tiles;     // prefill: query tiles in all (pk->tcu[pk->n])
+  int prefill_pairs;     // prefill: pairs of one request's consecutive query tiles, sum of ceil(tiles / 2)
   int S;           // positions per split (pooled caches: a multiple of 256)
   const int *order;  // decode: work-group row z serves column order[z] (longest first); NULL: z
   int n_split;     // splits per (query, kv head)
