@@ -630,7 +630,14 @@ __global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
   __syncthreads();
   if (wave >= QT) return;
   const int ms = wave;  // wave-uniform
-  const bool my_slot = ms == 0 ? slot[0] : slot[1];
+  bool my_slot = false;
+  int my_sq = 0;
+#pragma unroll
+  for (int s = 0; s < QT; ++s)
+    if (s == ms) {
+      my_slot = slot[s];
+      my_sq = sq[s];
+    }
   if (!my_slot) return;
   float M = s_ml[0][ms][0][lane];
 #pragma unroll
@@ -648,7 +655,7 @@ __global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
     for (int dt = 0; dt < 8; ++dt) O[dt] += wt * s_o[w2][ms][dt][lane];
   }
   // lane (c, q) holds rows d = (4 q + i) * 8 + dt of its column's output
-  const int64_t orow = roff + (ms == 0 ? sq[0] : sq[1]);
+  const int64_t orow = roff + my_sq;
   const int ocol = (j * G + sh) * HD;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
