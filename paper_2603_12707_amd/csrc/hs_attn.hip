@@ -54,17 +54,32 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   constexpr int UB = attn_batch(G);       // iterations per batch of loads
   // decode: the longest requests' work groups are dispatched first
   const int split = blockIdx.x, j = blockIdx.y, qi = a.order ? a.order[blockIdx.z] : (int)blockIdx.z;
-  int req, L;
-  if (!a.prefill) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int tg = lane / LPT, c = lane % LPT;
+  // the query chunks are requested first (also by a split past the end,
+  // which does not use them) and unpacked once the batch's K/V loads are in
+  // flight, so their latency overlaps the cache metadata and K/V loads
+  u32x4 qraw[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) qraw[h] = ld16((const S *)a.q + (int64_t)qi * a.ld_q + (j * G + h) * HD + c * CE);
+  // the request's length, capacity and (contiguous cache) first element,
+  // requested together
+  // (16-bit storage prefills through k_attn_prefill: here a.prefill is set
+  // for fp32 alone, and the 16-bit kernels compile the decode path only)
+  int req, last;  // last: the query's position
+  if (DT != HS_F32 || !a.prefill) {
     req = PAGED ? a.kv.act[qi] : qi;
-    L = a.kv.len[req] + 1;
+    last = a.kv.len[req];
   } else {
     const int i = packed_request(a.pk, qi);
     req = a.pk->req[i];
-    L = qi - a.pk->cu[i] + 1;
+    last = qi - a.pk->cu[i];
   }
   const int cap = a.kv.cap[req];
-  L = min(L, cap);
+  const int64_t b_req = PAGED ? 0 : a.kv.tab[req];
+  asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));  // the three loads issued together, one wait
+  const int L = min(last + 1, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;  // first (query, head) row of this group
   if (t0 >= L) {
@@ -80,9 +95,6 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   }
   const int n = min(a.S, L - t0);
   const int n_it = (n + STEP - 1) / STEP;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int tg = lane / LPT, c = lane % LPT;
   // one block per request: the split's rows are one range.  Several blocks:
   // each batch of loads (a whole number of which fills a block) reads the
   // block holding it, whose start is read one batch ahead.
@@ -96,19 +108,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
     vin = kin + (int64_t)a.n_kv * bt * HD;
     b_next = a.kv.tab[toff + t0 / bt];
   } else {
-    const int64_t b = a.kv.tab[req];
-    ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+    ko = b_req + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
     vo = ko + (int64_t)a.n_kv * cap * HD;
   }
   const uint32_t nbytes = (uint32_t)n * HD * SB;
   const rsrc_t kr = make_rsrc((const S *)a.kv.buf + max(ko, (int64_t)0), nbytes);
   const rsrc_t vr = make_rsrc((const S *)a.kv.buf + max(vo, (int64_t)0), nbytes);
 
-  // the query chunks are requested first and unpacked once the batch's K/V
-  // loads are in flight, so their latency overlaps
-  u32x4 qraw[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) qraw[h] = ld16((const S *)a.q + (int64_t)qi * a.ld_q + (j * G + h) * HD + c * CE);
   float qf[G][CE];
 
   float m[G], l[G], o[G][CE];
@@ -255,17 +261,23 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   constexpr int STEP = NW * 16;       // positions per work-group iteration
   // decode: the longest requests' work groups are dispatched first
   const int split = blockIdx.x, j = blockIdx.y, qi = a.order ? a.order[blockIdx.z] : (int)blockIdx.z;
-  int req, L;
-  if (!a.prefill) {
+  // (16-bit storage prefills through k_attn_prefill: here a.prefill is set
+  // for fp32 alone, and the 16-bit kernels compile the decode path only)
+  int req, last;  // last: the query's position
+  if (DT != HS_F32 || !a.prefill) {
     req = PAGED ? a.kv.act[qi] : qi;
-    L = a.kv.len[req] + 1;
+    last = a.kv.len[req];
   } else {
     const int i = packed_request(a.pk, qi);
     req = a.pk->req[i];
-    L = qi - a.pk->cu[i] + 1;
+    last = qi - a.pk->cu[i];
   }
+  // the request's length, capacity and (contiguous cache) first element,
+  // requested together, one wait
   const int cap = a.kv.cap[req];
-  L = min(L, cap);
+  const int64_t b_req = PAGED ? 0 : a.kv.tab[req];
+  asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));
+  const int L = min(last + 1, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;
   if (t0 >= L) {
@@ -297,8 +309,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
     vin = kin + (int64_t)a.n_kv * bt * HD;
     b_next = a.kv.tab[toff + t0 / bt];
   } else {
-    const int64_t b = a.kv.tab[req];
-    ko = b + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
+    ko = b_req + ((int64_t)((a.layer * 2) * a.n_kv + j) * cap + t0) * HD;
     vo = ko + (int64_t)a.n_kv * cap * HD;
   }
   const uint32_t nbytes = (uint32_t)n * HD * SB;
@@ -716,6 +727,7 @@ __global__ __launch_bounds__(HD) void k_combine(AttnArgs a) {
 
 template <int DT, int HD, bool PAGED>
 hipError_t attn_hd(int group, int nq, const AttnArgs &a, hipStream_t st) {
+  if (DT != HS_F32 && a.prefill) return hipErrorInvalidValue;  // 16-bit prefill runs k_attn_prefill
   const dim3 grid(a.n_split, a.n_kv, nq), block(64 * ATTN_WAVES);
   switch (group) {
     case 1: HS_LAUNCH((k_attn<DT, HD, 1, ATTN_WAVES, PAGED>), grid, block, 0, st, a); break;
