@@ -406,6 +406,16 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int li = lane & 15, lq = lane >> 4;
+  // The kernel arguments the first loads are built from, fetched in one
+  // round trip (fetched where first read, behind the column-group branch,
+  // they took three before the first weight load).
+  {
+    const int n_colg = a.n_colg, n_groups = a.n_groups, K0 = a.K, ncols = a.ncols;
+    const int r0 = a.rows[0], r1 = a.rows[1], r2 = a.rows[2];
+    const void *w0 = a.w[0], *w1 = a.w[1], *w2 = a.w[2], *x = a.x, *gain = a.gain;
+    asm volatile("" ::"s"(n_colg), "s"(n_groups), "s"(K0), "s"(ncols), "s"(r0), "s"(r1), "s"(r2), "s"(w0), "s"(w1),
+                 "s"(w2), "s"(x), "s"(gain));
+  }
   // Over several column groups the grid is one-dimensional and ordered so
   // that the column groups of a row group take consecutive slots of one XCD
   // (work groups are dealt to the 8 XCDs round robin): the later groups then
