@@ -415,6 +415,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
     const void *w0 = a.w[0], *w1 = a.w[1], *w2 = a.w[2], *x = a.x, *gain = a.gain;
     asm volatile("" ::"s"(n_colg), "s"(n_groups), "s"(K0), "s"(ncols), "s"(r0), "s"(r1), "s"(r2), "s"(w0), "s"(w1),
                  "s"(w2), "s"(x), "s"(gain));
+    if constexpr (epi_qkv(EPI) || PRO == PRO_COMBINE) {  // the q/k/v row map; the split partials
+      const int hd = a.head_dim, nh = a.n_heads, nkv = a.n_kv, nsp = a.n_split;
+      const float *po = a.part_o, *pm = a.part_ml;
+      asm volatile("" ::"s"(hd), "s"(nh), "s"(nkv), "s"(nsp), "s"(po), "s"(pm));
+    }
   }
   // Over several column groups the grid is one-dimensional and ordered so
   // that the column groups of a row group take consecutive slots of one XCD
