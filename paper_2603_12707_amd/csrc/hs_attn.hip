@@ -78,7 +78,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   }
   const int cap = a.kv.cap[req];
   const int64_t b_req = PAGED ? 0 : a.kv.tab[req];
-  asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));  // the three loads issued together, one wait
+  // the three loads issued together, one wait (a paged cache reads its block
+  // table in the loop, whose loads the pin would turn into vector loads)
+  if constexpr (!PAGED) asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));
   const int L = min(last + 1, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;  // first (query, head) row of this group
@@ -276,7 +278,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
   // requested together, one wait
   const int cap = a.kv.cap[req];
   const int64_t b_req = PAGED ? 0 : a.kv.tab[req];
-  asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));
+  if constexpr (!PAGED) asm volatile("" ::"s"(last), "s"(cap), "s"(b_req));  // as in k_attn
   const int L = min(last + 1, cap);
   const int t0 = split * a.S;
   const int64_t qh = (int64_t)qi * a.n_heads + j * G;
