@@ -151,7 +151,10 @@ int hs_pack_matrix_heads(int32_t dtype, const void *src, int64_t rows, int64_t c
 int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch, int32_t max_ctx, hs_model **out);
 int hs_model_free(hs_model *m);
 
-/* Lays out `batch` requests back to back, in order and without padding, in
+/* The per-request KV cache, taken when a request enters language prefill
+ * (§5.4 "Lazy KV Cache Allocation") and sized by Eq. 1 (§4.1): request b
+ * holds 2 * n_layers * n_kv * head_dim * capacity_b elements.
+ * Lays out `batch` requests back to back, in order and without padding, in
  * the caller-owned device buffer dev_buf, which must hold at least
  * sum_b kv_bytes(capacity_b) bytes.  Request b occupies capacity[b]
  * positions; its KV element (layer l, K|V = s, kv head j, position p,
@@ -234,7 +237,11 @@ int hs_handoff_pending(const hs_handoff *h, int32_t *n);
  * hs_kv_sync when graph replays have taken blocks). */
 int hs_kv_pool_blocks(const hs_kv *kv, int32_t *free_blocks, int32_t *n_blocks);
 
-/* Language prefill of request `req` from its projected visual embedding:
+/* Language prefill of request `req` from its projected visual embedding, the
+ * payload that crosses the modality boundary (§5.1: the embedding [1, N_v, d]
+ * enters the language model; §5.2 "Device Placement": the embedding is put
+ * in the language GPU's HBM just before prefill starts, so this call takes
+ * it as device memory):
  * rows 0..n_v-1 are emb [n_v, d] (device, model dtype), rows n_v..n_v+s_text-1
  * are the embeddings of text_ids [s_text] (device int32, 0 <= id < vocab).
  * RoPE: HS_ROPE_1D uses position r for row r and pos_thw must be NULL;
@@ -280,7 +287,10 @@ int hs_prefill_batch(hs_model *m, hs_kv *kv, int32_t n, const int32_t *reqs, con
  * outputs, normalised rows) to hold `rows` packed prefill rows, so that
  * hs_prefill_batch packs more requests per pass; never shrinks them.  It
  * allocates, and waits for the device to go idle before freeing the old
- * buffers: call it outside any stream capture and not from a serving loop. */
+ * buffers: call it outside any stream capture and not from a serving loop.
+ * When it grows them, a HIP graph captured earlier from this model's decode
+ * steps still holds the freed buffers' addresses: capture it again before
+ * replaying. */
 int hs_model_reserve_rows(hs_model *m, int64_t rows);
 
 /* One greedy decode step for every request of the handle: request b embeds
@@ -303,8 +313,14 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows);
 int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
                    float *hidden_out, hs_stream_t stream);
 
-/* Reads and clears the device-side input flags (bit 0: an out-of-range token
- * id was replaced by 0).  Synchronises the device. */
+/* Reads and clears the device-side flags.  Synchronises the device.
+ *   bit 0 (1): a token id outside [0, vocab) was replaced by 0;
+ *   bit 2 (4): a pooled cache ran out of free blocks inside a replayed decode
+ *              step (the host-side check covers eager calls only).  The
+ *              requests left without a block for their new position keep it
+ *              unstored, attention masks that position, and their outputs
+ *              from that step on are not the model's: release requests or
+ *              give the pool room before replaying again. */
 int hs_model_status(hs_model *m, int32_t *flags);
 
 /* ---- kernel replay (measurement hook) ---- */

@@ -731,26 +731,16 @@ int hs_kv_pool_create(hs_model *m, int32_t slots, int32_t block_tokens, void *de
   if (n_blocks < 1 || n_blocks > (1u << 30))
     return fail(HS_E_BUFFER, "hs_kv_pool_create: buffer holds %llu blocks of %llu bytes",
                 (unsigned long long)n_blocks, (unsigned long long)block_bytes);
-  // attention partials for the block-aligned splits
-  int64_t entries = m->part_entries;
+  // attention partials for the block-aligned splits: a pooled split is the
+  // unpooled one rounded up to whole POOL_SPANs, so it never needs more
+  // partials than hs_model_create sized for (and nothing here reallocates a
+  // workspace that a captured decode graph may hold)
   for (int nq = 1; nq <= std::min(slots, m->max_batch); ++nq) {
     int S, ns;
     kv_split_policy(c, true, nq, m->max_ctx, &S, &ns);
-    if (ns > 1) entries = std::max(entries, (int64_t)nq * c.n_heads * ns);
-  }
-  if (entries > m->part_entries) {
-    float *po = nullptr, *pm = nullptr;
-    if (hipMalloc(&po, (size_t)entries * c.head_dim * 4) != hipSuccess ||
-        hipMalloc(&pm, (size_t)entries * 2 * 4) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-      if (po) (void)hipFree(po);
-      if (pm) (void)hipFree(pm);
-      return fail(HS_E_DEVICE, "hs_kv_pool_create: attention workspace allocation failed");
-    }
-    (void)hipFree(m->part_o);
-    (void)hipFree(m->part_ml);
-    m->part_o = po;
-    m->part_ml = pm;
-    m->part_entries = entries;
+    if (ns > 1 && (int64_t)nq * c.n_heads * ns > m->part_entries)
+      return fail(HS_E_INVALID, "hs_kv_pool_create: %d queries x %d splits exceed the model's attention workspace",
+                  nq, ns);
   }
   hs_kv *kv = new (std::nothrow) hs_kv();
   if (!kv) return fail(HS_E_DEVICE, "hs_kv_pool_create: out of host memory");

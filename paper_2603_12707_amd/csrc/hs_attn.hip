@@ -133,8 +133,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
     u32x4 kc[UB], vc[UB];
     rsrc_t kb = kr, vb = vr;
     int rel = 0;
+    bool blk_ok = true;  // a paged batch's block is held (a pool that ran dry leaves it unheld)
     if constexpr (PAGED) {
       const int64_t b0 = b_next;
+      blk_ok = b0 >= 0;
       const int pb = t0 + it0 * STEP, pn = pb + UB * STEP;
       b_next = pn < t0 + n ? a.kv.tab[toff + pn / bt] : 0;
       const int64_t at = max(b0, (int64_t)0) + (int64_t)(pb % bt) * HD;
@@ -158,7 +160,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
       const int tt = (it0 + u) * STEP + wave * TPW + tg;
-      const bool valid = tt < n;
+      const bool valid = tt < n && blk_ok;  // positions of an unheld block are masked
       float kf[CE], vf[CE];
       unpack<DT>(kc[u], kf);
       unpack<DT>(vc[u], vf);
@@ -336,8 +338,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
     u32x4 kc[UB][KK], vc[UB][4];
     rsrc_t kb = kr, vb = vr;
     int rel = 0;
+    bool blk_ok = true;  // as in k_attn
     if constexpr (PAGED) {
       const int64_t b0 = b_next;
+      blk_ok = b0 >= 0;
       const int pb = t0 + it0 * STEP, pn = pb + UB * STEP;
       b_next = pn < t0 + n ? a.kv.tab[toff + pn / bt] : 0;
       const int64_t at = max(b0, (int64_t)0) + (int64_t)(pb % bt) * HD;
@@ -366,7 +370,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
       float tmax = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        sv[i] = p0 + 4 * lg + i < n ? sc[i] * a.scale : -INFINITY;
+        sv[i] = p0 + 4 * lg + i < n && blk_ok ? sc[i] * a.scale : -INFINITY;
         tmax = fmaxf(tmax, sv[i]);
       }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));

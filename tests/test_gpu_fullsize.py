@@ -26,6 +26,8 @@ from oracle import oracle as O
 from workload import configs, synth
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow, pytest.mark.timeout(900)]
+# positions bench.py allocates after each request's context (its default run)
+BENCH_TAIL = bench.steps_after_context(bench.DEFAULT_WARMUP, bench.DEFAULT_STEPS)
 TDT = {"f16": torch.float16, "bf16": torch.bfloat16, "f32": torch.float32}
 
 
@@ -129,7 +131,7 @@ def test_llava7b_b1_bench_configuration(llava):
     cfg, w_cpu, w_gpu = llava
     n_v, s_text = synth.request_lengths(cfg)
     ctx = n_v[0] + s_text[0]
-    cap = ctx + bench.steps_after_context(bench.DEFAULT_WARMUP, bench.DEFAULT_STEPS)
+    cap = ctx + BENCH_TAIL
     model = hs.Model(cfg, w_gpu, max_batch=1, max_ctx=cap, packed=True)
     # prefill from the real inputs
     kv = hs.KVCache(model, n_v, [cap])
@@ -159,7 +161,7 @@ def test_llava7b_b32_sampled_requests(llava):
     cfg = configs.get("llava7b_b32")
     n_v, s_text = synth.request_lengths(cfg)
     lens = [a + b for a, b in zip(n_v, s_text)]
-    caps = [n + 4 for n in lens]
+    caps = [n + BENCH_TAIL for n in lens]
     model = hs.Model(cfg, w_gpu, max_batch=32, max_ctx=max(caps), packed=True)
     kv = hs.KVCache(model, n_v, caps)
     sample = [0, 17, 31]
@@ -191,7 +193,7 @@ def test_qwen7b_b16_sampled_requests_mrope(qwen):
     cfg, w_cpu, w_gpu = qwen
     n_v, s_text = synth.request_lengths(cfg)
     lens = [a + b for a, b in zip(n_v, s_text)]
-    caps = [n + 4 for n in lens]
+    caps = [n + BENCH_TAIL for n in lens]
     model = hs.Model(cfg, w_gpu, max_batch=16, max_ctx=max(caps), packed=True)
     kv = hs.KVCache(model, n_v, caps)
     r0 = 3
@@ -227,7 +229,7 @@ def test_qwen_layer_b256_sampled_requests(pool_block):
     cfg = configs.get("qwen_layer_b256")
     w_cpu, w_gpu = _weights(cfg)
     lens = synth.kv_lengths(cfg)
-    caps = [n + 4 for n in lens]
+    caps = [n + BENCH_TAIL for n in lens]
     model = hs.Model(cfg, w_gpu, max_batch=256, max_ctx=max(caps), packed=True)
     if pool_block:
         kv = hs.KVPool(model, 256, pool_block, sum((c + pool_block - 1) // pool_block for c in caps))

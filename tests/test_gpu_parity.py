@@ -330,7 +330,8 @@ def test_prefill_then_decode_matches_longer_prefill(rope_kind):
 def test_decode_step_replays_from_a_hip_graph(case):
     """hs_decode_step recorded by stream capture (two steps, ping-ponging the
     token buffers) and replayed gives, replay after replay, the tokens and
-    logits of eager calls on an identical cache; eager work and
+    logits of eager calls on an identical cache, and the replayed logits of
+    sampled requests agree with the oracle fed the same tokens; eager work and
     synchronisation run between the replays.  Cases: 3 requests (activations
     staged in LDS), 20 requests at d = 1024 (packed activations read from
     memory), 150 requests (the weight-stationary gate/up and LM head)."""
@@ -367,6 +368,24 @@ def test_decode_step_replays_from_a_hip_graph(case):
         ref_tok.append(b.cpu().clone())
         ref_log.append(lg.cpu().clone())
         a, b = b, a
+    # the oracle on sampled requests, fed the tokens every step was fed
+    sample = sorted({0, B // 2, B - 1})
+    seqs = {}
+    for r in sample:
+        emb, ids, _ = pair.request_inputs(r, n_v[r], s_text[r])
+        seqs[r] = pair.ora.new_seq(caps[r])
+        seqs[r].prefill(emb if n_v[r] else None, ids)
+    feeds = [t_e.cpu().clone()] + ref_tok[:-1]
+    near = 0
+
+    def check_oracle(step, g_log, g_tok):
+        nonlocal near
+        for r in sample:
+            r_log, _, _ = seqs[r].decode(int(feeds[step][r]))
+            assert rel_err(g_log[r].numpy(), r_log) <= LOGIT_TOL, (step, r, rel_err(g_log[r].numpy(), r_log))
+            ok, tie = token_ok(int(g_tok[r]), g_log[r].numpy(), r_log)
+            assert ok, (step, r)
+            near += tie
     # captured: two steps per graph, replayed four times
     kv_g, t_g = handles[1]
     ga, gb = t_g.clone(), torch.empty_like(t_g)
@@ -387,6 +406,9 @@ def test_decode_step_replays_from_a_hip_graph(case):
         assert torch.equal(ga.cpu(), ref_tok[2 * k + 1]), k
         assert torch.equal(lg1.cpu(), ref_log[2 * k]), k
         assert torch.equal(lg2.cpu(), ref_log[2 * k + 1]), k
+        check_oracle(2 * k, lg1.cpu(), gb.cpu())
+        check_oracle(2 * k + 1, lg2.cpu(), ga.cpu())
+    assert near <= 1
     kv_g.sync()
     assert kv_g.lengths() == kv_e.lengths() == [n + s + 8 for n, s in zip(n_v, s_text)]
     for kv, _ in handles:

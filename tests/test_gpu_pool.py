@@ -213,8 +213,9 @@ def test_pool_layer0_rows_bit_identical_to_contiguous_cache():
 
 def test_pool_graph_replays_take_blocks_on_the_device():
     """Two decode steps captured once, replayed four times: the requests
-    cross block boundaries inside the replays, and the caches, lengths and
-    free blocks match an identical pool driven by eager calls bit for bit."""
+    cross block boundaries inside the replays, the caches, lengths and free
+    blocks match an identical pool driven by eager calls bit for bit, and the
+    replayed logits agree with the oracle fed the same tokens."""
     import paper_2603_12707_amd as hs
     cfg = small_cfg(n_layers=1, dtype="bf16")
     pair = Pair(cfg, max_batch=2, max_ctx=400)
@@ -233,21 +234,43 @@ def test_pool_graph_replays_take_blocks_on_the_device():
     ga, gb = firsts[1].clone(), torch.empty_like(firsts[1])
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
+    V = cfg["vocab"]
+    lg1, lg2 = torch.empty(2, V, device="cuda"), torch.empty(2, V, device="cuda")
     with torch.cuda.stream(s):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=s):
-            graphed.decode(ga, gb)
-            graphed.decode(gb, ga)
+            graphed.decode(ga, gb, lg1)
+            graphed.decode(gb, ga, lg2)
     torch.cuda.current_stream().wait_stream(s)
     graphed.sync()
     assert graphed.lengths() == [254, 253]  # capture ran nothing
+    # the oracle, fed the tokens each replayed step was fed
+    seqs = []
+    for r, (n_v, s_text) in enumerate(shapes):
+        emb, ids, _ = inputs[r]
+        seqs.append(pair.ora.new_seq(300))
+        seqs[-1].prefill(emb if n_v else None, ids)
+    near = 0
+
+    def check_oracle(feed, g_log, g_tok):
+        nonlocal near
+        for r in range(2):
+            r_log, _, _ = seqs[r].decode(feed[r])
+            assert rel_err(g_log[r], r_log) <= LOGIT_TOL, (r, rel_err(g_log[r], r_log))
+            ok, tie = token_ok(g_tok[r], g_log[r], r_log)
+            assert ok, r
+            near += tie
     for rep in range(4):
+        feed0 = ga.tolist()
         g.replay()
         for _ in range(2):
             eager.decode(ta, tb)
             ta, tb = tb, ta
         torch.cuda.synchronize()
         assert ga.tolist() == ta.tolist(), rep
+        check_oracle(feed0, lg1.cpu().numpy(), gb.tolist())
+        check_oracle(gb.tolist(), lg2.cpu().numpy(), ga.tolist())
+    assert near <= 1
     graphed.sync()
     assert graphed.lengths() == eager.lengths() == [262, 261]
     assert graphed.blocks() == eager.blocks() == (8 - 4, 8)
@@ -258,6 +281,58 @@ def test_pool_graph_replays_take_blocks_on_the_device():
         eager.read(r, 0, 1, 0, 0, n, a)
         graphed.read(r, 0, 1, 0, 0, n, b)
         assert torch.equal(a.view(torch.int16), b.view(torch.int16)), r
+
+
+def test_pool_running_dry_inside_replays_is_flagged():
+    """A pool with no spare block and a captured decode step replayed until
+    request 0's next position needs a block that is not there: that step sets
+    status bit 2, every kernel completes, request 0's outputs stay finite (its
+    new position unstored and masked from attention), request 1, whose block
+    suffices, keeps agreeing with the oracle fed the same tokens, and an eager
+    step is then refused by the host-side check."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=1, dtype="bf16")
+    pair = Pair(cfg, max_batch=2, max_ctx=400)
+    pool = hs.KVPool(pair.gpu, 2, BT, 2)  # one block each after prefill, none free
+    shapes = [(20, 230), (0, 100)]  # contexts 250 and 100
+    inputs = [pair.request_inputs(r, n, s) for r, (n, s) in enumerate(shapes)]
+    for slot, (n_v, s_text) in enumerate(shapes):
+        pool.admit(slot, n_v, 300)
+    first = pool.prefill_batch([0, 1], inputs[0][0].cuda(), torch.cat([inputs[0][1], inputs[1][1]]).cuda(),
+                               [230, 100])
+    torch.cuda.synchronize()
+    assert pool.blocks() == (0, 2)
+    seq1 = pair.ora.new_seq(300)
+    seq1.prefill(None, inputs[1][1])
+    V = cfg["vocab"]
+    ga, gb = first.clone(), torch.empty_like(first)
+    lg1, lg2 = torch.empty(2, V, device="cuda"), torch.empty(2, V, device="cuda")
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=st):
+            pool.decode(ga, gb, lg1)
+            pool.decode(gb, ga, lg2)
+    torch.cuda.current_stream().wait_stream(st)
+    assert pair.gpu.status() == 0
+    for rep in range(4):  # request 0 writes positions 250 + 2 rep and 251 + 2 rep
+        feed0 = ga.tolist()
+        g.replay()
+        torch.cuda.synchronize()
+        feed1 = gb.tolist()
+        flags = pair.gpu.status()
+        assert flags == (4 if rep == 3 else 0), (rep, flags)
+        for feed, lg, out in ((feed0, lg1, feed1), (feed1, lg2, ga.tolist())):
+            lg = lg.cpu().numpy()
+            assert np.all(np.isfinite(lg))
+            assert all(0 <= t < V for t in out)
+            r_log, _, _ = seq1.decode(feed[1])
+            assert rel_err(lg[1], r_log) <= LOGIT_TOL, (rep, rel_err(lg[1], r_log))
+    pool.sync()
+    assert pool.lengths() == [258, 108]
+    with pytest.raises(hs.HsError):
+        pool.decode(ga, gb)
 
 
 def test_pool_capacity_and_admission_errors():

@@ -4,7 +4,8 @@ Model shapes follow the two backbones of the paper's evaluation (§6.1
 "Models"): a LLaVA-1.5-7B language model (Vicuna-7B: 32 layers, MHA with 32
 KV heads) and a Qwen2.5-VL-7B language model (28 layers, GQA with 4 KV heads,
 dynamic visual token counts).  The remaining hyper-parameters are those of the
-public model cards; every weight is random.  Each request stands in for one
+public model cards (the Qwen-shaped model keeps its q/k/v biases); every
+weight is random.  Each request stands in for one
 image plus a short prompt and at most 128 generated tokens (§6.1
 "Workload"); COCO images are replaced by seeded N(0, 1) vision rows.
 """
@@ -16,7 +17,7 @@ LLAVA7B = dict(n_layers=32, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=12
                rope_theta=1e4, rms_eps=1e-5, rope_kind=0, mrope_section=(0, 0, 0), qkv_bias=0, dtype="f16")
 QWEN25VL7B = dict(n_layers=28, d_model=3584, n_heads=28, n_kv_heads=4, head_dim=128, ffn_dim=18944,
                   vocab=152064, rope_theta=1e6, rms_eps=1e-6, rope_kind=1, mrope_section=(16, 24, 24),
-                  qkv_bias=0, dtype="bf16")
+                  qkv_bias=1, dtype="bf16")
 
 CONFIGS = {
     # tiny fp32 decoder, batch 1: 576 vision rows + 32 text tokens, 16 greedy steps
