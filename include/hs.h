@@ -313,6 +313,24 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows);
 int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
                    float *hidden_out, hs_stream_t stream);
 
+/* hs_decode_step for callers that cannot allocate device memory (code under
+ * stream capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * step's scratch -- residual stream, q / attention / SwiGLU / normalised-row
+ * activations, K-split and attention-split partials, and the logits when
+ * `logits` is NULL -- lives in one static device array of
+ * HS_STATIC_SCRATCH_BYTES per GPU, held from the first call on that GPU
+ * until the process ends, instead of the model's workspaces.  Arguments,
+ * checks and results are those of hs_decode_step (the same kernels).  The
+ * call allocates nothing; a step whose scratch would exceed the array (for
+ * instance batch * vocab fp32 logits with logits NULL) fails with
+ * HS_E_INVALID before any launch.  Every call on a GPU shares that GPU's
+ * array: calls that overlap on one GPU (several streams, several host
+ * threads) race, and the array keeps the last call's contents.  The
+ * current device must be the model's. */
+#define HS_STATIC_SCRATCH_BYTES (64ull << 20)
+int hs_decode_step_static(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
+                          float *hidden_out, hs_stream_t stream);
+
 /* Reads and clears the device-side flags.  Synchronises the device.
  *   bit 0 (1): a token id outside [0, vocab) was replaced by 0;
  *   bit 2 (4): a pooled cache ran out of free blocks inside a replayed decode

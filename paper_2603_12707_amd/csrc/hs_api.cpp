@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "hs_internal.h"
@@ -152,7 +153,25 @@ void free_model(hs_model *m) {
   delete m;
 }
 
-// The launches of one pass over ncols activation rows held in m->x: decode
+// The device scratch one pass works in: the residual stream, the q,
+// attention, SwiGLU and normalised-row activations, the K-split and
+// attention-split partials, and the logits the LM head writes when the caller
+// passes no buffer.  Normally the model's workspaces (hs_model_create);
+// hs_decode_step_static carves them from a static device array instead.
+struct StepWs {
+  float *x;
+  void *q, *attn, *act, *hnorm;
+  float *splitk;
+  int64_t splitk_floats;
+  float *part_o, *part_ml;
+  float *logits;
+};
+
+StepWs model_ws(const hs_model *m) {
+  return StepWs{m->x, m->q, m->attn, m->act, m->hnorm, m->splitk, m->splitk_floats, m->part_o, m->part_ml, m->logits};
+}
+
+// The launches of one pass over ncols activation rows held in ws.x: decode
 // (one row per request, prefill = 0) or prefill (the packed rows of the
 // requests in pk).  Each member launches one kernel.
 struct Step {
@@ -164,6 +183,7 @@ struct Step {
   int rope_ld;
   int S, n_split;
   hipStream_t st;
+  StepWs ws;
 
   hipError_t qkv(int l) const {
     const hs_config &c = m->cfg;
@@ -181,11 +201,11 @@ struct Step {
     g.rows[1] = g.rows[2] = c.n_kv_heads * c.head_dim;
     g.K = c.d_model;
     g.ncols = ncols;
-    g.x = m->x;
+    g.x = ws.x;
     g.gain = W.attn_norm;
-    g.h_work = m->hnorm;
+    g.h_work = ws.hnorm;
     g.eps = c.rms_eps;
-    g.out = m->q;
+    g.out = ws.q;
     g.ld_out = c.n_heads * c.head_dim;
     g.head_dim = c.head_dim;
     g.n_heads = c.n_heads;
@@ -202,15 +222,15 @@ struct Step {
     g.rope_tab = m->rope_tab;
     g.rope_max = m->max_ctx;
     g.status = m->status;
-    g.splitk_ws = m->splitk;
-    g.splitk_cap = m->splitk_floats;
+    g.splitk_ws = ws.splitk;
+    g.splitk_cap = ws.splitk_floats;
     return launch_gemm(c.dtype, PRO_NORM, kv->pool ? EPI_QKV_PAGED : EPI_QKV, g, st);
   }
 
   AttnArgs attn_args(int l) const {
     const hs_config &c = m->cfg;
     AttnArgs a{};
-    a.q = m->q;
+    a.q = ws.q;
     a.ld_q = c.n_heads * c.head_dim;
     a.kv = kv_ref(kv);
     a.layer = l;
@@ -223,11 +243,11 @@ struct Step {
     for (int i = 0; i < pk.n; ++i) a.prefill_pairs += (pk.tcu[i + 1] - pk.tcu[i] + 1) / 2;
     a.S = S;
     a.n_split = n_split;
-    a.part_o = m->part_o;
-    a.part_ml = m->part_ml;
+    a.part_o = ws.part_o;
+    a.part_ml = ws.part_ml;
     a.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
     a.order = !prefill && ncols > 1 ? kv->d_order : nullptr;
-    a.out = m->attn;
+    a.out = ws.attn;
     // in the layout the O projection reads
     a.out_packed = gemm_x_packed(c.dtype, ncols, c.n_heads * c.head_dim) ? 1 : 0;
     return a;
@@ -262,28 +282,28 @@ struct Step {
     o.ncols = ncols;
     o.x = x;
     o.x_packed = x_packed;
-    o.resid = m->x;
+    o.resid = ws.x;
     o.ld_resid = c.d_model;
-    o.splitk_ws = m->splitk;
-    o.splitk_cap = m->splitk_floats;
+    o.splitk_ws = ws.splitk;
+    o.splitk_cap = ws.splitk_floats;
     return launch_gemm(c.dtype, PRO_PLAIN, EPI_RESID, o, st);
   }
 
   hipError_t oproj(int l) const {
     const hs_config &c = m->cfg;
     const int ko = c.n_heads * c.head_dim;
-    if (!combine_fused()) return residual(m->layers[l].wo, ko, m->attn, gemm_x_packed(c.dtype, ncols, ko) ? 1 : 0);
+    if (!combine_fused()) return residual(m->layers[l].wo, ko, ws.attn, gemm_x_packed(c.dtype, ncols, ko) ? 1 : 0);
     GemmArgs o{};
     o.w[0] = m->layers[l].wo;
     o.rows[0] = c.d_model;
     o.K = c.n_heads * c.head_dim;
     o.ncols = ncols;
-    o.part_o = m->part_o;
-    o.part_ml = m->part_ml;
+    o.part_o = ws.part_o;
+    o.part_ml = ws.part_ml;
     o.n_split = n_split;
     o.head_dim = c.head_dim;
     o.n_heads = c.n_heads;
-    o.resid = m->x;
+    o.resid = ws.x;
     o.ld_resid = c.d_model;
     return launch_gemm(c.dtype, PRO_COMBINE, EPI_RESID, o, st);
   }
@@ -297,11 +317,11 @@ struct Step {
     u.rows[0] = u.rows[1] = c.ffn_dim;
     u.K = c.d_model;
     u.ncols = ncols;
-    u.x = m->x;
+    u.x = ws.x;
     u.gain = W.mlp_norm;
-    u.h_work = m->hnorm;
+    u.h_work = ws.hnorm;
     u.eps = c.rms_eps;
-    u.out = m->act;
+    u.out = ws.act;
     // in the layout the down projection reads
     u.out_packed = gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0;
     u.ld_out = c.ffn_dim;
@@ -310,7 +330,7 @@ struct Step {
 
   hipError_t down(int l) const {
     const hs_config &c = m->cfg;
-    return residual(m->layers[l].w_down, c.ffn_dim, m->act, gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0);
+    return residual(m->layers[l].w_down, c.ffn_dim, ws.act, gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0);
   }
 
   // final RMSNorm + LM head over ncols rows starting at x_rows
@@ -323,7 +343,7 @@ struct Step {
     g.ncols = ncols;
     g.x = x_rows;
     g.gain = m->w.final_norm;
-    g.h_work = m->hnorm;
+    g.h_work = ws.hnorm;
     g.eps = c.rms_eps;
     g.out = logits;
     g.ld_out = c.vocab;
@@ -364,7 +384,7 @@ int decode_step_args(hs_model *m, hs_kv *kv, hipStream_t st, Step *out, int *blo
   kv_split_policy(c, kv->pool, B, kv->max_cap, &S, &ns);
   if (ns > 1 && (int64_t)B * c.n_heads * ns > m->part_entries)
     return fail(HS_E_INVALID, "decode: attention workspace too small");
-  *out = Step{m, kv, B, 0, PackedRows{}, kv->d_rope, B, S, ns, st};
+  *out = Step{m, kv, B, 0, PackedRows{}, kv->d_rope, B, S, ns, st, model_ws(m)};
   return HS_OK;
 }
 
@@ -447,7 +467,7 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     }
     // every row is its own query over the rows before it in its request; no
     // splits (S covers the longest request)
-    Step pre{m, kv, rows, 1, pk, pos_thw ? pos_thw + roff : nullptr, (int)total, rows, 1, st};
+    Step pre{m, kv, rows, 1, pk, pos_thw ? pos_thw + roff : nullptr, (int)total, rows, 1, st, model_ws(m)};
     const int rc = pre.layers();
     if (rc) return rc;
     HIP_TRY(launch_gather_last(m->x, c.d_model, pk, m->xlast, st));
@@ -617,8 +637,13 @@ int hs_model_create(const hs_config *cfg, const hs_weights *w, int32_t max_batch
       tab[((size_t)p * (hd / 2) + i) * 2] = (float)std::cos(ang);
       tab[((size_t)p * (hd / 2) + i) * 2 + 1] = (float)std::sin(ang);
     }
+  // activations read in the packed layout are read in whole k-blocks of 128,
+  // past K against zero weight rows: those elements must hold finite values
+  // (they are never written, so cleared once here)
   if (hipMemcpy(m->rope_tab, tab.data(), tab.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemset(m->status, 0, 4) != hipSuccess) {
+      hipMemset(m->status, 0, 4) != hipSuccess || hipMemset(m->attn, 0, (size_t)act_elems(rows, nh * hd) * b) ||
+      hipMemset(m->act, 0, (size_t)act_elems(rows, c.ffn_dim) * b) ||
+      hipMemset(m->hnorm, 0, (size_t)act_elems(rows, c.d_model) * b)) {
     free_model(m);
     return fail(HS_E_DEVICE, "hs_model_create: initial copies failed");
   }
@@ -864,8 +889,10 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows) {
         if (p) (void)hipFree(p);
       return fail(HS_E_DEVICE, "hs_model_reserve_rows: hipMalloc of %zu bytes failed", bytes[i]);
     }
-  // the old buffers may still be in use by queued work
-  if (hipDeviceSynchronize() != hipSuccess) {
+  // the old buffers may still be in use by queued work; the packed-layout
+  // activations start cleared (as in hs_model_create)
+  if (hipDeviceSynchronize() != hipSuccess || hipMemset(fresh[2], 0, bytes[2]) != hipSuccess ||
+      hipMemset(fresh[3], 0, bytes[3]) != hipSuccess || hipMemset(fresh[4], 0, bytes[4]) != hipSuccess) {
     for (void *p : fresh) (void)hipFree(p);
     return fail(HS_E_DEVICE, "hs_model_reserve_rows: device synchronisation failed");
   }
@@ -878,34 +905,37 @@ int hs_model_reserve_rows(hs_model *m, int64_t rows) {
   return HS_OK;
 }
 
-int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
-                   float *hidden_out, hs_stream_t stream) {
-  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "hs_decode_step: model/handle mismatch");
-  if (!tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_in is NULL");
+// One decode step (hs_decode_step); ovr, when given, replaces the model's
+// workspaces as the step's scratch.
+static int decode_impl(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
+                       float *hidden_out, hs_stream_t stream, const StepWs *ovr, const char *fn) {
+  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "%s: model/handle mismatch", fn);
+  if (!tokens_in) return fail(HS_E_INVALID, "%s: tokens_in is NULL", fn);
   const hs_config &c = m->cfg;
   if (m->w.lm_head) {
-    if (!tokens_out) return fail(HS_E_INVALID, "hs_decode_step: tokens_out is NULL");
-    if (tokens_out == tokens_in) return fail(HS_E_INVALID, "hs_decode_step: tokens_out aliases tokens_in");
+    if (!tokens_out) return fail(HS_E_INVALID, "%s: tokens_out is NULL", fn);
+    if (tokens_out == tokens_in) return fail(HS_E_INVALID, "%s: tokens_out aliases tokens_in", fn);
   } else if (logits) {
-    return fail(HS_E_INVALID, "hs_decode_step: model has no LM head, logits must be NULL");
+    return fail(HS_E_INVALID, "%s: model has no LM head, logits must be NULL", fn);
   }
   hipStream_t st = (hipStream_t)stream;
   Step step;
   int need = 0;
   int rc = decode_step_args(m, kv, st, &step, &need);
   if (rc) return rc;
+  if (ovr) step.ws = *ovr;
   const int B = kv->n_active;
   // a pooled request entering a new block takes it now, on the device
   if (kv->pool) HIP_TRY(launch_kv_reserve(kv_pool(kv), KvReserve{}, B, st));
   const int *act = kv->pool ? kv->d_act : nullptr;  // a contiguous cache decodes request c in column c
-  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, act, B, m->x, m->status, st));
+  HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, act, B, step.ws.x, m->status, st));
   rc = step.layers();
   if (rc) return rc;
   if (hidden_out)
-    HIP_TRY(hipMemcpyAsync(hidden_out, m->x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
+    HIP_TRY(hipMemcpyAsync(hidden_out, step.ws.x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
   if (m->w.lm_head) {
-    float *lg = logits ? logits : m->logits;
-    HIP_TRY(step.head(m->x, lg));
+    float *lg = logits ? logits : step.ws.logits;
+    HIP_TRY(step.head(step.ws.x, lg));
     HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, act, kv->d_len, kv->d_rope, 1, st));
   } else {
     HIP_TRY(launch_advance(kv->d_len, kv->d_rope, act, B, st));
@@ -919,6 +949,97 @@ int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *to
     kv->len[b] += 1;
   }
   return HS_OK;
+}
+
+int hs_decode_step(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out, float *logits,
+                   float *hidden_out, hs_stream_t stream) {
+  return decode_impl(m, kv, tokens_in, tokens_out, logits, hidden_out, stream, nullptr, "hs_decode_step");
+}
+
+// ---- the decode step with its scratch in a static device array ----
+//
+// scratch is a file-scope device array; every GPU the library runs on holds
+// its own copy until the process ends.  In host code its name is a stand-in,
+// not a device address: each device's address is looked up once, with that
+// device current, and only that address is handed to kernels and copies.
+static __device__ __align__(256) unsigned char scratch[HS_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+
+// the current device's copy of the scratch array (looked up once per device)
+int scratch_ptr(int dev, void **out) {
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return fail(HS_E_INVALID, "hs_decode_step_static: device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(HS_E_DEVICE, "hs_decode_step_static: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HS_OK;
+}
+}  // namespace
+
+extern "C" int hs_decode_step_static(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t *tokens_out,
+                                     float *logits, float *hidden_out, hs_stream_t stream) {
+  static const char *fn = "hs_decode_step_static";
+  if (!kv_matches(kv, m)) return fail(HS_E_INVALID, "%s: model/handle mismatch", fn);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(HS_E_DEVICE, "%s: no current device", fn);
+  if (dev != m->device) return fail(HS_E_INVALID, "%s: the current device %d is not the model's (%d)", fn, dev,
+                                    m->device);
+  const hs_config &c = m->cfg;
+  const int B = kv->n_active;
+  if (B <= 0) return fail(HS_E_STATE, "%s: no prefilled request", fn);
+  int S, ns;
+  kv_split_policy(c, kv->pool, B, kv->max_cap, &S, &ns);
+  // the step's scratch, carved in 256-byte aligned pieces
+  const int64_t b = dtype_bytes(c.dtype), nhd = (int64_t)c.n_heads * c.head_dim;
+  const int64_t qkv_rows = (int64_t)(c.n_heads + 2 * c.n_kv_heads) * c.head_dim;
+  const int64_t splitk_floats = (int64_t)SPLITK_MAX * B * std::max<int64_t>(c.d_model, qkv_rows);
+  const int64_t entries = ns > 1 ? (int64_t)B * c.n_heads * ns : 1;
+  const uint64_t sizes[10] = {(uint64_t)B * c.d_model * 4,
+                              (uint64_t)(B * nhd * b),
+                              (uint64_t)(act_elems(B, nhd) * b),
+                              (uint64_t)(act_elems(B, c.ffn_dim) * b),
+                              (uint64_t)(act_elems(B, c.d_model) * b),
+                              (uint64_t)splitk_floats * 4,
+                              (uint64_t)entries * c.head_dim * 4,
+                              (uint64_t)entries * 2 * 4,
+                              (m->w.lm_head && !logits) ? (uint64_t)B * c.vocab * 4 : 0u,
+                              0u};
+  uint64_t offs[10], total = 0;
+  for (int i = 0; i < 10; ++i) {
+    offs[i] = total;
+    total += (sizes[i] + 255) / 256 * 256;
+  }
+  if (total > HS_STATIC_SCRATCH_BYTES)
+    return fail(HS_E_INVALID, "%s: this step needs %llu bytes of scratch, the static array holds %llu", fn,
+                (unsigned long long)total, (unsigned long long)HS_STATIC_SCRATCH_BYTES);
+  void *base = nullptr;
+  int rc = scratch_ptr(dev, &base);
+  if (rc) return rc;
+  char *p = (char *)base;
+  StepWs ws{(float *)(p + offs[0]), p + offs[1], p + offs[2], p + offs[3], p + offs[4], (float *)(p + offs[5]),
+            splitk_floats, (float *)(p + offs[6]), (float *)(p + offs[7]),
+            sizes[8] ? (float *)(p + offs[8]) : nullptr};
+  // The array keeps whatever the last call left.  The activations read in the
+  // packed layout are read in whole k-blocks of 128 elements, past K up to
+  // the block's end, against weight rows that are zero there: those elements
+  // must hold finite values, so a K that is not a multiple of 128 has its
+  // buffer cleared first.  Everything else a step reads it writes first.
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t ks[3] = {nhd, c.ffn_dim, c.d_model};
+  void *bufs[3] = {ws.attn, ws.act, ws.hnorm};
+  for (int i = 0; i < 3; ++i)
+    if (ks[i] % 128 && gemm_x_packed(c.dtype, B, (int)ks[i]))
+      HIP_TRY(launch_zero(bufs[i], sizes[2 + i], st));
+  return decode_impl(m, kv, tokens_in, tokens_out, logits, hidden_out, stream, &ws, fn);
 }
 
 int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_stream_t stream) {

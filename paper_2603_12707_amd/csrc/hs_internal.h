@@ -92,6 +92,9 @@ struct GemmArgs {
 enum { PRO_PLAIN = 0, PRO_NORM = 1, PRO_COMBINE = 2 };
 // most K splits of a residual GEMM over many columns
 constexpr int SPLITK_MAX = 4;
+#ifndef HS_STATIC_SCRATCH_BYTES
+#define HS_STATIC_SCRATCH_BYTES (64ull << 20)
+#endif
 // the attention combine runs in the projection's prologue for at most this
 // many splits (and activations that fit the prologue's LDS copy)
 constexpr int COMBINE_FUSE_SPLITS = 8;
@@ -196,6 +199,8 @@ hipError_t launch_build_order(const int *len, const int *act, int n, int *order,
 hipError_t launch_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int blocks, hipStream_t st);
 // *p = v, in stream order
 hipError_t launch_set_int(int *p, int v, hipStream_t st);
+// zeroes bytes (a multiple of 16, 16-byte aligned) at p, in stream order
+hipError_t launch_zero(void *p, uint64_t bytes, hipStream_t st);
 // act = the ready requests in order (n requests)
 hipError_t launch_build_act(const int *ready, int n, int *act, hipStream_t st);
 // *dst = v, in stream order (the rows of a prefill pass, for the kernels that read them)

@@ -276,6 +276,12 @@ __global__ void k_set_int(int *p, int v) {
   if (threadIdx.x == 0) *p = v;
 }
 
+// zeroes n16 16-byte words (grid-strided vector stores)
+__global__ __launch_bounds__(256) void k_zero(u32x4 *p, int64_t n16) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (int64_t)gridDim.x * 256)
+    p[i] = u32x4{0u, 0u, 0u, 0u};
+}
+
 __global__ __launch_bounds__(256) void k_build_act(const int *ready, int n, int *act) {
   __shared__ int s_tmp[4];
   int base = 0;
@@ -365,6 +371,14 @@ hipError_t launch_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, i
 
 hipError_t launch_set_int(int *p, int v, hipStream_t st) {
   HS_LAUNCH(k_set_int, dim3(1), dim3(64), 0, st, p, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero(void *p, uint64_t bytes, hipStream_t st) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 <= 0) return hipSuccess;
+  const int grid = (int)std::min<int64_t>((n16 + 255) / 256, 1024);
+  HS_LAUNCH(k_zero, dim3(grid), dim3(256), 0, st, (u32x4 *)p, n16);
   return hipGetLastError();
 }
 

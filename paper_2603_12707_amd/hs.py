@@ -23,7 +23,7 @@ EXPORTS = ("hs_last_error", "hs_kv_bytes", "hs_model_create", "hs_model_free", "
            "hs_kv_read", "hs_kv_set_length", "hs_replay_kernels", "hs_packed_bytes", "hs_pack_matrix", "hs_pack_matrix_heads", "hs_kv_sync",
            "hs_prefill_batch", "hs_model_reserve_rows", "hs_kv_pool_create", "hs_kv_admit", "hs_kv_release",
            "hs_kv_pool_blocks", "hs_handoff_create", "hs_handoff_free", "hs_handoff_push", "hs_handoff_pop",
-           "hs_handoff_pending", "hs_stream_read")
+           "hs_handoff_pending", "hs_stream_read", "hs_decode_step_static")
 
 # projection matrices the library reads in its packed layout
 PACKED = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "lm_head")
@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
         "hs_handoff_pending": [P, ctypes.POINTER(I32)],
         "hs_stream_read": [P, U64, P, I32, P],
         "hs_decode_step": [P, P, P, P, P, P, P],
+        "hs_decode_step_static": [P, P, P, P, P, P, P],
         "hs_model_status": [P, ctypes.POINTER(I32)],
         "hs_kv_lengths": [P, P],
         "hs_kv_sync": [P],
@@ -308,6 +309,12 @@ class KVCache:
     def decode(self, tokens_in, tokens_out, logits=None, hidden_out=None, model=None) -> None:
         """One greedy step; `model` (default: the handle's) may be any model of the same configuration."""
         _call("hs_decode_step", (model or self.model).handle, self.handle, _ptr(tokens_in), _ptr(tokens_out),
+              _ptr(logits), _ptr(hidden_out), _stream())
+
+    def decode_static(self, tokens_in, tokens_out, logits=None, hidden_out=None, model=None) -> None:
+        """The same step with its scratch in the library's static device array
+        (hs_decode_step_static: allocates nothing)."""
+        _call("hs_decode_step_static", (model or self.model).handle, self.handle, _ptr(tokens_in), _ptr(tokens_out),
               _ptr(logits), _ptr(hidden_out), _stream())
 
     def sync(self) -> None:
