@@ -6,17 +6,31 @@ A step is one hs_decode_step call: embedding gather, every decoder layer
 projection, RMSNorm + gate/up + SwiGLU, down projection) and the final norm,
 LM head and greedy selection, for every request of the batch.  Inputs are
 seeded synthetic tensors generated directly in HBM; the KV cache is filled by
-hs_prefill_embeddings from the vision rows and text tokens before timing.
+prefill from the vision rows and text tokens (or, for the one-layer workload,
+with synthetic rows) before timing.
+
+The default run measures the headline workload (LLaVA-7B-shaped fp16,
+batch 1) and then, in the same process, the batched LLaVA-shaped, the
+Qwen2.5-VL-shaped and the one-layer batch-256 workloads.  For each it reports
+tokens/s, algorithmic HBM GB/s, the dominant kernel against the HBM roofline,
+the CPU oracle's rate on a bounded sample, and the parity of the GPU with that
+oracle on the same teacher-forced steps.
 
 Prints one JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-workloads]
+    python bench.py --summarise-stats TRACE_DIR BENCH_LOG WORKLOAD "COMMAND"
+    python bench.py --summarise-counters FETCH_DIR WRITE_DIR WORKLOAD KIND "KERNEL" "COMMAND"
 """
 from __future__ import annotations
 
 import argparse
+import csv
 import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -26,6 +40,11 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E
 WEIGHT_COPIES = 4  # one-layer workloads: weight sets rotated over the steps (4 x 0.47 GB > 256 MB Infinity Cache)
 METRIC = "decode tokens/s at batch B + achieved HBM GB/s vs peak, 7B-shaped fp16"
+HEADLINE = "llava7b_b1"
+WORKLOADS = ("llava7b_b32", "qwen7b_b16", "qwen_layer_b256")
+LOGIT_TOL = 2e-2
+# oracle steps per workload (bounded CPU sample, a few seconds per step at 7B size)
+ORACLE_STEPS = {"llava7b_b1": 5, "llava7b_b32": 2, "qwen7b_b16": 2, "qwen_layer_b256": 3}
 
 
 def log(msg: str) -> None:
@@ -115,15 +134,15 @@ def steps_after_context(warmup: int, steps: int) -> int:
     return warmup + steps + 1
 
 
-def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
+def make_weights(cfg: dict):
+    """Weight sets generated and packed in HBM (several copies for a one-layer
+    workload, so that the 256 MB Infinity Cache cannot carry one step's weights
+    into the next)."""
     import torch
 
     import paper_2603_12707_amd as hs
     from workload import synth
-    B = cfg["batch"]
     t = time.time()
-    # a one-layer workload rotates copies of its weights, so that the 256 MB
-    # Infinity Cache cannot serve one step's weights to the next
     copies = WEIGHT_COPIES if "kv_len" in cfg else 1
     ws = []
     for k in range(copies):
@@ -134,14 +153,38 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
             del t_row
         ws.append(w)
     torch.cuda.synchronize()
-    log(f"weights generated and packed in HBM: {copies} x "
+    log(f"{cfg['name']}: weights generated and packed in HBM: {copies} x "
         f"{sum(v.numel() * v.element_size() for v in ws[0].values()) / 1e9:.2f} GB in {time.time() - t:.1f} s")
+    return ws
+
+
+def context_lengths(cfg: dict) -> tuple:
+    from workload import synth
     if "kv_len" in cfg:  # layer stack fed from a synthetic cache
-        lens = synth.kv_lengths(cfg)
-        n_v = [0] * B
-    else:
-        n_v, s_text = synth.request_lengths(cfg)
-        lens = [a + b for a, b in zip(n_v, s_text)]
+        return [0] * cfg["batch"], synth.kv_lengths(cfg)
+    n_v, s_text = synth.request_lengths(cfg)
+    return n_v, [a + b for a, b in zip(n_v, s_text)]
+
+
+def fill_synthetic(cfg: dict, kv, lens: list) -> None:
+    """Every request's cache rows [0, len) from the seeded generator (the rows
+    the oracle leg reads too); RoPE position = length."""
+    from workload import synth
+    for r, n in enumerate(lens):
+        kv.set_length(r, n, n)  # a pool takes the blocks here
+        for layer in range(cfg["n_layers"]):
+            for sel in (0, 1):
+                for h in range(cfg["n_kv_heads"]):
+                    kv.write(r, layer, sel, h, 0, synth.kv_block(cfg, r, layer, sel, h, n, device="cuda"))
+
+
+def setup(cfg: dict, ws: list, n_steps_total: int, pool_block: int = 0):
+    import torch
+
+    import paper_2603_12707_amd as hs
+    from workload import synth
+    B = cfg["batch"]
+    n_v, lens = context_lengths(cfg)
     caps = [n + n_steps_total for n in lens]
     models = [hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True) for w in ws]
     model = models[0]
@@ -154,15 +197,12 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
         kv = hs.KVCache(model, n_v, caps)
     first = torch.empty(B, dtype=torch.int32, device="cuda")
     t = time.time()
+    prefill_ms = None
     if "kv_len" in cfg:
-        for r in range(B):
-            kv.set_length(r, lens[r], lens[r])  # a pool takes the blocks here
-            for layer in range(cfg["n_layers"]):
-                for sel in (0, 1):
-                    for h in range(cfg["n_kv_heads"]):
-                        kv.write(r, layer, sel, h, 0, synth.kv_block(cfg, r, layer, sel, h, lens[r], device="cuda"))
+        fill_synthetic(cfg, kv, lens)
         first.copy_(synth.decode_tokens(cfg, 0, B, device="cuda"))
     else:
+        _, s_text = synth.request_lengths(cfg)
         # inputs first, packed request by request; then the timed prefill
         embs = [synth.vision_rows(cfg, r, n_v[r], device="cuda") for r in range(B) if n_v[r]]
         idss = [synth.text_ids(cfg, r, s_text[r], device="cuda") for r in range(B) if s_text[r]]
@@ -180,9 +220,10 @@ def setup(cfg: dict, n_steps_total: int, pool_block: int = 0):
             kv.prefill_batch(list(range(B)), emb, ids, s_text, pos, first_tokens=first)
     torch.cuda.synchronize()
     ready_s = time.time() - t
-    log(f"context ready for {B} request(s) in {ready_s * 1e3:.1f} ms (lengths {min(lens)}..{max(lens)})")
-    setup.prefill_ms = None if "kv_len" in cfg else ready_s * 1e3 / B
-    return ws, models, kv, first, lens
+    log(f"{cfg['name']}: context ready for {B} request(s) in {ready_s * 1e3:.1f} ms (lengths {min(lens)}..{max(lens)})")
+    if "kv_len" not in cfg:
+        prefill_ms = ready_s * 1e3 / B
+    return models, kv, first, lens, prefill_ms
 
 
 def cpu_model() -> str:
@@ -196,83 +237,42 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(cfg: dict, ctx: int, n_tokens: int = 2) -> dict:
-    """The oracle, single-threaded on one host core, decoding n_tokens for one
-    request of the workload from a synthetic cache of ctx positions.  Its
-    row-major weights come from the same seeded generator (run on the GPU for
-    speed; the generator is bit-identical on CPU and GPU)."""
-    from oracle import oracle as O
-    from workload import synth
-    t = time.time()
-    w_cpu = {n: synth.make_weight(cfg, n, device="cuda").cpu() for n in synth.weight_names(cfg)}
-    model = O.Model(cfg, w_cpu)
-    seq = model.new_seq(ctx + n_tokens)
-    for layer in range(cfg["n_layers"]):
-        for sel in (0, 1):
-            for h in range(cfg["n_kv_heads"]):
-                seq.write_kv(layer, sel, h, 0, synth.kv_block(cfg, 0, layer, sel, h, ctx, device="cuda").float().cpu())
-    seq.set_len(ctx, ctx)
-    log(f"oracle inputs ready in {time.time() - t:.1f} s")
-    tok = int(synth.decode_tokens(cfg, 0, 1)[0])
-    # timed on one host core (the process is pinned to it meanwhile)
-    allowed = os.sched_getaffinity(0)
-    core = min(allowed)
-    os.sched_setaffinity(0, {core})
-    try:
-        t = time.perf_counter()
-        for _ in range(n_tokens):
-            _, _, nxt = seq.decode(tok)
-            tok = nxt if cfg.get("lm_head", True) else tok
-        el = time.perf_counter() - t
-    finally:
-        os.sched_setaffinity(0, allowed)
-    log(f"oracle: {n_tokens} tokens in {el:.1f} s")
-    del w_cpu
-    return {"value": n_tokens / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n_tokens} greedy decode steps of one request of the workload from a synthetic "
-                      f"{ctx}-position KV cache, single-threaded plain C oracle (fp64 accumulation), pinned to one "
-                      f"host core",
-            "cpu_model": cpu_model(), "host_cpus_available": len(allowed), "pinned_core": core}
-
-
-def main() -> int:
-    ap = argparse.ArgumentParser(description=__doc__)
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=DEFAULT_STEPS)
-    ap.add_argument("--warmup", type=int, default=DEFAULT_WARMUP)
-    ap.add_argument("--workload", default="llava7b_b1")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--graph", action="store_true",
-                    help="also time the decode step replayed from a HIP graph (stream capture)")
-    ap.add_argument("--kv-pool-block", type=int, default=0,
-                    help="decode from a block-granular KV pool with blocks of this many positions (0: contiguous)")
-    ap.add_argument("--copy-calibration-mib", type=int, default=0,
-                    help="also run a plain device copy of this many MiB (counter calibration)")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one MI355X: the library has no multi-GPU path (the decode step would be "
-              "sharded by request across GPUs with no exchange). Run with --gpus 1.",
-              file=sys.stderr)
-        return 2
-
+def stream_read_rate() -> float:
+    """The plain streaming-read rate of this GPU (the same 16-byte
+    non-temporal loads as the weight stream), best of three grids."""
     import torch
 
     import paper_2603_12707_amd as hs
-    from workload import configs
-    cfg = configs.get(args.workload)
-    B = cfg["batch"]
-    torch.cuda.set_device(0)
-    copies = WEIGHT_COPIES if "kv_len" in cfg else 1
-    per_graph = max(2, copies)  # decode steps captured in one graph: the token ping-pong and the weight rotation
-    graph_steps = per_graph * (max(1, args.steps // 4) + 1) if args.graph else 0
-    ws, models, kv, first, lens0 = setup(cfg, steps_after_context(args.warmup, args.steps) + graph_steps,
-                                       args.kv_pool_block)
+    buf = torch.empty(STREAM_READ_BYTES, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(max(STREAM_READ_BLOCKS), dtype=torch.int32, device="cuda")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = 0.0
+    for blocks in STREAM_READ_BLOCKS:
+        hs.stream_read(buf, sink, blocks)  # warm
+        ev0.record()
+        for _ in range(5):
+            hs.stream_read(buf, sink, blocks)
+        ev1.record()
+        torch.cuda.synchronize()
+        best = max(best, 5 * STREAM_READ_BYTES / (ev0.elapsed_time(ev1) / 1e3) / 1e9)
+    del buf, sink
+    return best
 
+
+def measure(cfg: dict, ws: list, steps: int, warmup: int, graph: bool = False, pool_block: int = 0,
+            stream_gbs: float = 0.0) -> dict:
+    """Times `steps` decode steps after `warmup`, then the per-kernel breakdown
+    and the dominant kernel replayed back to back."""
+    import torch
+    B = cfg["batch"]
+    copies = len(ws)
+    per_graph = max(2, copies)  # decode steps captured in one graph: the token ping-pong and the weight rotation
+    graph_steps = per_graph * (max(1, steps // 4) + 1) if graph else 0
+    models, kv, first, lens0, prefill_ms = setup(cfg, ws, steps_after_context(warmup, steps) + graph_steps,
+                                                 pool_block)
     tin = first.clone()
     tout = torch.empty_like(tin)
     has_head = cfg.get("lm_head", True)
-
     n_step = 0
 
     def step():
@@ -282,35 +282,34 @@ def main() -> int:
         if has_head:
             tin, tout = tout, tin
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-
     # timed region: K steps bracketed by device synchronisation
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     lens_after = kv.lengths()
 
     graph_ms = None
-    if args.graph:
+    if graph:
         # per_graph steps per graph (token buffers ping-pong, weight sets
         # rotate), graphs replayed back to back
         ga, gb = tin.clone(), torch.empty_like(tin)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
             for k in range(per_graph):
                 a, b = (ga, gb) if k % 2 == 0 else (gb, ga)
                 kv.decode(a, b if has_head else None, model=models[k % len(models)])
         kv.sync()
-        reps_g = max(1, args.steps // 4)
-        graph.replay()  # warm
+        reps_g = max(1, steps // 4)
+        g.replay()  # warm
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(reps_g):
-            graph.replay()
+            g.replay()
         torch.cuda.synchronize()
         graph_ms = (time.perf_counter() - t0) / (per_graph * reps_g) * 1e3
         kv.sync()
@@ -324,7 +323,6 @@ def main() -> int:
             for m in models:
                 kv.replay(kind, cfg["n_layers"], model=m)
     launches = cfg["n_layers"] * len(models)
-
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     breakdown = {}
     for kind in ("qkv", "attn", "combine", "oproj", "gateup", "down", "head"):
@@ -337,7 +335,6 @@ def main() -> int:
         ev1.record()
         torch.cuda.synchronize()
         breakdown[kind] = ev0.elapsed_time(ev1) / launches * 1e3  # us per launch
-
     # dominant kernel: the kind with the most time per step, replayed back
     # to back over every layer's weights (4 passes over each copy)
     per_step = {k: v * (1 if k == "head" else cfg["n_layers"]) for k, v in breakdown.items() if k in KIND_NAMES}
@@ -351,21 +348,366 @@ def main() -> int:
     torch.cuda.synchronize()
     dom_avg_s = ev0.elapsed_time(ev1) / 1e3 / reps
 
-    # the plain streaming-read rate of this GPU (the same loads as the weight
-    # stream), for reading roofline.frac against what HBM delivers
-    sr_buf = torch.empty(STREAM_READ_BYTES, dtype=torch.uint8, device="cuda")
-    sr_sink = torch.empty(max(STREAM_READ_BLOCKS), dtype=torch.int32, device="cuda")
-    stream_read_gbs = 0.0
-    for blocks in STREAM_READ_BLOCKS:  # the best grid
-        hs.stream_read(sr_buf, sr_sink, blocks)  # warm
-        ev0.record()
-        for _ in range(5):
-            hs.stream_read(sr_buf, sr_sink, blocks)
-        ev1.record()
-        torch.cuda.synchronize()
-        stream_read_gbs = max(stream_read_gbs, 5 * STREAM_READ_BYTES / (ev0.elapsed_time(ev1) / 1e3) / 1e9)
-    del sr_buf, sr_sink
+    ms_per_step = elapsed / steps * 1e3
+    lens_start = [n + warmup for n in lens0]
+    total_bytes = sum(step_bytes(cfg, [n + k for n in lens_start]) for k in range(steps))
+    gbs = total_bytes / elapsed / 1e9
+    assert lens_after == [n + steps for n in lens_start], (lens_after[:4], lens_start[:4])
+    dom_bytes = attn_bytes(cfg, lens_replay) if dominant == "attn" else weight_bytes(cfg)[dominant]
+    achieved = dom_bytes / dom_avg_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": stored_traffic(cfg["name"], dominant),
+                "kernel": KIND_NAMES[dominant], "kind": dominant,
+                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps}
+    if stream_gbs:
+        roofline["stream_read_gbps"] = round(stream_gbs, 1)
+        roofline["frac_of_stream_read"] = round(achieved / stream_gbs, 4)
+    out = {
+        "value": round(B * steps / elapsed, 2),
+        "unit": "tokens/s",
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "dtype": cfg["dtype"],
+        "config": {"workload": cfg["name"], "batch": B,
+                   "context_at_start": lens_start[0] if B == 1 else [min(lens_start), max(lens_start)],
+                   "n_layers": cfg["n_layers"], "d_model": cfg["d_model"], "n_heads": cfg["n_heads"],
+                   "n_kv_heads": cfg["n_kv_heads"], "ffn_dim": cfg["ffn_dim"],
+                   "vocab": cfg["vocab"] if has_head else None, "qkv_bias": cfg["qkv_bias"],
+                   "rope": "3-section M-RoPE" if cfg["rope_kind"] == 1 else "1-D RoPE",
+                   "parallelism": "none (one GPU)",
+                   "kv_cache": f"pool of {pool_block}-position blocks" if pool_block else "contiguous",
+                   "weight_copies": copies},
+        "hbm_gbps": round(gbs, 1),
+        "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "bytes_per_step": total_bytes // steps,
+        "roofline": roofline,
+        "kernel_us": {k: round(v, 2) for k, v in breakdown.items()},
+    }
+    if prefill_ms is not None:
+        out["prefill_ms_per_request"] = round(prefill_ms, 2)
+    if graph_ms is not None:
+        out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
+                        "note": "the same step replayed from a HIP graph (stream capture)"}
+    kv.close()
+    for m in models:
+        m.close()
+    return out
 
+
+def oracle_leg(cfg: dict, w: dict, n_steps: int) -> tuple:
+    """The CPU oracle against the GPU on the same teacher-forced steps.
+
+    Every request of the workload gets a synthetic cache of its context
+    length (rows from the seeded generator) on the GPU; request 0 gets the
+    same rows in the oracle.  Step k feeds every request a fixed seeded token.
+    The GPU runs the workload's batch (its launch configuration); the oracle
+    runs request 0 alone (decode rows are independent), single-threaded and
+    pinned to one host core, and is timed: its per-step time, scaled by the
+    batch, is the CPU baseline.  Parity: the largest relative error of
+    request 0's logits (of its residual stream without an LM head) over the
+    steps, and the near ties among its greedy choices."""
+    import numpy as np
+    import torch
+
+    import paper_2603_12707_amd as hs
+    from oracle import oracle as O
+    from workload import synth
+    B = cfg["batch"]
+    has_head = cfg.get("lm_head", True)
+    _, lens = context_lengths(cfg)
+    caps = [n + n_steps + 1 for n in lens]
+    model = hs.Model(cfg, w, max_batch=B, max_ctx=max(caps), packed=True)
+    kv = hs.KVCache(model, [0] * B, caps)
+    t = time.time()
+    fill_synthetic(cfg, kv, lens)
+    toks = [synth.decode_tokens(cfg, 1000 + k, B) for k in range(n_steps)]
+    g_out = []
+    tout = torch.empty(B, dtype=torch.int32, device="cuda")
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device="cuda") if has_head else None
+    hidden = torch.empty(B, cfg["d_model"], dtype=torch.float32, device="cuda")
+    for k in range(n_steps):
+        kv.decode(toks[k].cuda(), tout if has_head else None, logits, hidden)
+        torch.cuda.synchronize()
+        g_out.append((logits[0].cpu().numpy() if has_head else hidden[0].cpu().numpy(), int(tout[0].item())))
+    kv.close()
+    model.close()
+    # the oracle's row-major weights from the same generator (run on the GPU)
+    w_cpu = {n: synth.make_weight(cfg, n, device="cuda").cpu() for n in synth.weight_names(cfg)}
+    seq = O.Model(cfg, w_cpu).new_seq(caps[0])
+    for layer in range(cfg["n_layers"]):
+        for sel in (0, 1):
+            for h in range(cfg["n_kv_heads"]):
+                seq.write_kv(layer, sel, h, 0, synth.kv_block(cfg, 0, layer, sel, h, lens[0], device="cuda").float().cpu())
+    seq.set_len(lens[0], lens[0])
+    log(f"{cfg['name']}: GPU parity steps and oracle inputs ready in {time.time() - t:.1f} s")
+    allowed = os.sched_getaffinity(0)
+    core = min(allowed)
+    os.sched_setaffinity(0, {core})  # timed on one host core
+    try:
+        outs = []
+        t0 = time.perf_counter()
+        for k in range(n_steps):
+            outs.append(seq.decode(int(toks[k][0])))
+        el = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, allowed)
+    del w_cpu
+    worst, ties, mismatches = 0.0, 0, 0
+    for (g, g_tok), (r_log, r_hid, r_tok) in zip(g_out, outs):
+        ref = np.asarray(r_log if has_head else r_hid, np.float64)
+        g = np.asarray(g, np.float64)
+        delta = float(np.max(np.abs(g - ref)))
+        worst = max(worst, delta / max(float(np.max(np.abs(ref))), 1e-30))
+        if has_head and g_tok != r_tok:
+            if float(ref[r_tok] - ref[g_tok]) <= 2 * delta:
+                ties += 1
+            else:
+                mismatches += 1
+    per_step = el / n_steps
+    log(f"{cfg['name']}: oracle {n_steps} steps in {el:.1f} s; parity max rel err {worst:.3g}")
+    sample = (f"{n_steps} teacher-forced decode steps of request 0 from a synthetic {lens[0]}-position cache, "
+              f"single-threaded plain C oracle (fp64 dot products), pinned to one host core"
+              + (f"; rate scaled by the batch of {B} (decode rows are independent)" if B > 1 else ""))
+    base = {"value": B / per_step, "unit": "tokens/s", "cores": 1, "kind": "oracle", "sample": sample,
+            "cpu_model": cpu_model(), "host_cpus_available": len(allowed), "pinned_core": core}
+    parity = {"steps": n_steps, "request": 0, "batch": B, "bound": LOGIT_TOL,
+              ("max_logit_rel_err" if has_head else "max_hidden_rel_err"): round(worst, 6),
+              "near_ties": ties, "token_mismatches": mismatches,
+              "ok": worst <= LOGIT_TOL and mismatches == 0}
+    return base, parity
+
+
+def run_workload(name: str, args, ws_cache: dict, stream_gbs: float, headline: bool) -> dict:
+    import torch
+
+    from workload import configs
+    cfg = configs.get(name)
+    model_key = json.dumps({k: v for k, v in cfg.items() if k not in ("name", "batch", "n_v", "s_text", "n_dec")},
+                           sort_keys=True, default=str)
+    if model_key not in ws_cache:
+        ws_cache.clear()
+        torch.cuda.empty_cache()
+        ws_cache[model_key] = make_weights(cfg)
+    ws = ws_cache[model_key]
+    out = measure(cfg, ws, args.steps, args.warmup, graph=args.graph and headline,
+                  pool_block=args.kv_pool_block if headline else 0, stream_gbs=stream_gbs)
+    log(f"{name}: {out['ms_per_step']:.4f} ms/step, {out['value']:.1f} tokens/s, {out['hbm_frac']:.4f} of HBM peak")
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"], out["parity"] = oracle_leg(cfg, ws[0], ORACLE_STEPS.get(name, 2))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (the files under profiles/)
+# ---------------------------------------------------------------------------
+
+KERNEL_LEGEND = """Template arguments. `k_gemm<dtype, row tiles, column tiles, waves, k-blocks per group, prologue, LDS
+staging, epilogue, packed SwiGLU output, packed activations>` (columns <= 32); `k_gemm_lds<dtype, epilogue, row tiles,
+column tiles>` (LDS-staged, many columns); `k_gemm_ws<dtype, epilogue>` (weight-stationary: gate/up and the LM head at
+129..256 columns); `k_gemm_tile<dtype, row tiles/wave, column tiles/wave, wave rows, wave columns, epilogue>`;
+`k_attn<dtype, head_dim, group, waves, paged cache>` (scalar split attention), `k_attn_mma<...>` (GQA on the matrix
+cores), `k_attn_prefill<...>` (causal prefill); `k_combine<dtype, head_dim, splits unrolled>`. dtype 1 = f16,
+2 = bf16; prologue 0 = plain activations, 1 = RMSNorm, 2 = attention split combine; epilogue 0 = logits,
+1 = residual, 2 = SwiGLU, 3 = q/k/v + RoPE + KV append. `k_splitk_sum` adds the K-split partials of a residual
+GEMM; `k_rmsnorm` normalises rows into a workspace when a GEMM has more columns than its prologue stages."""
+
+
+def _short(name: str) -> str:
+    m = re.search(r"(k_\w+)(<[^>]*>)?", name)
+    return (m.group(1) + (m.group(2) or "")) if m else name[:60]
+
+
+def _csv_rows(d: str, suffix: str) -> list:
+    path = d if d.endswith(".csv") else next(
+        os.path.join(r, f) for r, _, fs in os.walk(d) for f in fs if f.endswith(suffix))
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _steps_summary(trace: list) -> str:
+    """Per-kernel durations inside the decode steps of a kernel trace (a step
+    runs from one k_embed to the next and ends in k_argmax / k_advance)."""
+    rows = sorted((r for r in trace if "hs::" in r["Kernel_Name"]), key=lambda r: int(r["Start_Timestamp"]))
+    steps, cur = [], None
+    for r in rows:
+        k = _short(r["Kernel_Name"]).replace(" ", "")
+        if k.startswith("k_embed"):
+            if cur:
+                steps.append(cur)
+            cur = []
+        if cur is not None:
+            cur.append((k, int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    if cur:
+        steps.append(cur)
+    full = [s for s in steps if any(k.startswith(("k_argmax", "k_advance")) for k, _, _ in s)]
+    inner = full[2:-2] if len(full) > 6 else full
+    if not inner:
+        return "no complete decode step in the trace"
+    dur, gaps, spans = {}, [], []
+    for s in inner:
+        spans.append(s[-1][2] - s[0][1])
+        for i, (k, a, b) in enumerate(s):
+            dur.setdefault(k, []).append(b - a)
+            if i:
+                gaps.append(a - s[i - 1][2])
+    lines = [f"steps {len(inner)} (of {len(full)})  step span median {statistics.median(spans) / 1e3:.1f} us"]
+    tot = 0.0
+    for k, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        per = sum(v) / len(inner)
+        tot += per
+        lines.append(f"{k:48s} n/step {len(v) / len(inner):5.1f}  avg {statistics.mean(v) / 1e3:8.2f} us  "
+                     f"per step {per / 1e3:8.1f} us")
+    lines.append(f"kernel time per step {tot / 1e3:.1f} us; gaps between launches: median "
+                 f"{statistics.median(gaps) / 1e3 if gaps else 0:.2f} us")
+    return "\n".join(lines)
+
+
+def summarise_stats(trace_dir: str, bench_log: str, workload: str, command: str) -> str:
+    """profiles/decode_<workload>_kernel_stats.md from a `rocprofv3 --kernel-trace
+    --stats --output-format csv` run of bench.py and that run's output."""
+    stats = [r for r in _csv_rows(trace_dir, "kernel_stats.csv") if "hs::" in r["Name"]]
+    trace = _csv_rows(trace_dir, "kernel_trace.csv")
+    line = [ln for ln in open(bench_log) if ln.startswith("{")][-1]
+    j = json.loads(line)
+    res = j if j.get("config", {}).get("workload") == workload else j.get("workloads", {}).get(workload, j)
+    tab = "\n".join(f"| `{_short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                    f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |" for r in stats)
+    rl = res["roofline"]
+    md = f"""# Decode, `{workload}` — rocprofv3 kernel statistics
+
+Command (GPU box, repository root), then `python bench.py --summarise-stats` on its output:
+
+```
+{command}
+```
+
+From the run's kernel statistics, libhs kernels only (torch's input-generation kernels omitted). Calls include the
+prefill (or the synthetic KV fill), the warm-up and timed decode steps, bench.py's kernel replays and its parity steps.
+
+{KERNEL_LEGEND}
+
+| Kernel | Calls | Avg µs | Min µs | Max µs |
+|---|---|---|---|---|
+{tab}
+
+Inside the decode steps (from the kernel trace's start/end stamps):
+
+```
+{_steps_summary(trace)}
+```
+
+bench.py measured the dominant kernel ({rl.get('kernel')}) with HIP events at {rl['avg_launch_us']} µs per launch.
+This workload's result from the same run (under the profiler):
+
+```
+{json.dumps({k: res.get(k) for k in ("value", "unit", "ms_per_step", "hbm_gbps", "hbm_frac", "roofline", "kernel_us")})}
+```
+"""
+    path = os.path.join(ROOT, "profiles", f"decode_{workload}_kernel_stats.md")
+    with open(path, "w") as f:
+        f.write(md)
+    return path
+
+
+def summarise_counters(fetch_dir: str, write_dir: str, workload: str, kind: str, kernel: str, command: str) -> str:
+    """profiles/<kind>_<workload>_counters.md from two `rocprofv3 --pmc` runs of
+    bench.py (FETCH_SIZE, then WRITE_SIZE) that also copy 1 GiB device to
+    device: each counter is scaled by what it reads for that copy."""
+    from workload import configs
+    cfg = configs.get(workload)
+
+    def per(d, counter):
+        rs = [r for r in _csv_rows(d, "counter_collection.csv") if r["Counter_Name"] == counter]
+        copy = [float(r["Counter_Value"]) for r in rs if "copyBuffer" in r["Kernel_Name"]]
+        ours = [float(r["Counter_Value"]) for r in rs if kernel.replace(" ", "") in r["Kernel_Name"].replace(" ", "")]
+        return max(copy), ours
+    cf, fk = per(fetch_dir, "FETCH_SIZE")
+    cw, wk = per(write_dir, "WRITE_SIZE")
+    ff, fw = 1048576.0 / cf, 1048576.0 / cw
+    mf, mw = statistics.median(fk), statistics.median(wk)
+    traffic = mf * 1024 * ff + mw * 1024 * fw
+    if kind == "attn":
+        _, lens = context_lengths(cfg)
+        alg = attn_bytes(cfg, [n + DEFAULT_WARMUP for n in lens])
+        alg_note = "K/V rows 0..len of every request at the context of the first replay, q and output rows"
+    else:
+        alg = weight_bytes(cfg)[kind]
+        alg_note = "every weight byte (and gain / bias) once"
+    md = f"""# {KIND_NAMES[kind]}, `{workload}` — HBM traffic counters
+
+kernel: `{kernel}`
+kernel_source_sha256: {kernel_source_hash(kind)}
+
+Commands (GPU box, repository root), one counter per run, then `python bench.py --summarise-counters` on their
+output:
+
+```
+{command}
+```
+
+Calibration: the same runs copy 1 GiB device to device (`--copy-calibration-mib 1024`: one copy dispatch reading
+1,048,576 KiB and writing 1,048,576 KiB); each counter is scaled by known / counted for that copy.
+
+| Counter | 1 GiB copy (KiB) | factor = known / counted | kernel per dispatch (KiB, median of {len(fk)}) | scaled bytes |
+|---|---|---|---|---|
+| FETCH_SIZE | {cf:.2f} | {ff:.5f} | {mf:.1f} | {mf * 1024 * ff:.0f} |
+| WRITE_SIZE | {cw:.1f} | {fw:.5f} | {mw:.1f} | {mw * 1024 * fw:.0f} |
+
+traffic_bytes_per_launch: {traffic:.0f}
+algorithmic_bytes_per_launch: {alg} ({alg_note})
+ratio traffic / algorithmic: {traffic / alg:.4f}
+"""
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}_counters.md")
+    with open(path, "w") as f:
+        f.write(md)
+    return path
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=DEFAULT_STEPS)
+    ap.add_argument("--warmup", type=int, default=DEFAULT_WARMUP)
+    ap.add_argument("--workload", default=HEADLINE, help="the workload of the headline line")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="measure the headline workload only (default: also " + ", ".join(WORKLOADS) + ")")
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle leg (CPU baseline and parity)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the headline step replayed from a HIP graph (stream capture)")
+    ap.add_argument("--kv-pool-block", type=int, default=0,
+                    help="headline decode from a block-granular KV pool with blocks of this many positions")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--summarise-stats", nargs=4, metavar=("TRACE_DIR", "BENCH_LOG", "WORKLOAD", "COMMAND"))
+    ap.add_argument("--summarise-counters", nargs=6,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "WORKLOAD", "KIND", "KERNEL", "COMMAND"))
+    args = ap.parse_args()
+    if args.summarise_stats:
+        print(summarise_stats(*args.summarise_stats))
+        return 0
+    if args.summarise_counters:
+        print(summarise_counters(*args.summarise_counters))
+        return 0
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one MI355X: the library has no multi-GPU path (the decode step would be "
+              "sharded by request across GPUs with no exchange). Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    torch.cuda.set_device(0)
+    stream_gbs = stream_read_rate()
+    log(f"streaming read: {stream_gbs:.0f} GB/s")
+    ws_cache: dict = {}
+    head = run_workload(args.workload, args, ws_cache, stream_gbs, headline=True)
+    extra = {}
+    if not args.no_workloads:
+        for name in WORKLOADS:
+            if name != args.workload:
+                extra[name] = run_workload(name, args, ws_cache, stream_gbs, headline=False)
+    ws_cache.clear()
     if args.copy_calibration_mib:
         src = torch.empty(args.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -373,56 +715,23 @@ def main() -> int:
         torch.cuda.synchronize()
         log(f"copy calibration: {args.copy_calibration_mib} MiB")
 
-    ms_per_step = elapsed / args.steps * 1e3
-    tok_s = B * args.steps / elapsed
-    lens_start = [n + args.warmup for n in lens0]
-    total_bytes = sum(step_bytes(cfg, [n + k for n in lens_start]) for k in range(args.steps))
-    gbs = total_bytes / elapsed / 1e9
-    assert lens_after == [n + args.steps for n in lens_start], (lens_after[:4], lens_start[:4])
-
-    dom_bytes = attn_bytes(cfg, lens_replay) if dominant == "attn" else weight_bytes(cfg)[dominant]
-    achieved = dom_bytes / dom_avg_s / 1e9
-    traffic = stored_traffic(args.workload, dominant)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": KIND_NAMES[dominant], "kind": dominant,
-                "bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": reps,
-                "stream_read_gbps": round(stream_read_gbs, 1), "frac_of_stream_read": round(achieved / stream_read_gbs, 4)}
-    kernels = {k: round(v, 2) for k, v in breakdown.items()}
-
     out = {
         "metric": METRIC,
-        "value": round(tok_s, 2),
+        "value": head["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": cfg["dtype"],
+        "dtype": head["dtype"],
         "data": "synthetic (seeded: N(0,0.02) weights, N(0,1) vision rows, uniform text ids; generated in HBM)",
-        "config": {"workload": args.workload, "batch": B, "context_at_start": lens_start[0] if B == 1 else
-                   [min(lens_start), max(lens_start)], "n_layers": cfg["n_layers"], "d_model": cfg["d_model"],
-                   "n_heads": cfg["n_heads"], "n_kv_heads": cfg["n_kv_heads"], "ffn_dim": cfg["ffn_dim"],
-                   "vocab": cfg["vocab"] if has_head else None, "parallelism": "none (one GPU)",
-                   "kv_cache": f"pool of {args.kv_pool_block}-position blocks" if args.kv_pool_block else "contiguous",
-                   "weight_copies": copies},
-        "hbm_gbps": round(gbs, 1),
-        "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
-        "bytes_per_step": total_bytes // args.steps,
-        "roofline": roofline,
-        "kernel_us": kernels,
     }
-    if getattr(setup, "prefill_ms", None) is not None:
-        out["prefill_ms_per_request"] = round(setup.prefill_ms, 2)
-    if graph_ms is not None:
-        out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
-                        "note": "the same step replayed from a HIP graph (stream capture)"}
-    if not args.no_cpu_baseline:
-        del ws, models
-        out["cpu_baseline"] = cpu_baseline(cfg, lens_start[0])
+    out.update({k: v for k, v in head.items() if k not in out and k not in ("steps", "warmup")})
+    if extra:
+        out["workloads"] = extra
     print(json.dumps(out), flush=True)
     return 0
 
