@@ -237,6 +237,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
   }
 }
 
+// storage-dtype parts the softmax probabilities enter the PV product as
+template <int DT>
+constexpr int P_PARTS = DT == HS_BF16 ? 3 : 2;
+
 // Attention for query-head groups of 4..16 heads on the matrix cores.  One
 // work group = (split, KV head j, query), as above; each wave takes tiles of 16
 // consecutive positions.  Per tile, the scores of the tile's positions for all
@@ -246,12 +250,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs a) {
 // lane % 16 -- exactly the B-operand layout of the 16x16x16 MFMA that updates
 // O^T (d x heads) += V^T P^T, so the online-softmax probabilities feed the
 // matrix cores from registers.  That MFMA takes 16-bit operands, so P enters
-// as the sum of two storage-dtype parts, p = hi + lo (hi = R(p), lo =
-// R(p - hi)), one MFMA each: the products with the stored V values are exact
-// and p is kept to ~16 significant bits, against fp32 in the definition (a
-// single rounding of p to bf16 doubled the error of o and, over 28 layers,
-// the error of the residual stream).  l sums hi + lo, so o stays a weighted
-// mean of the V rows.  For the V^T operand a lane loads
+// as the sum of storage-dtype parts, p = hi + lo (+ lo2) with hi = R(p),
+// lo = R(p - hi), lo2 = R(p - hi - lo), one MFMA each: the products with the
+// stored V values are exact and p keeps ~22 (fp16, two parts) or ~24 (bf16,
+// three parts) significant bits, against fp32 in the definition (a single
+// rounding of p to bf16 doubled the error of o and, over 28 layers, the
+// error of the residual stream; two bf16 parts left the Qwen-shaped logits
+// 1.8 % from the oracle, three 1.2 %).  l sums the parts, so o stays a
+// weighted mean of the V rows.  For the V^T operand a lane loads
 // chunk c = lane % 16 of the 4 positions it covers, and output row c of d-tile
 // dt is element d = 8 c + dt, which a lane gathers from its four chunks.
 // The waves merge through LDS as in k_attn.
@@ -380,15 +386,23 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
       float pr[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) pr[i] = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mn);
-      // the PV operands: p = hi + lo in the storage dtype; l sums hi + lo
-      u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u};
+      // the PV operands: p = hi + lo (+ lo2 in bf16) in the storage dtype;
+      // l sums the parts
+      u32x2 ph = u32x2{0u, 0u}, pl = u32x2{0u, 0u}, pt = u32x2{0u, 0u};
       float ps = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr[i]) : f32_to_bf16(pr[i]);
         const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
         const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr[i] - hf) : f32_to_bf16(pr[i] - hf);
-        ps += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));
+        const float lf = DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb);
+        if constexpr (P_PARTS<DT> == 3) {
+          const uint32_t tb = f32_to_bf16(pr[i] - hf - lf);
+          ps += hf + lf + bf16_to_f32(tb);
+          pt[i >> 1] |= tb << (16 * (i & 1));
+        } else {
+          ps += hf + lf;
+        }
         ph[i >> 1] |= hb << (16 * (i & 1));
         pl[i >> 1] |= lb << (16 * (i & 1));
       }
@@ -406,6 +420,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
         av[1] = ((vc[u][2][w] >> sh) & 0xFFFFu) | (((vc[u][3][w] >> sh) & 0xFFFFu) << 16);
         o[dt] = mma16<DT>(av, ph, o[dt]);
         o[dt] = mma16<DT>(av, pl, o[dt]);
+        if constexpr (P_PARTS<DT> == 3) o[dt] = mma16<DT>(av, pt, o[dt]);
       }
     }
   }
@@ -455,9 +470,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mma(AttnArgs a) {
 // tiles of 16 positions up to the pair's last row between them, each K/V tile
 // loaded once for both query tiles, masking the keys past each row, each wave
 // with an online softmax per query tile; the waves' states merge through LDS
-// at the end.  Operand layouts and the p = hi + lo split are those of
-// k_attn_mma, so the K/V rows a wave loads serve 2 x QPT x G (query, head)
-// pairs at once.
+// at the end.  Operand layouts and the split of p into storage-dtype parts
+// are those of k_attn_mma, so the K/V rows a wave loads serve 2 x QPT x G
+// (query, head) pairs at once.
 // Slack (in units of the natural-log score) by which a column's scores may
 // pass the running maximum before it is raised: exp(s - m) stays below e^8.
 constexpr float RESCALE_SLACK = 8.f;
@@ -567,7 +582,7 @@ __global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
       for (int s = 0; s < QT; ++s)
 #pragma unroll
         for (int u = 0; u < UB; ++u) sc[s][u] = mma<DT>(kc[u][kk], qb[s][kk], sc[s][u]);
-    u32x2 ph[QT][UB], pl[QT][UB];
+    u32x2 ph[QT][UB], pl[QT][UB], pt[QT][UB];
 #pragma unroll
     for (int s = 0; s < QT; ++s) {
       float sv[UB][4];
@@ -598,13 +613,21 @@ __global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
       for (int u = 0; u < UB; ++u) {
         ph[s][u] = u32x2{0u, 0u};
         pl[s][u] = u32x2{0u, 0u};
+        pt[s][u] = u32x2{0u, 0u};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float pr = sv[u][i] == -INFINITY ? 0.f : __expf(sv[u][i] - m[s]);
           const uint32_t hb = DT == HS_F16 ? f32_to_f16(pr) : f32_to_bf16(pr);
           const float hf = DT == HS_F16 ? f16_to_f32(hb) : bf16_to_f32(hb);
           const uint32_t lb = DT == HS_F16 ? f32_to_f16(pr - hf) : f32_to_bf16(pr - hf);
-          l[s] += hf + (DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb));  // this lane's keys only
+          const float lf = DT == HS_F16 ? f16_to_f32(lb) : bf16_to_f32(lb);
+          if constexpr (P_PARTS<DT> == 3) {  // this lane's keys only
+            const uint32_t tb = f32_to_bf16(pr - hf - lf);
+            l[s] += hf + lf + bf16_to_f32(tb);
+            pt[s][u][i >> 1] |= tb << (16 * (i & 1));
+          } else {
+            l[s] += hf + lf;
+          }
           ph[s][u][i >> 1] |= hb << (16 * (i & 1));
           pl[s][u][i >> 1] |= lb << (16 * (i & 1));
         }
@@ -624,6 +647,7 @@ __global__ __launch_bounds__(64 * NW, 2) void k_attn_prefill(AttnArgs a) {
         for (int s = 0; s < QT; ++s) {
           o[s][dt] = mma16<DT>(av, ph[s][u], o[s][dt]);
           o[s][dt] = mma16<DT>(av, pl[s][u], o[s][dt]);
+          if constexpr (P_PARTS<DT> == 3) o[s][dt] = mma16<DT>(av, pt[s][u], o[s][dt]);
         }
       }
   }
