@@ -1,13 +1,15 @@
 #!/usr/bin/env python3
 """Decode-step throughput of the language-decode hot path on one MI355X.
 
-A step is one hs_decode_step call: embedding gather, every decoder layer
+A step is one decode step (hs_decode_step): embedding gather, every decoder layer
 (RMSNorm + q/k/v + RoPE + KV append, split-K attention and combine, output
 projection, RMSNorm + gate/up + SwiGLU, down projection) and the final norm,
 LM head and greedy selection, for every request of the batch.  Inputs are
 seeded synthetic tensors generated directly in HBM; the KV cache is filled by
 prefill from the vision rows and text tokens (or, for the one-layer workload,
-with synthetic rows) before timing.
+with synthetic rows) before timing.  The timed steps are replayed from HIP
+graphs (one captured step per graph, the greedy tokens chaining on the device);
+the same number of direct calls is timed beside them.
 
 The default run measures the headline workload (LLaVA-7B-shaped fp16,
 batch 1) and then, in the same process, the batched LLaVA-shaped, the
@@ -277,62 +279,61 @@ def prewarm(seconds: float = 0.5) -> None:
     del buf, sink
 
 
-def measure(cfg: dict, ws: list, steps: int, warmup: int, graph: bool = False, pool_block: int = 0,
+def measure(cfg: dict, ws: list, steps: int, warmup: int, eager: bool = False, pool_block: int = 0,
             stream_gbs: float = 0.0) -> dict:
     """Times `steps` decode steps after `warmup`, then the per-kernel breakdown
-    and the dominant kernel replayed back to back."""
+    and the dominant kernel replayed back to back.
+
+    The timed steps are replayed from HIP graphs, one captured decode step
+    each (the paper's engine runs its decode iteration from CUDA graphs,
+    §5.4): graph i decodes from token buffer i % 2 into the other (greedy
+    tokens chain from step to step on the device) with weight copy
+    i % copies.  The same number of steps called directly is timed after
+    them and reported beside (`eager`: the other way round)."""
     import torch
     B = cfg["batch"]
     copies = len(ws)
-    per_graph = max(2, copies)  # decode steps captured in one graph: the token ping-pong and the weight rotation
-    graph_steps = per_graph * (max(1, steps // 4) + 1) if graph else 0
-    models, kv, first, lens0, prefill_ms = setup(cfg, ws, steps_after_context(warmup, steps) + graph_steps,
-                                                 pool_block)
-    tin = first.clone()
-    tout = torch.empty_like(tin)
     has_head = cfg.get("lm_head", True)
-    n_step = 0
+    P = copies if copies % 2 == 0 or not has_head else 2 * copies  # graphs: token ping-pong x weight rotation
+    models, kv, first, lens0, prefill_ms = setup(cfg, ws, steps_after_context(warmup, 2 * steps), pool_block)
+    tb = [first.clone(), torch.empty_like(first)]
+    graphs = []
+    for i in range(P):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            kv.decode(tb[i % 2] if has_head else tb[0], tb[(i + 1) % 2] if has_head else None,
+                      model=models[i % copies])
+        graphs.append(g)
+    kv.sync()  # capture launched nothing: the lengths are those after prefill
+    assert kv.lengths() == lens0
 
-    def step():
-        nonlocal tin, tout, n_step
-        kv.decode(tin, tout if has_head else None, model=models[n_step % len(models)])
-        n_step += 1
-        if has_head:
-            tin, tout = tout, tin
+    def replayed(n):
+        graphs[n % P].replay()
 
+    def called(n):
+        kv.decode(tb[n % 2] if has_head else tb[0], tb[(n + 1) % 2] if has_head else None,
+                  model=models[n % copies])
+
+    first_run, second_run = (called, replayed) if eager else (replayed, called)
     prewarm()
-    for _ in range(warmup):
-        step()
+    for n in range(warmup):
+        first_run(n)
     torch.cuda.synchronize()
     # timed region: K steps bracketed by device synchronisation
     t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
+    for n in range(warmup, warmup + steps):
+        first_run(n)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    kv.sync()
     lens_after = kv.lengths()
-
-    graph_ms = None
-    if graph:
-        # per_graph steps per graph (token buffers ping-pong, weight sets
-        # rotate), graphs replayed back to back
-        ga, gb = tin.clone(), torch.empty_like(tin)
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for k in range(per_graph):
-                a, b = (ga, gb) if k % 2 == 0 else (gb, ga)
-                kv.decode(a, b if has_head else None, model=models[k % len(models)])
-        kv.sync()
-        reps_g = max(1, steps // 4)
-        g.replay()  # warm
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(reps_g):
-            g.replay()
-        torch.cuda.synchronize()
-        graph_ms = (time.perf_counter() - t0) / (per_graph * reps_g) * 1e3
-        kv.sync()
-        lens_after = [n - per_graph * (reps_g + 1) for n in kv.lengths()]
+    t0 = time.perf_counter()
+    for n in range(warmup + steps, warmup + 2 * steps):
+        second_run(n)
+    torch.cuda.synchronize()
+    other_ms = (time.perf_counter() - t0) / steps * 1e3
+    kv.sync()
+    del graphs
 
     # per-kernel breakdown, the same way for every replayable kind: each
     # layer's launch replayed once per weight copy, HIP events around the
@@ -372,6 +373,7 @@ def measure(cfg: dict, ws: list, steps: int, warmup: int, graph: bool = False, p
     total_bytes = sum(step_bytes(cfg, [n + k for n in lens_start]) for k in range(steps))
     gbs = total_bytes / elapsed / 1e9
     assert lens_after == [n + steps for n in lens_start], (lens_after[:4], lens_start[:4])
+    assert kv.lengths() == [n + 2 * steps for n in lens_start]
     dom_bytes = attn_bytes(cfg, lens_replay) if dominant == "attn" else weight_bytes(cfg)[dominant]
     achieved = dom_bytes / dom_avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -405,9 +407,11 @@ def measure(cfg: dict, ws: list, steps: int, warmup: int, graph: bool = False, p
     }
     if prefill_ms is not None:
         out["prefill_ms_per_request"] = round(prefill_ms, 2)
-    if graph_ms is not None:
-        out["graph"] = {"ms_per_step": round(graph_ms, 4), "tokens_per_s": round(B / graph_ms * 1e3, 2),
-                        "note": "the same step replayed from a HIP graph (stream capture)"}
+    out["timed_as"] = "direct hs_decode_step calls" if eager else "decode steps replayed from HIP graphs"
+    out["eager" if not eager else "graph"] = {
+        "ms_per_step": round(other_ms, 4), "tokens_per_s": round(B / other_ms * 1e3, 2),
+        "note": ("the same number of steps right after, called directly (hs_decode_step per step)" if not eager
+                 else "the same number of steps right after, replayed from HIP graphs")}
     kv.close()
     for m in models:
         m.close()
@@ -509,9 +513,11 @@ def run_workload(name: str, args, ws_cache: dict, stream_gbs: float, headline: b
         torch.cuda.empty_cache()
         ws_cache[model_key] = make_weights(cfg)
     ws = ws_cache[model_key]
-    out = measure(cfg, ws, args.steps, args.warmup, graph=args.graph and headline,
+    out = measure(cfg, ws, args.steps, args.warmup, eager=args.eager,
                   pool_block=args.kv_pool_block if headline else 0, stream_gbs=stream_gbs)
-    log(f"{name}: {out['ms_per_step']:.4f} ms/step, {out['value']:.1f} tokens/s, {out['hbm_frac']:.4f} of HBM peak")
+    other = out.get("eager") or out.get("graph")
+    log(f"{name}: {out['ms_per_step']:.4f} ms/step ({out['timed_as']}; the other way {other['ms_per_step']:.4f}), "
+        f"{out['value']:.1f} tokens/s, {out['hbm_frac']:.4f} of HBM peak")
     if not args.no_cpu_baseline:
         out["cpu_baseline"], out["parity"] = oracle_leg(cfg, ws[0], ORACLE_STEPS.get(name, 2))
     return out
@@ -602,7 +608,8 @@ Command (GPU box, repository root), then `python bench.py --summarise-stats` on 
 ```
 
 From the run's kernel statistics, libhs kernels only (torch's input-generation kernels omitted). Calls include the
-prefill (or the synthetic KV fill), the warm-up and timed decode steps, bench.py's kernel replays and its parity steps.
+prefill (or the synthetic KV fill), the warm-up and timed decode steps, bench.py's kernel replays and (without
+--no-cpu-baseline) its parity steps.
 
 {KERNEL_LEGEND}
 
@@ -641,11 +648,6 @@ def summarise_counters(fetch_dir: str, write_dir: str, workload: str, kind: str,
         copy = [float(r["Counter_Value"]) for r in rs if "copyBuffer" in r["Kernel_Name"]]
         ours = [float(r["Counter_Value"]) for r in rs if kernel.replace(" ", "") in r["Kernel_Name"].replace(" ", "")]
         return max(copy), ours
-    cf, fk = per(fetch_dir, "FETCH_SIZE")
-    cw, wk = per(write_dir, "WRITE_SIZE")
-    ff, fw = 1048576.0 / cf, 1048576.0 / cw
-    mf, mw = statistics.median(fk), statistics.median(wk)
-    traffic = mf * 1024 * ff + mw * 1024 * fw
     if kind == "attn":
         _, lens = context_lengths(cfg)
         alg = attn_bytes(cfg, [n + DEFAULT_WARMUP for n in lens])
@@ -653,6 +655,18 @@ def summarise_counters(fetch_dir: str, write_dir: str, workload: str, kind: str,
     else:
         alg = weight_bytes(cfg)[kind]
         alg_note = "every weight byte (and gain / bias) once"
+    cf, fk = per(fetch_dir, "FETCH_SIZE")
+    cw, wk = per(write_dir, "WRITE_SIZE")
+    ff, fw = 1048576.0 / cf, 1048576.0 / cw
+    # a kernel that serves two projections (the residual GEMM: O and down) is
+    # told apart by what it fetches: the dispatches within 0.5x..3x of this
+    # kind's algorithmic bytes, and the same dispatches of the WRITE_SIZE run
+    # (the two runs launch the same sequence)
+    pick = [i for i, v in enumerate(fk) if 0.5 <= v * 1024 * ff / alg <= 3.0] or list(range(len(fk)))
+    fk = [fk[i] for i in pick]
+    wk = [wk[i] for i in pick if i < len(wk)]
+    mf, mw = statistics.median(fk), statistics.median(wk)
+    traffic = mf * 1024 * ff + mw * 1024 * fw
     md = f"""# {KIND_NAMES[kind]}, `{workload}` — HBM traffic counters
 
 kernel: `{kernel}`
@@ -692,8 +706,9 @@ def main() -> int:
     ap.add_argument("--no-workloads", action="store_true",
                     help="measure the headline workload only (default: also " + ", ".join(WORKLOADS) + ")")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle leg (CPU baseline and parity)")
-    ap.add_argument("--graph", action="store_true",
-                    help="also time the headline step replayed from a HIP graph (stream capture)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time direct hs_decode_step calls (default: the steps replayed from HIP graphs; the other "
+                         "way is timed beside)")
     ap.add_argument("--kv-pool-block", type=int, default=0,
                     help="headline decode from a block-granular KV pool with blocks of this many positions")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
