@@ -1369,11 +1369,10 @@ hipError_t gemm_launch(const GemmArgs &a, int n_groups, size_t shmem, hipStream_
   return hipGetLastError();
 }
 
-// Launch shape per epilogue.  Work groups of 4 waves for q/k/v, SwiGLU
-// (paired gate/up tiles) and the LM head when the activations are staged in
-// LDS, of 2 when they are read from memory (gemm_global_r), so that the whole
-// grid is resident at once; the residual projections, whose matrices have few
-// row tiles, take 8 waves per tile so that enough loads are in flight.  One k-block per group,
+// Launch shape per epilogue.  Work groups of 4 waves when the activations are
+// staged in LDS (the batch-1 down projection 16.3 against 16.9 µs with 8; the
+// O projection with the split combine keeps 8), of 2-4 when they are read from
+// memory (gemm_global_r).  One k-block per group,
 // two for the LM head at one staged column tile.
 // Columns staged in LDS (few): one row tile per work group (R = 1; SwiGLU 2).
 // Activations read from global memory: every row tile of a work group reuses
@@ -1386,13 +1385,15 @@ hipError_t gemm_global(const GemmArgs &p, int tiles16, hipStream_t st) {
   return gemm_launch<DT, R, NT, NW, 1, PRO_PLAIN, 0, EPI>(p, n_groups, 0, st);
 }
 
-// Waves per work group: 8 for the residual projections; 2 for q/k/v, the LM
-// head and, at one column tile, SwiGLU (batch 16, Qwen-shaped: gate/up 47.3
-// against 49.6 µs with 4 waves, q/k/v 14.2 against 14.9); SwiGLU over two
-// column tiles keeps 4.
+// Waves per work group: 2 for q/k/v, the LM head and, at one column tile,
+// SwiGLU (batch 16, Qwen-shaped: gate/up 47.3 against 49.6 µs with 4 waves,
+// q/k/v 14.2 against 14.9); SwiGLU over two column tiles keeps 4.  The
+// residual projections take 4 at one column tile and 2 at two (batch 16: O 7.8
+// against 8.8 µs with 8, down 27.3 against 27.9; batch 32: down 22.5 against
+// 24.4).
 template <int DT, int EPI, int NT>
 hipError_t gemm_global_r(const GemmArgs &p, int tiles16, hipStream_t st) {
-  constexpr int NW = EPI == EPI_RESID ? 8 : (EPI != EPI_SWIGLU || NT == 1) ? 2 : 4;
+  constexpr int NW = EPI == EPI_RESID ? (NT == 1 ? 4 : 2) : (EPI != EPI_SWIGLU || NT == 1) ? 2 : 4;
   if constexpr (EPI == EPI_SWIGLU) return gemm_global<DT, EPI, 2, NW, NT>(p, tiles16, st);
   else if constexpr (EPI == EPI_RESID) return gemm_global<DT, EPI, 1, NW, NT>(p, tiles16, st);
   else if constexpr (EPI == EPI_STORE) return gemm_global<DT, EPI, 4, NW, NT>(p, tiles16, st);
@@ -1510,7 +1511,7 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   const size_t xs = (size_t)a.ncols * a.K * b;
   if (tiles <= 1 && xs <= XS_MAX_BYTES) {
     constexpr int R = EPI == EPI_SWIGLU ? 2 : 1;
-    constexpr int NW = EPI == EPI_RESID ? 8 : 4;
+    constexpr int NW = 4;
     constexpr int U = EPI == EPI_STORE ? 2 : 1;
     return gemm_launch<DT, R, 1, NW, U, PRO, 1, EPI>(a, tiles16, xs, st);
   }
