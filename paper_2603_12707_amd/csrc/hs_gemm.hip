@@ -1387,13 +1387,14 @@ hipError_t gemm_global(const GemmArgs &p, int tiles16, hipStream_t st) {
 
 // Waves per work group: 2 for q/k/v, the LM head and, at one column tile,
 // SwiGLU (batch 16, Qwen-shaped: gate/up 47.3 against 49.6 µs with 4 waves,
-// q/k/v 14.2 against 14.9); SwiGLU over two column tiles keeps 4.  The
+// q/k/v 14.2 against 14.9); SwiGLU over two column tiles 1 (batch 32,
+// LLaVA-shaped: 38.2 against 39.5 with 4; one wave at one tile: 48.8).  The
 // residual projections take 4 at one column tile and 2 at two (batch 16: O 7.8
 // against 8.8 µs with 8, down 27.3 against 27.9; batch 32: down 22.5 against
 // 24.4).
 template <int DT, int EPI, int NT>
 hipError_t gemm_global_r(const GemmArgs &p, int tiles16, hipStream_t st) {
-  constexpr int NW = EPI == EPI_RESID ? (NT == 1 ? 4 : 2) : (EPI != EPI_SWIGLU || NT == 1) ? 2 : 4;
+  constexpr int NW = EPI == EPI_RESID ? (NT == 1 ? 4 : 2) : EPI != EPI_SWIGLU ? 2 : NT == 1 ? 2 : 1;
   if constexpr (EPI == EPI_SWIGLU) return gemm_global<DT, EPI, 2, NW, NT>(p, tiles16, st);
   else if constexpr (EPI == EPI_RESID) return gemm_global<DT, EPI, 1, NW, NT>(p, tiles16, st);
   else if constexpr (EPI == EPI_STORE) return gemm_global<DT, EPI, 4, NW, NT>(p, tiles16, st);
