@@ -1167,7 +1167,10 @@ __global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int k_spl
 // even split into 4-8 K ranges (O 47-55 us against 33, down 89 against 73):
 // each wave waits for its own weights once per stage, so with few work units
 // the latency of the weight stream is exposed.
-constexpr int WS_RT = 4, WS_CT = 8, WS_NWC = 6, WS_NP = 2, WS_DEPTH = 2, WS_PF = 3, WS_GRID = 256;
+// Five consumers: the Qwen-shaped gate/up at batch 256 is 240 work units on
+// 256 CUs (six made 208 units, leaving 48 CUs idle: 103.7 against 95.5 us).
+// A ring three stages deep spills at two waves per SIMD.
+constexpr int WS_RT = 4, WS_CT = 8, WS_NWC = 5, WS_NP = 2, WS_DEPTH = 2, WS_PF = 3, WS_GRID = 256;
 constexpr int WS_MIN_COLS = 129, WS_MAX_COLS = 256;
 
 // one work-group barrier once this wave's LDS accesses are complete; the
