@@ -161,6 +161,21 @@ def test_packed_activation_layout():
     assert near <= 2
 
 
+@pytest.mark.parametrize("dtype,B,d", [("bf16", 12, 2056), ("f16", 16, 1032), ("f16", 5, 4360)])
+def test_one_column_tile_read_from_memory(dtype, B, d):
+    """5..16 requests whose activations do not fit the LDS copy: every GEMM of
+    the decode step reads one column tile from memory in the packed layout
+    (2-wave q/k/v, SwiGLU and LM head work groups, 4-wave residual ones), after
+    the separate RMSNorm.  d = 2056 and 1032 end in a half row tile and a
+    partial k-block; two layers, GQA-4 with q/k/v bias."""
+    cfg = small_cfg(n_layers=2, d_model=d, n_heads=8, n_kv_heads=2, head_dim=128, ffn_dim=1000, dtype=dtype,
+                    qkv_bias=1)
+    n_v = [(11 * b) % 29 for b in range(B)]
+    s_text = [1 + (3 * b) % 7 for b in range(B)]
+    near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 2
+
+
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 def test_packed_prefill_mha(dtype):
     """Six requests of mixed shapes (no vision rows, no text, one row)
