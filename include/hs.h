@@ -203,9 +203,10 @@ int hs_kv_admit(hs_kv *kv, int32_t slot, int32_t n_v, int32_t capacity, hs_strea
 int hs_kv_release(hs_kv *kv, int32_t slot, hs_stream_t stream);
 /* Measurement: reads `bytes` (a positive multiple of 16) of device memory at
  * buf (16-byte aligned) with the same 16-byte non-temporal loads the kernels
- * stream weights with, writing one word per work group to sink (device,
- * [blocks]) so the reads cannot be skipped.  The plain HBM read rate that the
- * kernels' own rates are compared with. */
+ * stream weights with, each work group 32 KB of consecutive bytes at a time,
+ * writing one word per work group to sink (device, [blocks]) so the reads
+ * cannot be skipped.  The plain HBM read rate that the kernels' own rates are
+ * compared with. */
 int hs_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int32_t blocks, hs_stream_t stream);
 
 /* Aligned batch handoff (§5.2 "Aligned Batch Handoff"): requests whose

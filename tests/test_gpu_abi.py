@@ -241,3 +241,20 @@ def test_generator_is_bit_identical_on_cpu_and_gpu(dtype):
     a = synth.uniform_int(0, "req.1.text", 5000, 0, 152063, "cpu")
     b = synth.uniform_int(0, "req.1.text", 5000, 0, 152063, "cuda").cpu()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("nbytes,blocks", [(5 * 2**20 + 48, 7), (2**20, 64), (16, 3)])
+def test_stream_read_reads_every_word_once(nbytes, blocks):
+    """hs_stream_read folds every 32-bit word of the buffer into the XOR of its
+    work groups' sink words (a word read twice or skipped changes it), for
+    sizes with a partial last 32 KB round and more work groups than rounds."""
+    import paper_2603_12707_amd as hs
+    g = torch.Generator().manual_seed(nbytes)
+    host = torch.randint(0, 2**31 - 1, (nbytes // 4,), dtype=torch.int32, generator=g)
+    buf = host.cuda()
+    sink = torch.zeros(blocks, dtype=torch.int32, device="cuda")
+    hs.stream_read(buf, sink, blocks)
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(host.numpy().view(np.uint32))
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == want
