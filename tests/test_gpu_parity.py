@@ -429,3 +429,45 @@ def test_decode_step_replays_from_a_hip_graph(case):
     for kv, _ in handles:
         kv.close()
     pair.gpu.close()
+
+
+@pytest.mark.parametrize("case", ["b1_splits", "b40"])
+def test_repeat_runs_are_bit_identical(case):
+    """Determinism: the same prefills and decode steps on two fresh caches give
+    bit-identical tokens, logits and K/V rows (no floating-point atomics; every
+    reduction in a fixed order): one request long enough for split attention
+    merged in the O projection's prologue, and 40 requests (K-split LDS GEMMs,
+    split attention and the combine kernel)."""
+    import paper_2603_12707_amd as hs
+    if case == "b1_splits":
+        cfg = small_cfg(dtype="f16")
+        n_v, s_text = [900], [20]
+    else:
+        cfg = small_cfg(dtype="bf16", n_heads=8, n_kv_heads=2, head_dim=64)
+        n_v, s_text = [(37 * b) % 300 for b in range(40)], [1 + (5 * b) % 9 for b in range(40)]
+    B, steps = len(n_v), 3
+    caps = [n + s + steps for n, s in zip(n_v, s_text)]
+    pair = Pair(cfg, max_batch=B, max_ctx=max(caps))
+    runs = []
+    for _ in range(2):
+        kv = hs.KVCache(pair.gpu, n_v, caps)
+        first = torch.empty(B, dtype=torch.int32, device="cuda")
+        for r in range(B):
+            emb, ids, _ = pair.request_inputs(r, n_v[r], s_text[r])
+            kv.prefill(r, emb.cuda() if n_v[r] else None, ids.cuda(), first_token=first[r:r + 1])
+        tin, tout = first.clone(), torch.empty_like(first)
+        lg = torch.empty(B, cfg["vocab"], device="cuda")
+        out = [first.cpu()]
+        for _ in range(steps):
+            kv.decode(tin, tout, lg)
+            out += [tout.cpu().clone(), lg.cpu().clone()]
+            tin, tout = tout, tin
+        n = kv.lengths()[B - 1]
+        rows = torch.empty(n, cfg["head_dim"], dtype=torch.float16 if cfg["dtype"] == "f16" else torch.bfloat16)
+        kv.read(B - 1, cfg["n_layers"] - 1, 1, cfg["n_kv_heads"] - 1, 0, n, rows)
+        out.append(rows)
+        runs.append(out)
+        kv.close()
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+    pair.gpu.close()
