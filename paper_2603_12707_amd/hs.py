@@ -11,7 +11,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libhs.so")
+# HS_LIBRARY names another build of the same library (the host-sanitizer
+# build of the tests); by default the in-tree libhs.so
+LIB_PATH = os.environ.get("HS_LIBRARY") or os.path.join(HERE, "libhs.so")
 
 HS_OK, HS_E_INVALID, HS_E_CAPACITY, HS_E_BUFFER, HS_E_STATE, HS_E_DEVICE = 0, -1, -2, -3, -4, -5
 HS_F32, HS_F16, HS_BF16 = 0, 1, 2
