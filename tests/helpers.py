@@ -17,13 +17,14 @@ from workload import synth
 
 LOGIT_TOL = 2e-2
 # Appended K/V rows (not logits).  At layer 0 a row depends on its input row
-# alone and the two sides round it identically up to one storage rounding.
-# After the last layer a row is a rounded projection of the residual stream,
-# which carries the depth-accumulated error that LOGIT_TOL bounds on the
-# logits; the same max-abs statistic taken over the d_h values of one row,
-# against that row's own maximum, spreads further, hence the factor 1.5.
+# alone and the two sides round it identically up to one storage rounding:
+# each row against its own maximum.  A deeper layer's rows are rounded
+# projections of the residual stream, which carries the depth-accumulated
+# error that LOGIT_TOL bounds on the logits: the K (or V) rows of all KV heads
+# of the position are compared as one vector, with the logits' statistic and
+# bound (max-abs error against the vector's maximum).
 KV_ROW0_TOL = 2.0 ** -8
-KV_ROW_DEEP_TOL = 1.5 * LOGIT_TOL
+KV_ROWS_DEEP_TOL = LOGIT_TOL
 
 
 def small_cfg(**kw) -> dict:
