@@ -13,7 +13,10 @@ vocabulary indices, relative to the oracle's largest |logit|, against the
 2e-2 bound; and the GPU's token must be the oracle's, or else a near tie:
 among the oracle's 8 largest, with an oracle margin no more than twice the
 GPU's largest logit error on that step (several results correct).  Near ties
-are counted and reported with the smallest margin-to-error ratio.
+are counted and reported with the smallest margin-to-error ratio.  The
+batched workloads' stored runs (request 0 alone in the oracle) are replayed
+with request 0 decoding among the whole batch, every request prefilled from
+its real inputs in packed passes, as bench.py runs them.
 """
 from __future__ import annotations
 
@@ -103,3 +106,72 @@ def test_llava7b_b1_free_running_128_steps_token_for_token():
     """The LLaVA-shaped fp16 batch-1 workload: the real 576 + 64-row prefill,
     then all 128 greedy steps."""
     assert len(_free_running("llava7b_b1")) <= 1
+
+
+def _free_running_batch(name):
+    """Request 0 of a batched workload against the oracle's stored run, in
+    bench.py's launch configuration: every request prefilled from its real
+    inputs in packed passes, then the whole batch decodes n_dec steps; request
+    0 is fed the oracle's previous token (its own wherever the two agree), the
+    other requests their own tokens."""
+    with open(os.path.join(GOLDEN, f"greedy_{name}.json")) as f:
+        gold = json.load(f)
+    cfg = configs.get(name)
+    n_v, s_text = synth.request_lengths(cfg)
+    assert gold["seed"] == cfg["seed"] and (gold["n_v"], gold["s_text"]) == (n_v[0], s_text[0])
+    n_dec, B, V = gold["n_dec"], cfg["batch"], cfg["vocab"]
+    tail = max(n_dec, bench.steps_after_context(bench.DEFAULT_WARMUP, bench.DEFAULT_STEPS))
+    models, kv, first, lens, _ = bench.setup(cfg, bench.make_weights(cfg), tail)
+    model = models[0]
+    torch.cuda.synchronize()
+    s0 = gold["steps"][0]
+    tok0 = int(first[0].item())
+    assert tok0 == s0["token"] or (tok0 in dict((i, v) for i, v in s0["top"]) and
+                                   s0["top1"] - dict((i, v) for i, v in s0["top"])[tok0] <= 2 * LOGIT_TOL * s0["max_abs"])
+    idx = torch.tensor(sorted(set(gold["sample_indices"]) | {i for s in gold["steps"] for i, _ in s["top"]}),
+                       dtype=torch.long, device="cuda")
+    pos_of = {int(i): k for k, i in enumerate(idx.tolist())}
+    logits = torch.empty(B, V, dtype=torch.float32, device="cuda")
+    tin, tout = first.clone(), torch.empty_like(first)
+    worst_rel, ties, equal = 0.0, [], int(tok0 == s0["token"])
+    for k in range(1, n_dec + 1):
+        gs = gold["steps"][k]
+        tin[0] = gold["steps"][k - 1]["token"]
+        kv.decode(tin, tout, logits)
+        row = logits[0].index_select(0, idx).cpu().numpy()
+        tok = int(tout[0].item())
+        lg = {i: float(row[pos_of[i]]) for i in pos_of}
+        pairs = list(gs["top"]) + list(zip(gold["sample_indices"], gs["sample"]))
+        err = max(abs(lg[int(i)] - v) for i, v in pairs)
+        rel = err / gs["max_abs"]
+        assert rel <= LOGIT_TOL, (k, rel)
+        worst_rel = max(worst_rel, rel)
+        if tok == gs["token"]:
+            equal += 1
+        else:
+            ref = dict((i, v) for i, v in gs["top"])
+            assert tok in ref and gs["top1"] - ref[tok] <= 2 * err, (k, tok, gs["token"], gs["top1"] - gs["top2"], err)
+            ties.append(k)
+        tin, tout = tout, tin
+    assert kv.lengths()[0] == lens[0] + n_dec
+    assert model.status() == 0
+    kv.close()
+    for m in models:
+        m.close()
+    print(f"\n[greedy {name} request 0 at batch {B}] {equal} of {n_dec + 1} tokens equal, near ties at steps "
+          f"{ties}; max logit rel err {worst_rel:.3g}", flush=True)
+    return ties
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_qwen7b_b16_request0_free_running_256_steps_at_batch_16():
+    """The Qwen-shaped bf16 batch-16 workload (GQA 28/4, 3-section M-RoPE,
+    q/k/v bias): the real 515 + 128-row prefill of request 0 among 16 packed
+    requests, then all 256 greedy steps of the batch.  Every differing token
+    is a near tie by the per-step rule; in bf16 the oracle's top-2 margin is
+    within twice the 2e-2 bound on 141 of the 257 steps, and at most 5 % of
+    the steps may differ (measured: 10, steps 5 ... 253)."""
+    ties = _free_running_batch("qwen7b_b16")
+    assert len(ties) <= 0.05 * 257
+
