@@ -175,3 +175,12 @@ def test_qwen7b_b16_request0_free_running_256_steps_at_batch_16():
     ties = _free_running_batch("qwen7b_b16")
     assert len(ties) <= 0.05 * 257
 
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_llava7b_b32_request0_free_running_128_steps_at_batch_32():
+    """The LLaVA-shaped fp16 batch-32 workload: the real 576 + 223-row
+    prefill of request 0 among 32 packed requests, then all 128 greedy steps
+    of the batch."""
+    ties = _free_running_batch("llava7b_b32")
+    assert len(ties) <= 0.05 * 129
