@@ -534,8 +534,9 @@ column tiles>` (LDS-staged, many columns); `k_gemm_ws<dtype, epilogue>` (weight-
 `k_attn<dtype, head_dim, group, waves, paged cache>` (scalar split attention), `k_attn_mma<...>` (GQA on the matrix
 cores), `k_attn_prefill<...>` (causal prefill); `k_combine<dtype, head_dim, splits unrolled>`. dtype 1 = f16,
 2 = bf16; prologue 0 = plain activations, 1 = RMSNorm, 2 = attention split combine; epilogue 0 = logits,
-1 = residual, 2 = SwiGLU, 3 = q/k/v + RoPE + KV append. `k_splitk_sum` adds the K-split partials of a residual
-GEMM; `k_rmsnorm` normalises rows into a workspace when a GEMM has more columns than its prologue stages."""
+1 = residual, 2 = SwiGLU, 3 = q/k/v + RoPE + KV append, 5 = residual as two fp64 K-split partials. `k_splitk_sum`
+adds the K-split partials of a residual GEMM; `k_rmsnorm<dtype, pending splits>` normalises rows into a workspace
+when a GEMM has more columns than its prologue stages, after adding a deferred residual sum's partials."""
 
 
 def _short(name: str) -> str:

@@ -185,7 +185,21 @@ struct Step {
   hipStream_t st;
   StepWs ws;
 
-  hipError_t qkv(int l) const {
+  // K splits the residual projection over K inputs leaves in ws.splitk for
+  // the next RMSNorm to add (decode at 2..32 columns whose activations are
+  // read from memory; 0: it adds into ws.x itself)
+  int defer(int K) const {
+    const hs_config &c = m->cfg;
+    return prefill ? 0 : resid_defer_splits(c.dtype, ncols, K, c.d_model, ws.splitk_floats);
+  }
+  int o_defer() const {
+    const hs_config &c = m->cfg;
+    return combine_fused() ? 0 : defer(c.n_heads * c.head_dim);
+  }
+  int down_defer() const { return defer(m->cfg.ffn_dim); }
+
+  // pend: splits of partials the previous residual projection left pending
+  hipError_t qkv(int l, int pend) const {
     const hs_config &c = m->cfg;
     const hs_layer_weights &W = m->layers[l];
     GemmArgs g{};
@@ -205,6 +219,8 @@ struct Step {
     g.gain = W.attn_norm;
     g.h_work = ws.hnorm;
     g.eps = c.rms_eps;
+    g.pend = (const double *)ws.splitk;
+    g.pend_s = pend;
     g.out = ws.q;
     g.ld_out = c.n_heads * c.head_dim;
     g.head_dim = c.head_dim;
@@ -273,9 +289,10 @@ struct Step {
     return launch_combine(c.dtype, c.head_dim, ncols, attn_args(l), st);
   }
 
-  hipError_t residual(const void *w, int K, const void *x, int x_packed) const {
+  hipError_t residual(const void *w, int K, const void *x, int x_packed, int defer_s) const {
     const hs_config &c = m->cfg;
     GemmArgs o{};
+    o.defer = defer_s;
     o.w[0] = w;
     o.rows[0] = c.d_model;
     o.K = K;
@@ -292,7 +309,8 @@ struct Step {
   hipError_t oproj(int l) const {
     const hs_config &c = m->cfg;
     const int ko = c.n_heads * c.head_dim;
-    if (!combine_fused()) return residual(m->layers[l].wo, ko, ws.attn, gemm_x_packed(c.dtype, ncols, ko) ? 1 : 0);
+    if (!combine_fused())
+      return residual(m->layers[l].wo, ko, ws.attn, gemm_x_packed(c.dtype, ncols, ko) ? 1 : 0, o_defer());
     GemmArgs o{};
     o.w[0] = m->layers[l].wo;
     o.rows[0] = c.d_model;
@@ -308,7 +326,7 @@ struct Step {
     return launch_gemm(c.dtype, PRO_COMBINE, EPI_RESID, o, st);
   }
 
-  hipError_t gateup(int l) const {
+  hipError_t gateup(int l, int pend) const {
     const hs_config &c = m->cfg;
     const hs_layer_weights &W = m->layers[l];
     GemmArgs u{};
@@ -321,6 +339,8 @@ struct Step {
     u.gain = W.mlp_norm;
     u.h_work = ws.hnorm;
     u.eps = c.rms_eps;
+    u.pend = (const double *)ws.splitk;
+    u.pend_s = pend;
     u.out = ws.act;
     // in the layout the down projection reads
     u.out_packed = gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0;
@@ -330,11 +350,13 @@ struct Step {
 
   hipError_t down(int l) const {
     const hs_config &c = m->cfg;
-    return residual(m->layers[l].w_down, c.ffn_dim, ws.act, gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0);
+    return residual(m->layers[l].w_down, c.ffn_dim, ws.act, gemm_x_packed(c.dtype, ncols, c.ffn_dim) ? 1 : 0,
+                    down_defer());
   }
 
-  // final RMSNorm + LM head over ncols rows starting at x_rows
-  hipError_t head(const float *x_rows, float *logits) const {
+  // final RMSNorm + LM head over ncols rows starting at x_rows (pend: as
+  // for qkv, the rows being ws.x)
+  hipError_t head(const float *x_rows, float *logits, int pend) const {
     const hs_config &c = m->cfg;
     GemmArgs g{};
     g.w[0] = m->w.lm_head;
@@ -345,18 +367,22 @@ struct Step {
     g.gain = m->w.final_norm;
     g.h_work = ws.hnorm;
     g.eps = c.rms_eps;
+    g.pend = (const double *)ws.splitk;
+    g.pend_s = pend;
     g.out = logits;
     g.ld_out = c.vocab;
     return launch_gemm(c.dtype, PRO_NORM, EPI_STORE, g, st);
   }
 
+  // every layer; the last down projection's partials (down_defer()) stay
+  // pending for the caller
   int layers() const {
     for (int l = 0; l < m->cfg.n_layers; ++l) {
-      HIP_TRY(qkv(l));
+      HIP_TRY(qkv(l, l ? down_defer() : 0));
       HIP_TRY(attn(l));
       HIP_TRY(combine(l));
       HIP_TRY(oproj(l));
-      HIP_TRY(gateup(l));
+      HIP_TRY(gateup(l, o_defer()));
       HIP_TRY(down(l));
     }
     return HS_OK;
@@ -474,7 +500,7 @@ int prefill_requests(hs_model *m, hs_kv *kv, int n, const int32_t *reqs, const v
     float *lg = last_logits ? last_logits + (int64_t)i0 * c.vocab : m->logits;
     Step last = pre;
     last.ncols = pk.n;
-    HIP_TRY(last.head(m->xlast, lg));
+    HIP_TRY(last.head(m->xlast, lg, 0));
     HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, pk.n, first_tokens + i0, nullptr, nullptr, nullptr, 0, st));
     for (int k = 0; k < pk.n; ++k)
       HIP_TRY(launch_prefill_finish(kv->d_len, kv->d_rope, kv->d_ready, pk.req[k], pk.cu[k + 1] - pk.cu[k],
@@ -931,15 +957,19 @@ static int decode_impl(hs_model *m, hs_kv *kv, const int32_t *tokens_in, int32_t
   HIP_TRY(launch_embed(c.dtype, m->w.embed, c.vocab, c.d_model, tokens_in, act, B, step.ws.x, m->status, st));
   rc = step.layers();
   if (rc) return rc;
-  if (hidden_out)
-    HIP_TRY(hipMemcpyAsync(hidden_out, step.ws.x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
+  // the last down projection's pending partials: added by the final norm,
+  // else here
+  const int pend = step.down_defer();
   if (m->w.lm_head) {
     float *lg = logits ? logits : step.ws.logits;
-    HIP_TRY(step.head(step.ws.x, lg));
+    HIP_TRY(step.head(step.ws.x, lg, pend));
     HIP_TRY(launch_argmax(lg, c.vocab, c.vocab, B, tokens_out, act, kv->d_len, kv->d_rope, 1, st));
   } else {
+    if (pend) HIP_TRY(launch_resid_pending((const double *)step.ws.splitk, pend, B, c.d_model, step.ws.x, st));
     HIP_TRY(launch_advance(kv->d_len, kv->d_rope, act, B, st));
   }
+  if (hidden_out)
+    HIP_TRY(hipMemcpyAsync(hidden_out, step.ws.x, (size_t)B * c.d_model * 4, hipMemcpyDeviceToDevice, st));
   for (int b : kv->act_host) {
     if (kv->pool) {
       const int k = blocks_for(kv, kv->len[b] + 1) - kv->nblk[b];
@@ -1057,13 +1087,13 @@ int hs_replay_kernels(hs_model *m, hs_kv *kv, int32_t kind, int32_t count, hs_st
     const int l = i % L;
     hipError_t e;
     switch (kind) {
-      case HS_K_QKV: e = step.qkv(l); break;
+      case HS_K_QKV: e = step.qkv(l, l ? step.down_defer() : 0); break;
       case HS_K_ATTN: e = step.attn(l); break;
       case HS_K_COMBINE: e = step.combine(l); break;
       case HS_K_OPROJ: e = step.oproj(l); break;
-      case HS_K_GATEUP: e = step.gateup(l); break;
+      case HS_K_GATEUP: e = step.gateup(l, step.o_defer()); break;
       case HS_K_DOWN: e = step.down(l); break;
-      case HS_K_HEAD: e = step.head(m->x, m->logits); break;
+      case HS_K_HEAD: e = step.head(m->x, m->logits, step.down_defer()); break;
       default: return fail(HS_E_INVALID, "hs_replay_kernels: kind %d cannot be replayed", kind);
     }
     HIP_TRY(e);

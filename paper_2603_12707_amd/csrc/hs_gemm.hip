@@ -342,27 +342,69 @@ __device__ __forceinline__ void gain4(rsrc_t gr, int k, bool ok, float *g) {
 // row's first 4096 elements and their gains are requested together and stay
 // in registers from the sum of squares to the scaling (one memory round trip);
 // a longer row reads the rest twice.
-template <int DT>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gain, float eps, int K, void *h,
-                                                int packed) {
+// PS > 0: the previous residual projection left its PS K-split partials
+// pend[s][row][k] in fp64; x + R32(p_0 + ... + p_{PS-1}) (summed in split
+// order in fp64, rounded once: the rounding of the projection's own residual
+// epilogue) is the residual row, written back to x and normalised.  The
+// longer-row passes recompute it rather than read back what this thread
+// stored.
+template <int DT, int PS>
+__global__ __launch_bounds__(256) void k_rmsnorm(float *x, const void *gain, float eps, int K, void *h, int packed,
+                                                const double *pend, int ncols) {
   constexpr int NV = 4;  // 16-byte chunks per thread held in registers
   constexpr int SB = DT == HS_F32 ? 4 : 2;
-  const float *xr = x + (int64_t)blockIdx.x * K;
+  float *xr = x + (int64_t)blockIdx.x * K;
   const rsrc_t xq = make_rsrc(xr, (uint32_t)K * 4u);
   const rsrc_t gr = make_rsrc(gain, (uint32_t)K * SB);
+  rsrc_t pq[PS > 0 ? PS : 1];
+#pragma unroll
+  for (int s = 0; s < PS; ++s) pq[s] = make_rsrc(pend + ((int64_t)s * ncols + blockIdx.x) * K, (uint32_t)K * 8u);
+  // partials of elements k..k+3: two 16-byte loads per split
+  using P4 = u32x4[2];
+  auto pend4 = [&](int k, bool ok, P4 (&p)[PS > 0 ? PS : 1]) {
+#pragma unroll
+    for (int s = 0; s < PS; ++s)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) p[s][hf] = bld16(pq[s], ok ? (uint32_t)k * 8u + hf * 16u : BUF_OOB);
+  };
+  // the residual row's elements k..k+3 (in range: k < K)
+  auto row4 = [&](f32x4 v, const P4 (&p)[PS > 0 ? PS : 1]) -> f32x4 {
+    if constexpr (PS > 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        double t = 0.0;
+#pragma unroll
+        for (int s = 0; s < PS; ++s) {
+          const uint32_t lo = p[s][e >> 1][2 * (e & 1)], hi = p[s][e >> 1][2 * (e & 1) + 1];
+          const double d = __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+          t = s ? t + d : d;
+        }
+        v[e] += (float)t;
+      }
+    }
+    return v;
+  };
   __shared__ double s_part[4];
   f32x4 xv[NV];
+  P4 pv[NV][PS > 0 ? PS : 1];
   float gv[NV][4];
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
     const int k = (u * 256 + (int)threadIdx.x) * 4;
     xv[u] = __builtin_bit_cast(f32x4, bld16(xq, k < K ? (uint32_t)k * 4u : BUF_OOB));
+    pend4(k, k < K, pv[u]);
     gain4<DT>(gr, k, k < K, gv[u]);
   }
+#pragma unroll
+  for (int u = 0; u < NV; ++u) xv[u] = row4(xv[u], pv[u]);  // zeros past K
   double ss = 0.0;
 #pragma unroll
-  for (int u = 0; u < NV; ++u) ss += sumsq_f64(xv[u]);  // zeros past K
-  for (int k = (NV * 256 + (int)threadIdx.x) * 4; k < K; k += 1024) ss += sumsq_f64(*(const f32x4 *)(xr + k));
+  for (int u = 0; u < NV; ++u) ss += sumsq_f64(xv[u]);
+  for (int k = (NV * 256 + (int)threadIdx.x) * 4; k < K; k += 1024) {
+    P4 p[PS > 0 ? PS : 1];
+    pend4(k, true, p);
+    ss += sumsq_f64(row4(*(const f32x4 *)(xr + k), p));
+  }
   const float rs = (float)(1.0 / sqrt(block_sum<4>(ss, s_part) / (double)K + (double)eps));
   const int nkb = (K / 8 + 15) / 16;
   // (packed: the 4 elements stay consecutive, k being a multiple of 4)
@@ -370,12 +412,19 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gai
 #pragma unroll
   for (int u = 0; u < NV; ++u) {
     const int k = (u * 256 + (int)threadIdx.x) * 4;
-    if (k < K) put_h<DT>((unsigned char *)h, at(k), xv[u], rs, gv[u]);
+    if (k < K) {
+      if constexpr (PS > 0) *(f32x4 *)(xr + k) = xv[u];
+      put_h<DT>((unsigned char *)h, at(k), xv[u], rs, gv[u]);
+    }
   }
   for (int k = (NV * 256 + (int)threadIdx.x) * 4; k < K; k += 1024) {
     float g[4];
     gain4<DT>(gr, k, true, g);
-    put_h<DT>((unsigned char *)h, at(k), *(const f32x4 *)(xr + k), rs, g);
+    P4 p[PS > 0 ? PS : 1];
+    pend4(k, true, p);
+    const f32x4 v = row4(*(const f32x4 *)(xr + k), p);
+    if constexpr (PS > 0) *(f32x4 *)(xr + k) = v;
+    put_h<DT>((unsigned char *)h, at(k), v, rs, g);
   }
 }
 
@@ -395,7 +444,11 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float *x, const void *gai
 // memory (PRO_PLAIN, XS = 0), requested with the weights.  The waves' partial
 // tiles are summed in a fixed order through LDS and handed to the epilogue.
 // PK: the SwiGLU output in the packed layout; XP: activations read from
-// memory in the packed layout (a.out_packed, a.x_packed)
+// memory in the packed layout (a.out_packed, a.x_packed).
+// EPI_PART: work group b takes the k-blocks of split b mod a.k_split (a
+// contiguous range, the splits as equal as whole k-blocks allow) of row
+// group b / a.k_split and stores its tile, summed in fp64, as that split's
+// fp64 partial.
 template <int DT, int R, int NT, int NW, int U, int PRO, int XS, int EPI, bool PK, bool XP>
 __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   static_assert(PRO == PRO_PLAIN || XS == 1, "only plain activations are read from global memory");
@@ -435,6 +488,15 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   const int col0 = cgi * 16 * NT;
   const int K = a.K, kchunks = K / CE, nkb = (kchunks + 15) >> 4;
   const int nst = min(a.ncols - col0, 16 * NT);
+  // the k-blocks [kb_lo, kb_hi) of this work group
+  int sp = 0, kb_lo = 0, kb_hi = nkb;
+  if constexpr (EPI == EPI_PART) {
+    const int ks = a.k_split, per = (nkb + ks - 1) / ks;
+    sp = grp % ks;
+    grp /= ks;
+    kb_lo = min(nkb, sp * per);
+    kb_hi = min(nkb, kb_lo + per);
+  }
 
   int mat[R], row0[R];
   tile_map<EPI, R>(a, grp, mat, row0);
@@ -444,12 +506,12 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   for (int r = 0; r < R; ++r)
     wr[r] = make_rsrc((const S *)a.w[mat[r]] + (int64_t)(row0[r] >> 4) * nkb * 256 * CE,
                       row0[r] < a.rows[mat[r]] ? (uint32_t)nkb * 4096u : 0u);
-  // group g of this wave: k-blocks wave + (g * U + u) * NW
+  // group g of this wave: k-blocks kb_lo + wave + (g * U + u) * NW
   auto load_w = [&](u32x4 (&wv)[U][R][4], int g) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kb = wave + (g * U + u) * NW;
-      const uint32_t off = kb < nkb ? (uint32_t)kb * 4096u + (uint32_t)lane * 16u : BUF_OOB;
+      const int kb = kb_lo + wave + (g * U + u) * NW;
+      const uint32_t off = kb < kb_hi ? (uint32_t)kb * 4096u + (uint32_t)lane * 16u : BUF_OOB;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -595,11 +657,15 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   u32x4 xq[XRING ? D : 1][U][NT][4];
   auto load_xg = [&](u32x4 (&xv)[U][NT][4], int g) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      const int kb = kb_lo + wave + (g * U + u) * NW;
+      // past the split's range: past the data (zeros, like the weights)
+      const int kc0 = EPI != EPI_PART || kb < kb_hi ? kb * 16 : kchunks;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) xv[u][t][s] = load_x(t, (wave + (g * U + u) * NW) * 16 + s * 4 + lq);
+        for (int t = 0; t < NT; ++t) xv[u][t][s] = load_x(t, kc0 + s * 4 + lq);
+    }
   };
   // residual epilogue: the 4 rows of x this thread adds into, read now (no
   // other work group writes them) so the epilogue does not wait for them
@@ -689,7 +755,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   // The MFMAs of one k-group accumulate in fp32 from zero; with ACC64 each
   // group's tile is then added into fp64 accumulators, so that fp32 rounding
   // only ever acts on sums of 4 * U * 32 products (where the registers allow).
-  constexpr bool ACC64 = R * NT <= 2;
+  constexpr bool ACC64 = R * NT <= 2 || EPI == EPI_PART;
   f32x4 acc[R][NT];
   double acc64[ACC64 ? R : 1][ACC64 ? NT : 1][4];
 #pragma unroll
@@ -702,7 +768,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
         for (int e = 0; e < 4; ++e) acc64[r][t][e] = 0.0;
     }
 
-  const int nblk = wave < nkb ? (nkb - 1 - wave) / NW + 1 : 0;  // k-blocks of this wave
+  const int nk = kb_hi - kb_lo;
+  const int nblk = wave < nk ? (nk - 1 - wave) / NW + 1 : 0;  // k-blocks of this wave
   const int ng = (nblk + U - 1) / U;
   for (int g0 = 0; g0 < ng; g0 += D) {
 #pragma unroll
@@ -758,6 +825,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
   for (int item = threadIdx.x; item < NT * 64; item += 64 * NW) {
     const int t = item >> 6, ln = item & 63;
     f32x4 v[R];
+    double vd[EPI == EPI_PART ? R : 1][4];  // EPI_PART: the fp64 sums themselves
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       if constexpr (ACC64) {
@@ -767,6 +835,9 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) sum[e] += s_red64[(((w2 * R + r) * NT + t) * 4 + e) * 64 + ln];
         v[r] = f32x4{(float)sum[0], (float)sum[1], (float)sum[2], (float)sum[3]};
+        if constexpr (EPI == EPI_PART)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vd[r][e] = sum[e];
       } else {
         v[r] = s_red[((0 * R + r) * NT + t) * 64 + ln];
 #pragma unroll
@@ -784,6 +855,17 @@ __global__ __launch_bounds__(64 * NW) void k_gemm(GemmArgs a) {
       }
     } else if constexpr (epi_qkv(EPI)) {
       if (col < a.ncols) qkv_store<DT, R, EPI == EPI_QKV_PAGED>(a, mat, row0, v, col, 4 * (ln >> 4), qin);
+    } else if constexpr (EPI == EPI_PART) {
+      if (col < a.ncols) {
+        double *o = (double *)a.splitk_ws + ((int64_t)sp * a.ncols + col) * a.rows[0];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int row = row0[r] + 4 * (ln >> 4) + e;
+            if (row < a.rows[0]) o[row] = vd[r][e];
+          }
+      }
     } else {
       if (col < a.ncols) gemm_epilogue<DT, EPI, R, PK>(a, mat, row0, v, col, 4 * (ln >> 4));
     }
@@ -1146,6 +1228,17 @@ __global__ __launch_bounds__(256) void k_splitk_sum(const float *part, int k_spl
   *xp += s;
 }
 
+// x[col][row] += R32(the fp64 K-split partials of (col, row) summed in split
+// order), one element per thread: the pending residual sum of a pass that
+// ends without a normalisation
+__global__ __launch_bounds__(256) void k_resid_pending(const double *part, int k_split, int ncols, int rows, float *x) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x, slice = (int64_t)ncols * rows;
+  if (i >= slice) return;
+  double t = part[i];
+  for (int k = 1; k < k_split; ++k) t += part[k * slice + i];
+  x[i] += (float)t;
+}
+
 // ---------------------------------------------------------------------------
 // weight-stationary GEMM for a few hundred columns
 // ---------------------------------------------------------------------------
@@ -1506,6 +1599,25 @@ hipError_t gemm_tiled(const GemmArgs &p, int tiles16, hipStream_t st) {
   else return gemm_tile_launch<DT, 2, 4, 2, 2, EPI>(p, tiles16, st);
 }
 
+// A residual projection that leaves its sum to the next RMSNorm
+// (resid_defer_splits): two row tiles per work group of 2 waves and K split
+// in two, as many work groups as one row tile each over the whole K (the
+// activation chunks a work group loads feed twice the MFMAs).  Batch 16,
+// Qwen-shaped: down 22.8 against 27.0 us, O 6.2 against 7.0; batch 32,
+// LLaVA-shaped: down 18.1 against 21.4, O 8.1 against 9.1 (kernels alone).
+constexpr int DEFER_SPLITS = 2;
+template <int DT>
+hipError_t gemm_defer(const GemmArgs &a, int tiles16, int tiles, hipStream_t st) {
+  if (DT == HS_F32 || !a.x_packed || tiles > 2 || a.defer != DEFER_SPLITS || !a.splitk_ws ||
+      2 * (int64_t)a.defer * a.ncols * a.rows[0] > a.splitk_cap)
+    return hipErrorInvalidValue;
+  GemmArgs g = a;
+  g.k_split = a.defer;
+  const int n_groups = (tiles16 + 1) / 2 * a.defer;
+  if (tiles <= 1) return gemm_launch<DT, 2, 1, 2, 1, PRO_PLAIN, 0, EPI_PART>(g, n_groups, 0, st);
+  return gemm_launch<DT, 2, 2, 2, 1, PRO_PLAIN, 0, EPI_PART>(g, n_groups, 0, st);
+}
+
 template <int DT, int PRO, int EPI>
 hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   // row tiles of 16 (SwiGLU: of one of its two matrices)
@@ -1513,7 +1625,13 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
   const int tiles = (a.ncols + 15) / 16;
   const int b = DT == HS_F32 ? 4 : 2;
   const size_t xs = (size_t)a.ncols * a.K * b;
+  if constexpr (EPI == EPI_RESID && PRO == PRO_PLAIN)
+    if (a.defer) {
+      if constexpr (DT == HS_F32) return hipErrorInvalidValue;
+      else return gemm_defer<DT>(a, tiles16, tiles, st);
+    }
   if (tiles <= 1 && xs <= XS_MAX_BYTES) {
+    if (a.pend_s) return hipErrorInvalidValue;  // pending partials are added by k_rmsnorm alone
     constexpr int R = EPI == EPI_SWIGLU ? 2 : 1;
     constexpr int NW = 4;
     constexpr int U = EPI == EPI_STORE ? 2 : 1;
@@ -1525,8 +1643,15 @@ hipError_t gemm_shape(const GemmArgs &a, hipStream_t st) {
     // them as plain activations (in the packed layout where the GEMM reads
     // them through MFMA-operand loads)
     p.x_packed = gemm_x_packed(DT, a.ncols, a.K) ? 1 : 0;
-    HS_LAUNCH(k_rmsnorm<DT>, dim3(a.ncols), dim3(256), 0, st, (const float *)a.x, a.gain, a.eps, a.K, a.h_work,
-              p.x_packed);
+    float *x = (float *)a.x;  // rewritten with the pending partials added
+    if (a.pend_s == 0)
+      HS_LAUNCH((k_rmsnorm<DT, 0>), dim3(a.ncols), dim3(256), 0, st, x, a.gain, a.eps, a.K, a.h_work, p.x_packed,
+                nullptr, a.ncols);
+    else if (a.pend_s == DEFER_SPLITS && a.pend)
+      HS_LAUNCH((k_rmsnorm<DT, DEFER_SPLITS>), dim3(a.ncols), dim3(256), 0, st, x, a.gain, a.eps, a.K, a.h_work,
+                p.x_packed, a.pend, a.ncols);
+    else
+      return hipErrorInvalidValue;
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     p.x = a.h_work;
@@ -1564,6 +1689,26 @@ bool gemm_x_packed(int dtype, int ncols, int K) {
   if (dtype == HS_F32 || ncols <= 0) return false;
   const int tiles = (ncols + 15) / 16;
   return tiles <= 2 && !(tiles <= 1 && (size_t)ncols * K * 2 <= XS_MAX_BYTES);
+}
+
+int resid_defer_splits(int dtype, int ncols, int K, int d_model, int64_t cap) {
+  // the projection reads its activations from memory (k_gemm over 2..32
+  // columns), the next normalisation runs in k_rmsnorm (its columns do not
+  // fit the prologue's LDS copy), every split holds a k-block, whole float4
+  // rows, and the fp64 partials fit the workspace
+  if (!gemm_x_packed(dtype, ncols, K)) return 0;
+  const int tiles = (ncols + 15) / 16;
+  if (tiles <= 1 && (size_t)ncols * d_model * 2 <= XS_MAX_BYTES) return 0;
+  if ((K / 8 + 15) / 16 < DEFER_SPLITS || d_model % 4) return 0;
+  if (2 * (int64_t)DEFER_SPLITS * ncols * d_model > cap) return 0;
+  return DEFER_SPLITS;
+}
+
+hipError_t launch_resid_pending(const double *part, int k_split, int ncols, int rows, float *x, hipStream_t st) {
+  if (ncols <= 0 || rows <= 0 || k_split <= 0) return hipSuccess;
+  const int64_t n = (int64_t)ncols * rows;
+  HS_LAUNCH(k_resid_pending, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, k_split, ncols, rows, x);
+  return hipGetLastError();
 }
 
 int64_t act_elems(int64_t rows, int64_t K) { return std::max(rows * K, (int64_t)32 * ((K + 127) / 128 * 128)); }

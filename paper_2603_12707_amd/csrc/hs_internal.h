@@ -72,6 +72,15 @@ struct GemmArgs {
   float *splitk_ws;
   int64_t splitk_cap;
   int k_split;  // set by the launcher
+  // residual epilogue left to the next normalisation: the K-split partials
+  // go to splitk_ws as fp64 [defer][ncols][rows[0]] (2 floats of the
+  // workspace each) and resid is not touched
+  int defer;
+  // PRO_NORM: pending fp64 partials of the previous residual projection,
+  // [pend_s][ncols][K], added into the residual rows x (which are rewritten)
+  // before they are normalised
+  const double *pend;
+  int pend_s;
   // q/k/v epilogue: RoPE and KV append
   int head_dim, n_heads, n_kv;
   KvRef kv;
@@ -110,7 +119,8 @@ constexpr bool attn_uses_mma(int dtype, int group) { return dtype != HS_F32 && g
 constexpr int ATTN_MMA_BATCH = 2;
 constexpr int ATTN_MAX_SPLITS = 256;
 // EPI_QKV_PAGED: the q/k/v epilogue for a cache of several blocks per request
-enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_QKV_PAGED = 4 };
+// EPI_PART: the residual epilogue as K-split partials (GemmArgs::defer)
+enum { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3, EPI_QKV_PAGED = 4, EPI_PART = 5 };
 constexpr bool epi_qkv(int e) { return e == EPI_QKV || e == EPI_QKV_PAGED; }
 
 struct AttnArgs {
@@ -138,6 +148,14 @@ hipError_t launch_gemm(int dtype, int pro, int epi, const GemmArgs &a, hipStream
 // from memory through MFMA-operand loads (2..32 columns that the LDS copy
 // cannot hold); its producer then writes them in the packed activation layout
 bool gemm_x_packed(int dtype, int ncols, int K);
+// K splits a residual projection over K inputs leaves pending for the next
+// RMSNorm over d_model (0: it adds into the residual rows itself); cap is
+// the floats of the partials workspace
+int resid_defer_splits(int dtype, int ncols, int K, int d_model, int64_t cap);
+// x[col][0..rows) += the pending fp64 partials [k_split][ncols][rows]
+// summed in split order (the sum k_rmsnorm applies), for a pass that ends
+// without a normalisation
+hipError_t launch_resid_pending(const double *part, int k_split, int ncols, int rows, float *x, hipStream_t st);
 // elements an activation buffer of `rows` rows of K needs, the packed layout
 // of up to 32 columns included
 int64_t act_elems(int64_t rows, int64_t K);

@@ -283,6 +283,64 @@ def test_rows_longer_than_one_pass(B):
     assert near <= 1
 
 
+def test_deferred_residual_sum_rows_longer_than_one_pass():
+    """6 requests at d = 4608 whose O and down projections (3072 inputs each)
+    read their activations from memory: each leaves two fp64 K-split partials
+    that the next RMSNorm adds, in both of its passes (a row's first 4096
+    elements held in registers, the remaining 512 read again); two layers,
+    so the second layer's q/k/v norm takes the first layer's down partials,
+    and the LM head's norm the last ones."""
+    cfg = small_cfg(n_layers=2, d_model=4608, n_heads=24, n_kv_heads=6, head_dim=128, ffn_dim=3072, vocab=512,
+                    dtype="bf16")
+    n_v = [(7 * b) % 13 for b in range(6)]
+    s_text = [2 + b % 3 for b in range(6)]
+    near = _run_pair(cfg, n_v, s_text, 3)
+    assert near <= 1
+
+
+def test_deferred_residual_sum_without_lm_head():
+    """8 requests of a two-layer model without an LM head, whose output is the
+    residual stream after the last layer: at d = 2304 (O over 2304 inputs,
+    down over 2560) both residual projections of each layer leave their sums
+    pending, and the last down projection's is added by the step's own
+    kernel.  Caches of 5..54 positions written alike to both sides, three
+    teacher-forced steps, every request's residual stream against the
+    oracle's."""
+    import paper_2603_12707_amd as hs
+    cfg = small_cfg(n_layers=2, d_model=2304, n_heads=18, n_kv_heads=9, head_dim=128, ffn_dim=2560, dtype="bf16",
+                    qkv_bias=1, lm_head=False)
+    B = 8
+    lens = [5 + 7 * b for b in range(B)]
+    caps = [n + 3 for n in lens]
+    pair = Pair(cfg, max_batch=B, max_ctx=max(caps))
+    kv = hs.KVCache(pair.gpu, [0] * B, caps)
+    seqs = []
+    for r in range(B):
+        kv.set_length(r, lens[r], lens[r])
+        s = pair.ora.new_seq(caps[r])
+        for layer in range(cfg["n_layers"]):
+            for sel in (0, 1):
+                for h in range(cfg["n_kv_heads"]):
+                    rows = synth.kv_block(cfg, r, layer, sel, h, lens[r], device="cuda")
+                    kv.write(r, layer, sel, h, 0, rows)
+                    s.write_kv(layer, sel, h, 0, rows.float().cpu())
+        s.set_len(lens[r], lens[r])
+        seqs.append(s)
+    hidden = torch.empty(B, cfg["d_model"], dtype=torch.float32, device="cuda")
+    for step in range(3):
+        toks = synth.decode_tokens(cfg, step, B).tolist()
+        kv.decode(torch.tensor(toks, dtype=torch.int32, device="cuda"), None, None, hidden)
+        torch.cuda.synchronize()
+        g_hid = hidden.cpu().numpy()
+        for b in range(B):
+            _, r_hid, _ = seqs[b].decode(toks[b])
+            assert rel_err(g_hid[b], r_hid) <= LOGIT_TOL, (step, b, rel_err(g_hid[b], r_hid))
+    assert kv.lengths() == [n + 3 for n in lens]
+    assert pair.gpu.status() == 0
+    kv.close()
+    pair.gpu.close()
+
+
 @pytest.mark.parametrize("n_v,dtype", [(1100, "f16"), (2400, "f16"), (2400, "f32")])
 def test_long_context_many_splits(n_v, dtype):
     """Contexts long enough for many attention splits in decode: at most 8
