@@ -298,17 +298,21 @@ def test_deferred_residual_sum_rows_longer_than_one_pass():
     assert near <= 1
 
 
-def test_deferred_residual_sum_without_lm_head():
+@pytest.mark.parametrize("n_heads,ffn_dim", [(18, 2560), (16, 2560), (18, 1536)])
+def test_deferred_residual_sum_without_lm_head(n_heads, ffn_dim):
     """8 requests of a two-layer model without an LM head, whose output is the
-    residual stream after the last layer: at d = 2304 (O over 2304 inputs,
-    down over 2560) both residual projections of each layer leave their sums
-    pending, and the last down projection's is added by the step's own
+    residual stream after the last layer, at d = 2304.  A residual projection
+    leaves its sum pending when its activations do not fit the LDS copy
+    (8 x K x 2 bytes > 32 KB): O over 2304 inputs and down over 2560 both do;
+    O over 2048 inputs (16 heads) adds its sum itself while down defers; down
+    over 1536 adds its own while O defers.  Each pending sum goes to the next
+    norm, and the last down projection's, when pending, to the step's own
     kernel.  Caches of 5..54 positions written alike to both sides, three
     teacher-forced steps, every request's residual stream against the
     oracle's."""
     import paper_2603_12707_amd as hs
-    cfg = small_cfg(n_layers=2, d_model=2304, n_heads=18, n_kv_heads=9, head_dim=128, ffn_dim=2560, dtype="bf16",
-                    qkv_bias=1, lm_head=False)
+    cfg = small_cfg(n_layers=2, d_model=2304, n_heads=n_heads, n_kv_heads=n_heads // 2, head_dim=128,
+                    ffn_dim=ffn_dim, dtype="bf16", qkv_bias=1, lm_head=False)
     B = 8
     lens = [5 + 7 * b for b in range(B)]
     caps = [n + 3 for n in lens]
