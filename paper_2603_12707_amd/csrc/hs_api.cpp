@@ -186,8 +186,9 @@ struct Step {
   StepWs ws;
 
   // K splits the residual projection over K inputs leaves in ws.splitk for
-  // the next RMSNorm to add (decode at 2..32 columns whose activations are
-  // read from memory; 0: it adds into ws.x itself)
+  // the next RMSNorm to add: in decode, when the projection reads its
+  // activations from memory and that norm runs in its own kernel (0: it adds
+  // into ws.x itself)
   int defer(int K) const {
     const hs_config &c = m->cfg;
     return prefill ? 0 : resid_defer_splits(c.dtype, ncols, K, c.d_model, ws.splitk_floats);
