@@ -233,9 +233,10 @@ def test_packed_prefill_more_requests_than_a_pass():
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_many_columns_split_k(dtype):
     """40 requests (three column tiles) and a long, ragged down projection
-    (K = 2040): the residual GEMM splits K four ways into fp32 partials and
-    sums them into the residual stream."""
-    cfg = small_cfg(n_layers=1, ffn_dim=2040, dtype=dtype)
+    (K = 2040), two layers: the residual GEMM splits K four ways into fp32
+    partials and sums them into the residual stream that the second layer
+    and the LM head read."""
+    cfg = small_cfg(n_layers=2, ffn_dim=2040, dtype=dtype)
     n_v = [(11 * b) % 29 for b in range(40)]
     s_text = [1 + (3 * b) % 7 for b in range(40)]
     near = _run_pair(cfg, n_v, s_text, 2)
